@@ -1,0 +1,271 @@
+/*
+ * laep_moe.h -- C ABI of one mixture-of-experts layer on one MI355X (gfx950),
+ * the data-parallel hot path that Layer-Adaptive Expert Pruning (LAEP) acts on.
+ *
+ * The paper (arXiv 2601.14327) states the problem in these terms
+ * (Section 3.2): E[i, j, l] = 1 iff token j of layer l is routed to expert i;
+ * the load of expert i is sum_j E[i, j, l]; experts are pruned by an
+ * individual-load threshold alpha (Eq. (1)) and a cumulative-load threshold
+ * beta (Eq. (2)), as carried out by Algorithm 1 (Appendix); surviving
+ * experts are placed on devices by Algorithm 2 (Section 3.3, Appendix).
+ * The router, the gating function and the expert FFN are not spelled out in
+ * the paper; this library implements a linear router, top-k softmax gating
+ * and a SwiGLU expert FFN (three d x f matrices per expert, as the paper's
+ * parameter counts imply).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Pointers marked "device" are HIP device (HBM) addresses; "host" ones are
+ *    ordinary CPU memory.  The caller owns and allocates every buffer; the
+ *    library allocates no device memory.  Scratch memory comes in through
+ *    `ws` / `ws_bytes`, sized by moe_workspace_bytes().
+ *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.
+ *    Every device call only enqueues work on `stream`: no host/device copy,
+ *    no synchronisation.  Inputs must stay valid until that work completes.
+ *  - `dtype` is LAEP_F32 or LAEP_BF16 and applies to activations and expert
+ *    weights (x, w_router, w_gate_up, w_down, x_perm, y_perm, act_save, out
+ *    and their gradients).  Router logits, gates, gate gradients and weight
+ *    gradients are always float32.  Layouts are row-major; weight matrices
+ *    are stored [out_features, in_features] (w_gate_up[e] stacks the gate
+ *    rows [0, d_ff) over the up rows [d_ff, 2*d_ff)).
+ *  - Activation and weight pointers must be 16-byte aligned.
+ *  - Return value: LAEP_OK or an error code.  Arguments are validated on the
+ *    host before any HIP call; an invalid call enqueues nothing.  The message
+ *    of the last error of the calling thread is laep_last_error().
+ *    A fault inside a kernel surfaces at the caller's next synchronisation.
+ *  - Results are deterministic: identical inputs give identical bits (no
+ *    floating-point atomics anywhere).
+ *  - Calls are thread-safe; the only library state is the per-thread error
+ *    message.
+ */
+#ifndef LAEP_MOE_H
+#define LAEP_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* dtypes */
+#define LAEP_F32 0
+#define LAEP_BF16 1
+
+/* return codes */
+#define LAEP_OK 0
+#define LAEP_ERR_INVALID_ARG 1 /* null pointer, bad size, misaligned pointer */
+#define LAEP_ERR_UNSUPPORTED 2 /* dtype or shape this build does not handle  */
+#define LAEP_ERR_WORKSPACE 3   /* ws_bytes smaller than moe_workspace_bytes() */
+#define LAEP_ERR_HIP 4         /* a HIP launch reported an error              */
+#define LAEP_ERR_INFEASIBLE 5  /* the request cannot be met (e.g. capacity)   */
+
+/* `which_call` of moe_workspace_bytes() */
+#define LAEP_CALL_ROUTE 0
+#define LAEP_CALL_COUNTS 1
+#define LAEP_CALL_FFN_FWD 2
+#define LAEP_CALL_FFN_BWD 3
+
+/* Limits of this build. */
+#define LAEP_MAX_EXPERTS 256
+
+/*
+ * moe_route -- router scoring and top-k gating (produces E[i, j, l] of
+ * Section 3.2 in compact form: the k expert ids of each token).
+ *
+ *   logits[t, e] = sum_c x[t, c] * w_router[e, c] (+ bias[e])   (fp32 accumulation)
+ *   dead experts (alive[e] == 0) are excluded;
+ *   topk_idx[t, 0..k-1] = the k largest logits, descending, ties to the
+ *                         lower expert index;
+ *   topk_gate[t, j] = renorm ? softmax over the k selected logits
+ *                            : softmax over all alive experts, at the k selected.
+ *
+ *   x        device [T, d_model] dtype        w_router device [E, d_model] dtype
+ *   bias     device [E] fp32 or NULL          alive    device [E] uint8 or NULL (all alive)
+ *   logits   device [T, E] fp32 or NULL (written when non-NULL; dead experts -inf)
+ *   topk_idx device [T, k] int32              topk_gate device [T, k] fp32
+ *   Constraints: 1 <= E <= 256, 1 <= k <= E, d_model % 8 == 0, T >= 0.
+ *   If fewer than k experts are alive, every alive expert is selected and the
+ *   remaining slots get topk_idx = -1 and topk_gate = 0 (such slots are not
+ *   routed by the calls below).
+ *   Workspace: none (ws may be NULL).
+ */
+int moe_route(const void* x, const void* w_router, const float* bias,
+              const uint8_t* alive, int dtype, int T, int d_model, int E, int k,
+              int renorm, float* logits, int32_t* topk_idx, float* topk_gate,
+              void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * moe_expert_counts -- per-expert token load (the left-hand side of Eq. (1);
+ * ETN of Algorithm 1, Step 1, for one iteration and one layer), the expert
+ * offsets and the stable dispatch permutation.
+ *
+ *   counts[e]   = #{(t, j) : topk_idx[t, j] == e}
+ *   offsets     = exclusive prefix sum of counts, offsets[E] = routed rows
+ *   dest_row[t*k + j] = offsets[e] + #{(t', j') : topk_idx[t', j'] == e, t' < t}
+ *                 (rows grouped by expert, ordered by token); -1 for slots
+ *                 with topk_idx == -1
+ *   row_src[dest_row[s]] = s   (inverse map; optional)
+ *   etn_accum[e] += counts[e]  (optional int64 running ETN row)
+ *
+ *   topk_idx device [T, k] int32, values in [0, E) or -1
+ *   counts device [E] int32, offsets device [E + 1] int32,
+ *   dest_row device [T * k] int32, row_src device [T * k] int32 or NULL,
+ *   etn_accum device [E] int64 or NULL.
+ *   Workspace: moe_workspace_bytes(LAEP_CALL_COUNTS, T, k, E, 0, 0).
+ */
+int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E,
+                      int32_t* counts, int32_t* offsets, int32_t* dest_row,
+                      int32_t* row_src, int64_t* etn_accum, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/*
+ * laep_prune_mask -- the LAEP prune decision for one layer and one counted
+ * batch (Section 3.2, Eqs. (1) and (2); Algorithm 1, Step 2 with ITER = 1).
+ *
+ *   Experts are ranked by (counts[e], e) ascending.  Walking that order with
+ *   an inclusive running sum, an expert is pruned iff
+ *       (double)running < (double)total * beta                    (Eq. (2))
+ *   and (double)count   < ((double)total * alpha) / (double)E     (Eq. (1))
+ *   (strict comparisons, as in Algorithm 1; alpha = INFINITY disables Eq. (1)).
+ *   The pruned set is a prefix of that ranking.
+ *
+ *   counts device [E] int32 (>= 0); total = S * topK (tokens times k);
+ *   alive device [E] uint8 (out: 1 = kept, 0 = pruned);
+ *   n_pruned device int32 (out).
+ *   The rule has no lower bound: it may prune below k survivors.
+ */
+int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha,
+                    double beta, uint8_t* alive, int32_t* n_pruned,
+                    void* stream);
+
+/*
+ * moe_permute -- dispatch: x_perm[dest_row[t*k + j]] = x[t] (a copy; slots
+ * with dest_row == -1 are skipped).
+ *   x device [T, d_model] dtype; dest_row device [T * k] int32;
+ *   x_perm device [rows, d_model] dtype, rows = number of routed slots.
+ *   d_model % 8 == 0.
+ */
+int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T,
+                int k, int d_model, void* x_perm, void* stream);
+
+/*
+ * moe_grouped_ffn_fwd -- SwiGLU expert FFN over the routed rows, as one
+ * grouped GEMM pass over the experts that have rows (pruned experts have
+ * none and cost nothing).
+ *
+ *   for each expert e with rows [offsets[e], offsets[e+1]) and weight slot
+ *   p = expert_map ? expert_map[e] : e:
+ *     A = X_e W_gu[p]^T                         (fp32 accumulation, [M_e, 2*d_ff])
+ *     act_save = A rounded to dtype             (optional, for the backward)
+ *     H = round(silu(A[:, :d_ff]) * A[:, d_ff:])
+ *     Y_e = round(H W_d[p]^T)                   -> y_perm rows of expert e
+ *
+ *   x_perm device [R, d_model]; w_gate_up device [E_phys, 2*d_ff, d_model];
+ *   w_down device [E_phys, d_model, d_ff]; offsets device [E + 1] int32
+ *   (offsets[E] <= R); expert_map device [E] int32 or NULL (identity), -1 =
+ *   pruned (such experts must have no rows; the map must not repeat a slot);
+ *   y_perm device [R, d_model]; act_save device [R, 2*d_ff] or NULL.
+ *   Constraints: d_model % 64 == 0, d_ff % 64 == 0, R < 2^31.
+ *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff)
+ *   (holds H and the tile table).
+ */
+int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
+                        const void* w_down, const int32_t* offsets,
+                        const int32_t* expert_map, int dtype, int E,
+                        int d_model, int d_ff, int64_t R, void* y_perm,
+                        void* act_save, void* ws, size_t ws_bytes,
+                        void* stream);
+
+/*
+ * moe_grouped_ffn_bwd -- backward of moe_grouped_ffn_fwd (data and weight
+ * gradients), evaluated at the saved pre-activations act_save (Â):
+ *
+ *   dH   = dY W_d[p]
+ *   dA_g = dH * Â_u * s * (1 + Â_g (1 - s)),  s = sigmoid(Â_g)
+ *   dA_u = dH * silu(Â_g)                      dA = round([dA_g, dA_u])
+ *   H_b  = round(silu(Â_g) * Â_u)
+ *   dX   = round(dA W_gu[p])                   -> dx_perm
+ *   dW_gu[p] (+)= dA^T X,   dW_d[p] (+)= dY^T H_b   (fp32; `accumulate` adds)
+ *   Slots p of experts without rows get zero gradient (or keep their value
+ *   when accumulating).
+ *
+ *   dy_perm, x_perm device [R, d_model]; act_save device [R, 2*d_ff];
+ *   dx_perm device [R, d_model]; dw_gate_up device fp32 [E_phys, 2*d_ff, d_model];
+ *   dw_down device fp32 [E_phys, d_model, d_ff].
+ *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d_model, d_ff).
+ *   On return the workspace holds dA [R, 2*d_ff] (dtype) at byte offset 0 and
+ *   H_b [R, d_ff] (dtype) at byte offset laep_ws_hb_offset(R, d_ff, dtype).
+ *   Only LAEP_BF16 is supported.
+ */
+int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
+                        const void* act_save, const void* w_gate_up,
+                        const void* w_down, const int32_t* offsets,
+                        const int32_t* expert_map, int dtype, int E,
+                        int d_model, int d_ff, int64_t R, void* dx_perm,
+                        float* dw_gate_up, float* dw_down, int accumulate,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Byte offset of H_b inside the moe_grouped_ffn_bwd workspace. */
+size_t laep_ws_hb_offset(int64_t R, int d_ff, int dtype);
+
+/*
+ * moe_combine -- gate-weighted combine (return path of the dispatch):
+ *   out[t] = round(sum_j topk_gate[t, j] * y_perm[dest_row[t*k + j]])
+ *   (fp32 accumulation in slot order; slots with dest_row == -1 skipped).
+ *   y_perm device [rows, d_model]; topk_gate device [T, k] fp32;
+ *   dest_row device [T * k] int32; out device [T, d_model].
+ */
+int moe_combine(const void* y_perm, const float* topk_gate,
+                const int32_t* dest_row, int T, int k, int d_model, int dtype,
+                void* out, void* stream);
+
+/*
+ * moe_combine_bwd -- backward of moe_combine:
+ *   dgate[t, j]  = <dout[t], y_perm[row]>          (fp32 accumulation)
+ *   dy_perm[row] = round(topk_gate[t, j] * dout[t]),  row = dest_row[t*k + j]
+ *   dout device [T, d_model]; dy_perm device [rows, d_model]; dgate device [T, k] fp32
+ *   (0 for unrouted slots).
+ */
+int moe_combine_bwd(const void* dout, const void* y_perm,
+                    const float* topk_gate, const int32_t* dest_row, int T,
+                    int k, int d_model, int dtype, void* dy_perm, float* dgate,
+                    void* stream);
+
+/*
+ * moe_permute_bwd -- backward of moe_permute:
+ *   dx[t] = round(sum_j dx_perm[dest_row[t*k + j]])   (fp32 accumulation)
+ */
+int moe_permute_bwd(const void* dx_perm, const int32_t* dest_row, int T, int k,
+                    int d_model, int dtype, void* dx, void* stream);
+
+/* Workspace bytes a call needs (0 if none).  For the FFN calls pass T = R
+ * (routed rows) and k = 1; the LAEP_CALL_FFN_FWD size covers both dtypes. */
+size_t moe_workspace_bytes(int which_call, int T, int k, int E, int d_model,
+                           int d_ff);
+
+/*
+ * laep_rearrange -- host utility: greedy placement of n experts into
+ * n_groups device groups that balances their loads (Section 3.3;
+ * Algorithm 2).  Experts are visited in descending load order (equal loads
+ * by index) and each goes to the group with the smallest running sum that
+ * still has room (ties to the lower group index).  Capacity per group is
+ * ceil(n / n_groups) (the printed floor cannot place every expert when
+ * n_groups does not divide n).
+ *
+ *   loads host [n]; group_of host [n] (out: group of each expert);
+ *   order host [n] (out: the flattened group lists, In_flat);
+ *   group_sums host [n_groups] (out: sum of loads per group).
+ *   Returns LAEP_ERR_INVALID_ARG for n < 0, n_groups < 1 or null pointers.
+ */
+int laep_rearrange(const double* loads, int n, int n_groups, int32_t* group_of,
+                   int32_t* order, double* group_sums);
+
+/* Message of the calling thread's last error ("" if none). */
+const char* laep_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAEP_MOE_H */

@@ -1,0 +1,30 @@
+"""LAEP MoE layer on MI355X: Python binding of the liblaep_moe C ABI.
+
+Steps of one MoE layer (the data-parallel hot path that Layer-Adaptive
+Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
+
+    moe_route            router scoring + top-k gating
+    moe_expert_counts    per-expert token loads (ETN), offsets, dispatch rows
+    laep_prune_mask      LAEP prune decision (alpha / beta thresholds)
+    moe_permute          dispatch of token rows to expert order
+    moe_grouped_ffn_fwd  grouped SwiGLU expert FFN (bf16 MFMA)
+    moe_combine          gate-weighted combine
+    moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
+    laep_rearrange       host utility: balanced expert placement
+"""
+from ._lib import LAEP_BF16, LAEP_F32, LaepError, LIB_PATH, lib  # noqa: F401
+from .api import (  # noqa: F401
+    ffn_bwd_ws_views,
+    laep_prune_mask,
+    laep_rearrange,
+    moe_combine,
+    moe_combine_bwd,
+    moe_expert_counts,
+    moe_grouped_ffn_bwd,
+    moe_grouped_ffn_fwd,
+    moe_permute,
+    moe_permute_bwd,
+    moe_route,
+    workspace_bytes,
+)
+from .layer import MoELayerPlan, layer_forward  # noqa: F401

@@ -1,0 +1,232 @@
+"""Python binding of the LAEP MoE C ABI on torch tensors.
+
+Argument marshalling only: each function checks tensor placement and
+layout, allocates missing outputs with torch (device memory is PyTorch's
+job), and calls the same-named C entry point on the current HIP stream.
+Every step of the layer runs in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Tuple
+
+import torch
+
+from ._lib import (LAEP_BF16, LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD,
+                   LAEP_F32, LaepError, check, lib)
+
+_DT = {torch.float32: LAEP_F32, torch.bfloat16: LAEP_BF16}
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype not in _DT:
+        raise LaepError(2, f"unsupported dtype {t.dtype}")
+    return _DT[t.dtype]
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def workspace_bytes(which: int, T: int, k: int, E: int, d_model: int = 0, d_ff: int = 0) -> int:
+    return int(lib().moe_workspace_bytes(which, T, k, E, d_model, d_ff))
+
+
+def _workspace(ws, nbytes, device):
+    if ws is None:
+        return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+    if ws.numel() * ws.element_size() < nbytes:
+        raise LaepError(3, f"workspace {ws.numel() * ws.element_size()} < {nbytes} bytes")
+    return ws
+
+
+# ---------------------------------------------------------------------------
+def moe_route(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=None, alive=None,
+              renorm: bool = True, want_logits: bool = False, topk_idx=None, topk_gate=None):
+    """Router scoring + top-k gating.  Returns (topk_idx, topk_gate[, logits])."""
+    _dev(x, "x"), _dev(w_router, "w_router")
+    T, d = x.shape
+    E = w_router.shape[0]
+    dev = x.device
+    if topk_idx is None:
+        topk_idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    if topk_gate is None:
+        topk_gate = torch.empty((T, k), dtype=torch.float32, device=dev)
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev) if want_logits else None
+    if bias is not None:
+        _dev(bias, "bias")
+    if alive is not None:
+        _dev(alive, "alive")
+    check(lib().moe_route(_ptr(x), _ptr(w_router), _ptr(bias), _ptr(alive), _dtype_code(x), T, d,
+                          E, k, int(renorm), _ptr(logits), _ptr(topk_idx), _ptr(topk_gate), None,
+                          0, _stream(dev)))
+    return (topk_idx, topk_gate, logits) if want_logits else (topk_idx, topk_gate)
+
+
+def moe_expert_counts(topk_idx: torch.Tensor, E: int, *, want_row_src: bool = False,
+                      etn_accum=None, ws=None, counts=None, offsets=None, dest_row=None):
+    """Returns (counts [E] i32, offsets [E+1] i32, dest_row [T*k] i32[, row_src])."""
+    _dev(topk_idx, "topk_idx")
+    T, k = topk_idx.shape
+    dev = topk_idx.device
+    counts = torch.empty(E, dtype=torch.int32, device=dev) if counts is None else counts
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev) if offsets is None else offsets
+    dest_row = torch.empty(T * k, dtype=torch.int32, device=dev) if dest_row is None else dest_row
+    row_src = torch.empty(T * k, dtype=torch.int32, device=dev) if want_row_src else None
+    nbytes = workspace_bytes(LAEP_CALL_COUNTS, T, k, E)
+    ws = _workspace(ws, nbytes, dev)
+    check(lib().moe_expert_counts(_ptr(topk_idx), T, k, E, _ptr(counts), _ptr(offsets),
+                                  _ptr(dest_row), _ptr(row_src), _ptr(etn_accum), _ptr(ws),
+                                  ws.numel(), _stream(dev)))
+    out = (counts, offsets, dest_row)
+    return out + (row_src,) if want_row_src else out
+
+
+def laep_prune_mask(counts: torch.Tensor, total: int, alpha: float = math.inf,
+                    beta: float = 0.0, *, alive=None, n_pruned=None):
+    """LAEP prune decision.  Returns (alive [E] uint8, n_pruned [1] int32)."""
+    _dev(counts, "counts")
+    E = counts.shape[0]
+    dev = counts.device
+    alive = torch.empty(E, dtype=torch.uint8, device=dev) if alive is None else alive
+    n_pruned = torch.empty(1, dtype=torch.int32, device=dev) if n_pruned is None else n_pruned
+    check(lib().laep_prune_mask(_ptr(counts), E, int(total), float(alpha), float(beta),
+                                _ptr(alive), _ptr(n_pruned), _stream(dev)))
+    return alive, n_pruned
+
+
+def moe_permute(x: torch.Tensor, dest_row: torch.Tensor, k: int, rows: Optional[int] = None,
+                *, out=None):
+    """x_perm[dest_row[t*k+j]] = x[t].  ``rows`` defaults to T*k."""
+    _dev(x, "x"), _dev(dest_row, "dest_row")
+    T, d = x.shape
+    rows = T * k if rows is None else rows
+    out = torch.empty((rows, d), dtype=x.dtype, device=x.device) if out is None else out
+    check(lib().moe_permute(_ptr(x), _dtype_code(x), _ptr(dest_row), T, k, d, _ptr(out),
+                            _stream(x.device)))
+    return out
+
+
+def moe_grouped_ffn_fwd(x_perm: torch.Tensor, w_gate_up: torch.Tensor, w_down: torch.Tensor,
+                        offsets: torch.Tensor, *, expert_map=None, save_act: bool = True,
+                        ws=None, y_perm=None, act_save=None):
+    """Grouped SwiGLU FFN.  Returns (y_perm, act_save or None)."""
+    for t, n in ((x_perm, "x_perm"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
+                 (offsets, "offsets")):
+        _dev(t, n)
+    R, d = x_perm.shape
+    f = w_down.shape[2]
+    E = offsets.shape[0] - 1
+    dev = x_perm.device
+    y_perm = torch.empty_like(x_perm) if y_perm is None else y_perm
+    if save_act and act_save is None:
+        act_save = torch.empty((R, 2 * f), dtype=x_perm.dtype, device=dev)
+    if not save_act:
+        act_save = None
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d, f), dev)
+    check(lib().moe_grouped_ffn_fwd(_ptr(x_perm), _ptr(w_gate_up), _ptr(w_down), _ptr(offsets),
+                                    _ptr(expert_map), _dtype_code(x_perm), E, d, f, R,
+                                    _ptr(y_perm), _ptr(act_save), _ptr(ws), ws.numel(),
+                                    _stream(dev)))
+    return y_perm, act_save
+
+
+def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *,
+                        expert_map=None, dw_gate_up=None, dw_down=None, accumulate=False,
+                        ws=None, dx_perm=None, return_ws: bool = False):
+    """Backward of the grouped FFN.  Returns (dx_perm, dw_gate_up, dw_down[, ws])."""
+    for t, n in ((dy_perm, "dy_perm"), (x_perm, "x_perm"), (act_save, "act_save"),
+                 (w_gate_up, "w_gate_up"), (w_down, "w_down"), (offsets, "offsets")):
+        _dev(t, n)
+    R, d = x_perm.shape
+    f = w_down.shape[2]
+    E = offsets.shape[0] - 1
+    dev = x_perm.device
+    dx_perm = torch.empty_like(x_perm) if dx_perm is None else dx_perm
+    if dw_gate_up is None:
+        dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32, device=dev)
+    if dw_down is None:
+        dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=dev)
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d, f), dev)
+    check(lib().moe_grouped_ffn_bwd(_ptr(dy_perm), _ptr(x_perm), _ptr(act_save),
+                                    _ptr(w_gate_up), _ptr(w_down), _ptr(offsets),
+                                    _ptr(expert_map), _dtype_code(x_perm), E, d, f, R,
+                                    _ptr(dx_perm), _ptr(dw_gate_up), _ptr(dw_down),
+                                    int(accumulate), _ptr(ws), ws.numel(), _stream(dev)))
+    out = (dx_perm, dw_gate_up, dw_down)
+    return out + (ws,) if return_ws else out
+
+
+def ffn_bwd_ws_views(ws: torch.Tensor, R: int, d_ff: int, dtype: torch.dtype):
+    """dA [R, 2f] and H_b [R, f] as left in the backward workspace."""
+    code = _DT[dtype]
+    esz = torch.empty((), dtype=dtype).element_size()
+    off = int(lib().laep_ws_hb_offset(R, d_ff, code))
+    raw = ws.view(torch.uint8)
+    dA = raw[: R * 2 * d_ff * esz].view(dtype).view(R, 2 * d_ff)
+    hb = raw[off: off + R * d_ff * esz].view(dtype).view(R, d_ff)
+    return dA, hb
+
+
+def moe_combine(y_perm: torch.Tensor, topk_gate: torch.Tensor, dest_row: torch.Tensor,
+                *, out=None):
+    """out[t] = sum_j g[t,j] * y_perm[dest_row[t*k+j]]."""
+    _dev(y_perm, "y_perm"), _dev(topk_gate, "topk_gate"), _dev(dest_row, "dest_row")
+    T, k = topk_gate.shape
+    d = y_perm.shape[1]
+    out = torch.empty((T, d), dtype=y_perm.dtype, device=y_perm.device) if out is None else out
+    check(lib().moe_combine(_ptr(y_perm), _ptr(topk_gate), _ptr(dest_row), T, k, d,
+                            _dtype_code(y_perm), _ptr(out), _stream(y_perm.device)))
+    return out
+
+
+def moe_combine_bwd(dout: torch.Tensor, y_perm: torch.Tensor, topk_gate: torch.Tensor,
+                    dest_row: torch.Tensor, *, dy_perm=None, dgate=None):
+    """Returns (dy_perm, dgate)."""
+    for t, n in ((dout, "dout"), (y_perm, "y_perm"), (topk_gate, "topk_gate"),
+                 (dest_row, "dest_row")):
+        _dev(t, n)
+    T, k = topk_gate.shape
+    d = dout.shape[1]
+    dev = dout.device
+    dy_perm = torch.empty_like(y_perm) if dy_perm is None else dy_perm
+    dgate = torch.empty((T, k), dtype=torch.float32, device=dev) if dgate is None else dgate
+    check(lib().moe_combine_bwd(_ptr(dout), _ptr(y_perm), _ptr(topk_gate), _ptr(dest_row), T, k,
+                                d, _dtype_code(dout), _ptr(dy_perm), _ptr(dgate), _stream(dev)))
+    return dy_perm, dgate
+
+
+def moe_permute_bwd(dx_perm: torch.Tensor, dest_row: torch.Tensor, T: int, k: int, *, out=None):
+    """dx[t] = sum_j dx_perm[dest_row[t*k+j]]."""
+    _dev(dx_perm, "dx_perm"), _dev(dest_row, "dest_row")
+    d = dx_perm.shape[1]
+    out = torch.empty((T, d), dtype=dx_perm.dtype, device=dx_perm.device) if out is None else out
+    check(lib().moe_permute_bwd(_ptr(dx_perm), _ptr(dest_row), T, k, d, _dtype_code(dx_perm),
+                                _ptr(out), _stream(dx_perm.device)))
+    return out
+
+
+def laep_rearrange(loads, n_groups: int):
+    """Host utility (Algorithm 2).  Returns dict(group_of, order, sums)."""
+    import numpy as np
+
+    loads = np.ascontiguousarray(loads, dtype=np.float64)
+    n = loads.shape[0]
+    group_of = np.empty(n, dtype=np.int32)
+    order = np.empty(n, dtype=np.int32)
+    sums = np.empty(max(n_groups, 1), dtype=np.float64)
+    check(lib().laep_rearrange(loads.ctypes.data, n, n_groups, group_of.ctypes.data,
+                               order.ctypes.data, sums.ctypes.data))
+    return dict(group_of=group_of, order=order, sums=sums[:n_groups])

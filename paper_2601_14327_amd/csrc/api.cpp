@@ -1,0 +1,284 @@
+// C-ABI entry points (include/laep_moe.h): argument validation, workspace
+// sizing and kernel dispatch.  Validation is pure host code and runs before
+// any HIP call, so an invalid call enqueues nothing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/laep_moe.h"
+#include "internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return LAEP_OK;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e != hipSuccess) return fail(LAEP_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE(cond, code, ...) \
+  do {                           \
+    if (!(cond)) return fail(code, __VA_ARGS__); \
+  } while (0)
+
+int check_dtype(int dtype) {
+  if (dtype != LAEP_F32 && dtype != LAEP_BF16)
+    return fail(LAEP_ERR_UNSUPPORTED, "dtype %d is not LAEP_F32 (0) or LAEP_BF16 (1)", dtype);
+  return LAEP_OK;
+}
+
+int check_experts(int E, int k) {
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(k >= 1 && k <= E, LAEP_ERR_INVALID_ARG, "k=%d outside [1, E=%d]", k, E);
+  return LAEP_OK;
+}
+
+int check_rows(int T, int k, int d_model) {
+  REQUIRE(T >= 0, LAEP_ERR_INVALID_ARG, "T=%d < 0", T);
+  REQUIRE(d_model > 0 && d_model % 8 == 0, LAEP_ERR_INVALID_ARG,
+          "d_model=%d must be a positive multiple of 8", d_model);
+  REQUIRE((long long)T * k <= 0x7FFFFFFFll, LAEP_ERR_INVALID_ARG, "T*k=%lld exceeds int32",
+          (long long)T * k);
+  return LAEP_OK;
+}
+
+size_t elem_bytes(int dtype) { return dtype == LAEP_BF16 ? 2 : 4; }
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+int check_ffn_shape(int dtype, int E, int d_model, int d_ff, int64_t R) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(R >= 0 && R <= 0x7FFFFFFFll, LAEP_ERR_INVALID_ARG, "R=%lld outside [0, 2^31)",
+          (long long)R);
+  REQUIRE(d_model > 0 && d_ff > 0, LAEP_ERR_INVALID_ARG, "d_model=%d, d_ff=%d must be > 0",
+          d_model, d_ff);
+  REQUIRE(d_model % 64 == 0 && d_ff % 64 == 0, LAEP_ERR_UNSUPPORTED,
+          "d_model=%d and d_ff=%d must be multiples of 64", d_model, d_ff);
+  return LAEP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* laep_last_error(void) { return g_err; }
+
+size_t moe_workspace_bytes(int which_call, int T, int k, int E, int d_model, int d_ff) {
+  if (T < 0 || k < 1 || E < 1 || E > LAEP_MAX_EXPERTS) return 0;
+  const int64_t R = (int64_t)T * k;
+  switch (which_call) {
+    case LAEP_CALL_ROUTE:
+      return 0;
+    case LAEP_CALL_COUNTS:
+      return laep::counts_ws_bytes(T, k, E);
+    case LAEP_CALL_FFN_FWD: {
+      // large enough for either dtype: H in fp32 plus the tile table
+      return laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeF32);
+    }
+    case LAEP_CALL_FFN_BWD:
+      return laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeBf16);
+    default:
+      return 0;
+  }
+}
+
+size_t laep_ws_hb_offset(int64_t R, int d_ff, int dtype) {
+  return laep::ffn_bwd_hb_offset(R, d_ff, dtype);
+}
+
+int moe_route(const void* x, const void* w_router, const float* bias, const uint8_t* alive,
+              int dtype, int T, int d_model, int E, int k, int renorm, float* logits,
+              int32_t* topk_idx, float* topk_gate, void* ws, size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  if ((rc = check_experts(E, k))) return rc;
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  if (T == 0) return ok();
+  REQUIRE(x && w_router && topk_idx && topk_gate, LAEP_ERR_INVALID_ARG,
+          "moe_route: x, w_router, topk_idx and topk_gate must be non-null");
+  REQUIRE(aligned16(x) && aligned16(w_router), LAEP_ERR_INVALID_ARG,
+          "moe_route: x and w_router must be 16-byte aligned");
+  return hip_status(laep::launch_route(x, w_router, bias, alive, dtype, T, d_model, E, k,
+                                       renorm != 0, logits, topk_idx, topk_gate,
+                                       as_stream(stream)),
+                    "moe_route");
+}
+
+int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E, int32_t* counts,
+                      int32_t* offsets, int32_t* dest_row, int32_t* row_src, int64_t* etn_accum,
+                      void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_experts(E, k);
+  if (rc) return rc;
+  REQUIRE(T >= 0, LAEP_ERR_INVALID_ARG, "T=%d < 0", T);
+  REQUIRE((long long)T * k <= 0x7FFFFFFFll, LAEP_ERR_INVALID_ARG, "T*k exceeds int32");
+  REQUIRE(counts && offsets, LAEP_ERR_INVALID_ARG,
+          "moe_expert_counts: counts and offsets must be non-null");
+  REQUIRE(T == 0 || (topk_idx && dest_row), LAEP_ERR_INVALID_ARG,
+          "moe_expert_counts: topk_idx and dest_row must be non-null");
+  const size_t need = laep::counts_ws_bytes(T, k, E);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_expert_counts: workspace %zu < %zu bytes",
+          ws_bytes, need);
+  REQUIRE(need == 0 || ws, LAEP_ERR_INVALID_ARG, "moe_expert_counts: ws must be non-null");
+  return hip_status(laep::launch_counts(topk_idx, T, k, E, counts, offsets, dest_row, row_src,
+                                        etn_accum, ws, as_stream(stream)),
+                    "moe_expert_counts");
+}
+
+int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha, double beta,
+                    uint8_t* alive, int32_t* n_pruned, void* stream) {
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(counts && alive && n_pruned, LAEP_ERR_INVALID_ARG,
+          "laep_prune_mask: counts, alive and n_pruned must be non-null");
+  REQUIRE(total >= 0, LAEP_ERR_INVALID_ARG, "laep_prune_mask: total=%lld < 0", (long long)total);
+  REQUIRE(!std::isnan(alpha) && !std::isnan(beta) && alpha >= 0 && beta >= 0,
+          LAEP_ERR_INVALID_ARG, "laep_prune_mask: alpha and beta must be >= 0 (got %g, %g)",
+          alpha, beta);
+  return hip_status(
+      laep::launch_prune(counts, E, total, alpha, beta, alive, n_pruned, as_stream(stream)),
+      "laep_prune_mask");
+}
+
+int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T, int k, int d_model,
+                void* x_perm, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(k >= 1, LAEP_ERR_INVALID_ARG, "k=%d < 1", k);
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  if (T == 0) return ok();
+  REQUIRE(x && dest_row && x_perm, LAEP_ERR_INVALID_ARG,
+          "moe_permute: x, dest_row and x_perm must be non-null");
+  REQUIRE(aligned16(x) && aligned16(x_perm), LAEP_ERR_INVALID_ARG,
+          "moe_permute: x and x_perm must be 16-byte aligned");
+  return hip_status(laep::launch_permute(x, (int)elem_bytes(dtype), dest_row, T, k, d_model,
+                                         x_perm, as_stream(stream)),
+                    "moe_permute");
+}
+
+int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up, const void* w_down,
+                        const int32_t* offsets, const int32_t* expert_map, int dtype, int E,
+                        int d_model, int d_ff, int64_t R, void* y_perm, void* act_save, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
+  if (rc) return rc;
+  REQUIRE(offsets, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd: offsets must be non-null");
+  if (R == 0) return ok();
+  REQUIRE(x_perm && w_gate_up && w_down && y_perm && ws, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd: x_perm, w_gate_up, w_down, y_perm and ws must be non-null");
+  REQUIRE(aligned16(x_perm) && aligned16(w_gate_up) && aligned16(w_down) && aligned16(y_perm) &&
+              aligned16(act_save) && aligned16(ws),
+          LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd: buffers must be 16-byte aligned");
+  const size_t need = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, dtype);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_grouped_ffn_fwd: workspace %zu < %zu bytes",
+          ws_bytes, need);
+  hipError_t e =
+      dtype == LAEP_BF16
+          ? laep::launch_ffn_fwd_bf16(x_perm, w_gate_up, w_down, offsets, expert_map, E, d_model,
+                                      d_ff, R, y_perm, act_save, ws, as_stream(stream))
+          : laep::launch_ffn_fwd_f32(x_perm, w_gate_up, w_down, offsets, expert_map, E, d_model,
+                                     d_ff, R, y_perm, act_save, ws, as_stream(stream));
+  return hip_status(e, "moe_grouped_ffn_fwd");
+}
+
+int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act_save,
+                        const void* w_gate_up, const void* w_down, const int32_t* offsets,
+                        const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
+                        int64_t R, void* dx_perm, float* dw_gate_up, float* dw_down,
+                        int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
+  if (rc) return rc;
+  REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_bwd: only LAEP_BF16 is supported");
+  REQUIRE(offsets && dw_gate_up && dw_down && ws, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_bwd: offsets, dw_gate_up, dw_down and ws must be non-null");
+  REQUIRE(R == 0 || (dy_perm && x_perm && act_save && w_gate_up && w_down && dx_perm),
+          LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd: activation pointers must be non-null");
+  REQUIRE(aligned16(dy_perm) && aligned16(x_perm) && aligned16(act_save) &&
+              aligned16(w_gate_up) && aligned16(w_down) && aligned16(dx_perm) &&
+              aligned16(dw_gate_up) && aligned16(dw_down) && aligned16(ws),
+          LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd: buffers must be 16-byte aligned");
+  const size_t need = laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, dtype);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_grouped_ffn_bwd: workspace %zu < %zu bytes",
+          ws_bytes, need);
+  return hip_status(laep::launch_ffn_bwd_bf16(dy_perm, x_perm, act_save, w_gate_up, w_down,
+                                              offsets, expert_map, E, d_model, d_ff, R, dx_perm,
+                                              dw_gate_up, dw_down, accumulate != 0, ws,
+                                              as_stream(stream)),
+                    "moe_grouped_ffn_bwd");
+}
+
+int moe_combine(const void* y_perm, const float* topk_gate, const int32_t* dest_row, int T, int k,
+                int d_model, int dtype, void* out, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(k >= 1, LAEP_ERR_INVALID_ARG, "k=%d < 1", k);
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  if (T == 0) return ok();
+  REQUIRE(y_perm && topk_gate && dest_row && out, LAEP_ERR_INVALID_ARG,
+          "moe_combine: y_perm, topk_gate, dest_row and out must be non-null");
+  REQUIRE(aligned16(y_perm) && aligned16(out), LAEP_ERR_INVALID_ARG,
+          "moe_combine: y_perm and out must be 16-byte aligned");
+  return hip_status(laep::launch_combine(y_perm, topk_gate, dest_row, T, k, d_model, dtype, out,
+                                         as_stream(stream)),
+                    "moe_combine");
+}
+
+int moe_combine_bwd(const void* dout, const void* y_perm, const float* topk_gate,
+                    const int32_t* dest_row, int T, int k, int d_model, int dtype, void* dy_perm,
+                    float* dgate, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(k >= 1, LAEP_ERR_INVALID_ARG, "k=%d < 1", k);
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  if (T == 0) return ok();
+  REQUIRE(dout && y_perm && topk_gate && dest_row && dy_perm && dgate, LAEP_ERR_INVALID_ARG,
+          "moe_combine_bwd: pointers must be non-null");
+  REQUIRE(aligned16(dout) && aligned16(y_perm) && aligned16(dy_perm), LAEP_ERR_INVALID_ARG,
+          "moe_combine_bwd: dout, y_perm and dy_perm must be 16-byte aligned");
+  return hip_status(laep::launch_combine_bwd(dout, y_perm, topk_gate, dest_row, T, k, d_model,
+                                             dtype, dy_perm, dgate, as_stream(stream)),
+                    "moe_combine_bwd");
+}
+
+int moe_permute_bwd(const void* dx_perm, const int32_t* dest_row, int T, int k, int d_model,
+                    int dtype, void* dx, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(k >= 1, LAEP_ERR_INVALID_ARG, "k=%d < 1", k);
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  if (T == 0) return ok();
+  REQUIRE(dx_perm && dest_row && dx, LAEP_ERR_INVALID_ARG,
+          "moe_permute_bwd: dx_perm, dest_row and dx must be non-null");
+  REQUIRE(aligned16(dx_perm) && aligned16(dx), LAEP_ERR_INVALID_ARG,
+          "moe_permute_bwd: dx_perm and dx must be 16-byte aligned");
+  return hip_status(laep::launch_combine(dx_perm, nullptr, dest_row, T, k, d_model, dtype, dx,
+                                         as_stream(stream)),
+                    "moe_permute_bwd");
+}
+
+}  // extern "C"

@@ -1,0 +1,56 @@
+// Host-side launch entry points of the kernels (internal to the library).
+// Every launcher only enqueues work on `s`; arguments are validated by the
+// C-ABI layer before these are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace laep {
+
+constexpr int kDtypeF32 = 0;
+constexpr int kDtypeBf16 = 1;
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+hipError_t launch_route(const void* x, const void* w, const float* bias, const uint8_t* alive,
+                        int dtype, int T, int d, int E, int k, int renorm, float* logits,
+                        int32_t* idx, float* gate, hipStream_t s);
+
+size_t counts_ws_bytes(int T, int k, int E);
+hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* counts,
+                         int32_t* offsets, int32_t* dest_row, int32_t* row_src, int64_t* etn,
+                         void* ws, hipStream_t s);
+
+hipError_t launch_prune(const int32_t* counts, int E, int64_t total, double alpha, double beta,
+                        uint8_t* alive, int32_t* n_pruned, hipStream_t s);
+
+hipError_t launch_permute(const void* x, int elem_bytes, const int32_t* dest_row, int T, int k,
+                          int d, void* x_perm, hipStream_t s);
+hipError_t launch_combine(const void* y, const float* gate, const int32_t* dest_row, int T, int k,
+                          int d, int dtype, void* out, hipStream_t s);
+hipError_t launch_combine_bwd(const void* dout, const void* y, const float* gate,
+                              const int32_t* dest_row, int T, int k, int d, int dtype, void* dy,
+                              float* dgate, hipStream_t s);
+
+// Grouped SwiGLU FFN.
+size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
+hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
+                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
+                               int f, int64_t R, void* y_perm, void* act_save, void* ws,
+                               hipStream_t s);
+hipError_t launch_ffn_fwd_f32(const void* x_perm, const void* w_gu, const void* w_d,
+                              const int32_t* offsets, const int32_t* expert_map, int E, int d,
+                              int f, int64_t R, void* y_perm, void* act_save, void* ws,
+                              hipStream_t s);
+
+size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
+size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype);
+hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
+                               const void* w_gu, const void* w_d, const int32_t* offsets,
+                               const int32_t* expert_map, int E, int d, int f, int64_t R,
+                               void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
+                               void* ws, hipStream_t s);
+
+}  // namespace laep

@@ -1,0 +1,165 @@
+// Row movement kernels of the dispatch and return paths:
+//   moe_permute      x_perm[dest_row[t*k + j]] = x[t]
+//   moe_combine      out[t] = sum_j g[t, j] * y[dest_row[t*k + j]]
+//   moe_permute_bwd  dx[t]  = sum_j dx_perm[dest_row[t*k + j]]
+//   moe_combine_bwd  dgate[t, j] = <dout[t], y[row]>, dy[row] = g[t, j] * dout[t]
+// All are HBM-bound.  Rows move as 16-byte vectors; consecutive threads own
+// consecutive vectors of a row, so every wave access is one contiguous run.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace laep {
+namespace {
+
+constexpr int kRowThreads = 256;
+
+// Tokens per workgroup: enough vectors for every thread to have ~2.
+__host__ __device__ inline int tokens_per_block(int vec_per_row) {
+  int tpb = (2 * kRowThreads) / (vec_per_row > 0 ? vec_per_row : 1);
+  return tpb < 1 ? 1 : (tpb > 16 ? 16 : tpb);
+}
+
+__global__ __launch_bounds__(kRowThreads) void permute_kernel(
+    const u32x4_t* __restrict__ x, const int32_t* __restrict__ dest_row, int n_tok, int k,
+    int vec_per_row, int tpb, u32x4_t* __restrict__ x_perm) {
+  const int t_lo = blockIdx.x * tpb;
+  const int n_vec = tpb * vec_per_row;
+  for (int i = threadIdx.x; i < n_vec; i += kRowThreads) {
+    const int t = t_lo + i / vec_per_row;
+    const int v = i % vec_per_row;
+    if (t >= n_tok) break;
+    const u32x4_t val = x[(size_t)t * vec_per_row + v];
+    for (int j = 0; j < k; ++j) {
+      const int r = dest_row[(size_t)t * k + j];
+      if (r >= 0) x_perm[(size_t)r * vec_per_row + v] = val;
+    }
+  }
+}
+
+template <typename T, bool GATED>
+__global__ __launch_bounds__(kRowThreads) void combine_kernel(
+    const T* __restrict__ y, const float* __restrict__ gate, const int32_t* __restrict__ dest_row,
+    int n_tok, int k, int d, int tpb, T* __restrict__ out) {
+  const int vec_per_row = d / 8;
+  const int t_lo = blockIdx.x * tpb;
+  const int n_vec = tpb * vec_per_row;
+  for (int i = threadIdx.x; i < n_vec; i += kRowThreads) {
+    const int t = t_lo + i / vec_per_row;
+    const int v = i % vec_per_row;
+    if (t >= n_tok) break;
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
+    for (int j = 0; j < k; ++j) {
+      const size_t s = (size_t)t * k + j;
+      const int r = dest_row[s];
+      if (r < 0) continue;
+      const float g = GATED ? gate[s] : 1.0f;
+      float val[8];
+      Elem<T>::load8(y + (size_t)r * d + (size_t)v * 8, val);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[q] += g * val[q];
+    }
+    Elem<T>::store8(out + (size_t)t * d + (size_t)v * 8, acc);
+  }
+}
+
+// One workgroup per token.
+template <typename T>
+__global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
+    const T* __restrict__ dout, const T* __restrict__ y, const float* __restrict__ gate,
+    const int32_t* __restrict__ dest_row, int n_tok, int k, int d, T* __restrict__ dy,
+    float* __restrict__ dgate) {
+  __shared__ float s_red[kRowThreads / 64];
+  const int t = blockIdx.x;
+  const int vec_per_row = d / 8;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const T* drow = dout + (size_t)t * d;
+  for (int j = 0; j < k; ++j) {
+    const size_t s = (size_t)t * k + j;
+    const int r = dest_row[s];
+    if (r < 0) {  // uniform across the workgroup
+      if (threadIdx.x == 0) dgate[s] = 0.0f;
+      continue;
+    }
+    const float g = gate[s];
+    float part = 0.0f;
+    for (int v = threadIdx.x; v < vec_per_row; v += kRowThreads) {
+      float dv[8], yv[8], o[8];
+      Elem<T>::load8(drow + (size_t)v * 8, dv);
+      Elem<T>::load8(y + (size_t)r * d + (size_t)v * 8, yv);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        part += dv[q] * yv[q];
+        o[q] = g * dv[q];
+      }
+      Elem<T>::store8(dy + (size_t)r * d + (size_t)v * 8, o);
+    }
+    part = wave_sum(part);
+    if (lane == 0) s_red[wave] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float tot = 0.0f;
+      for (int w = 0; w < kRowThreads / 64; ++w) tot += s_red[w];
+      dgate[s] = tot;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_permute(const void* x, int elem_bytes, const int32_t* dest_row, int T, int k,
+                          int d, void* x_perm, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int vec_per_row = d * elem_bytes / 16;
+  const int tpb = tokens_per_block(vec_per_row);
+  hipLaunchKernelGGL(permute_kernel, dim3((T + tpb - 1) / tpb), dim3(kRowThreads), 0, s,
+                     static_cast<const u32x4_t*>(x), dest_row, T, k, vec_per_row, tpb,
+                     static_cast<u32x4_t*>(x_perm));
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const void* y, const float* gate, const int32_t* dest_row, int T, int k,
+                          int d, int dtype, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int tpb = tokens_per_block(d / 8);
+  dim3 grid((T + tpb - 1) / tpb), block(kRowThreads);
+  if (dtype == kDtypeBf16) {
+    if (gate)
+      hipLaunchKernelGGL((combine_kernel<bf16_t, true>), grid, block, 0, s,
+                         static_cast<const bf16_t*>(y), gate, dest_row, T, k, d, tpb,
+                         static_cast<bf16_t*>(out));
+    else
+      hipLaunchKernelGGL((combine_kernel<bf16_t, false>), grid, block, 0, s,
+                         static_cast<const bf16_t*>(y), gate, dest_row, T, k, d, tpb,
+                         static_cast<bf16_t*>(out));
+  } else {
+    if (gate)
+      hipLaunchKernelGGL((combine_kernel<float, true>), grid, block, 0, s,
+                         static_cast<const float*>(y), gate, dest_row, T, k, d, tpb,
+                         static_cast<float*>(out));
+    else
+      hipLaunchKernelGGL((combine_kernel<float, false>), grid, block, 0, s,
+                         static_cast<const float*>(y), gate, dest_row, T, k, d, tpb,
+                         static_cast<float*>(out));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_bwd(const void* dout, const void* y, const float* gate,
+                              const int32_t* dest_row, int T, int k, int d, int dtype, void* dy,
+                              float* dgate, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (dtype == kDtypeBf16)
+    hipLaunchKernelGGL((combine_bwd_kernel<bf16_t>), dim3(T), dim3(kRowThreads), 0, s,
+                       static_cast<const bf16_t*>(dout), static_cast<const bf16_t*>(y), gate,
+                       dest_row, T, k, d, static_cast<bf16_t*>(dy), dgate);
+  else
+    hipLaunchKernelGGL((combine_bwd_kernel<float>), dim3(T), dim3(kRowThreads), 0, s,
+                       static_cast<const float*>(dout), static_cast<const float*>(y), gate,
+                       dest_row, T, k, d, static_cast<float*>(dy), dgate);
+  return hipGetLastError();
+}
+
+}  // namespace laep

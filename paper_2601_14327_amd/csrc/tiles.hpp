@@ -1,0 +1,117 @@
+// Device-side tile tables of the grouped GEMMs.  Built from the expert
+// offsets on the GPU, so the host never learns the per-expert row counts.
+#pragma once
+
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace laep {
+namespace {
+
+struct TileEntry {
+  int row0;    // first routed row of the expert (ragged) / K base (wgrad)
+  int rows;    // rows in this tile (ragged) / rows of the expert (wgrad)
+  int expert;  // logical expert
+  int phys;    // weight slot
+};
+
+// ---------------------------------------------------------------------------
+// Tile tables
+// ---------------------------------------------------------------------------
+constexpr int kTableThreads = 256;
+
+__device__ __forceinline__ int block_excl_scan_256(int v, int* s_tmp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int n = __shfl_up(inc, off, 64);
+    if (lane >= off) inc += n;
+  }
+  if (lane == 63) s_tmp[wave] = inc;
+  __syncthreads();
+  int pre = 0;
+  for (int w = 0; w < wave; ++w) pre += s_tmp[w];
+  __syncthreads();
+  return pre + inc - v;
+}
+
+// mode 0: one entry per BM-row tile of every expert with rows (ragged M)
+// mode 1: one entry per expert that has a weight slot, longest first (wgrad)
+__global__ __launch_bounds__(kTableThreads) void build_table_kernel(
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ expert_map, int E, int BM,
+    int mode, int max_entries, int* __restrict__ n_entries, TileEntry* __restrict__ table) {
+  __shared__ int s_rows[kTableThreads];
+  __shared__ int s_ok[kTableThreads];
+  __shared__ int s_tmp[4];
+  const int e = threadIdx.x;
+  int rows = 0, phys = -1;
+  if (e < E) {
+    rows = offsets[e + 1] - offsets[e];
+    phys = expert_map ? expert_map[e] : e;
+  }
+  int cnt;
+  if (mode == 0)
+    cnt = (e < E && phys >= 0 && rows > 0) ? (rows + BM - 1) / BM : 0;
+  else
+    cnt = (e < E && phys >= 0) ? 1 : 0;
+  s_rows[e] = rows;
+  s_ok[e] = cnt;
+  __syncthreads();
+  int start;
+  if (mode == 0) {
+    start = block_excl_scan_256(cnt, s_tmp);
+  } else {  // rank by rows descending, then index
+    start = 0;
+    if (cnt)
+      for (int j = 0; j < E; ++j)
+        start += s_ok[j] && (s_rows[j] > rows || (s_rows[j] == rows && j < e));
+  }
+  if (mode == 0) {
+    for (int i = 0; i < cnt; ++i) {
+      const int pos = start + i;
+      if (pos < max_entries) {
+        TileEntry te;
+        te.row0 = offsets[e] + i * BM;
+        te.rows = min(BM, rows - i * BM);
+        te.expert = e;
+        te.phys = phys;
+        table[pos] = te;
+      }
+    }
+    const int total = block_excl_scan_256(cnt, s_tmp) + cnt;  // last thread holds the total
+    if (e == kTableThreads - 1) *n_entries = min(total, max_entries);
+  } else {
+    if (cnt && start < max_entries) {
+      TileEntry te;
+      te.row0 = offsets[e];
+      te.rows = rows;
+      te.expert = e;
+      te.phys = phys;
+      table[start] = te;
+    }
+    int tot = block_excl_scan_256(cnt, s_tmp) + cnt;
+    if (e == kTableThreads - 1) *n_entries = min(tot, max_entries);
+  }
+}
+
+struct TableWs {
+  int* n_entries;
+  TileEntry* table;
+  int max_entries;
+};
+
+inline size_t table_bytes(int max_entries) {
+  return align_up(256 + (size_t)max_entries * sizeof(TileEntry), 256);
+}
+
+inline TableWs carve_table(void* base, int max_entries) {
+  TableWs t;
+  t.n_entries = static_cast<int*>(base);
+  t.table = reinterpret_cast<TileEntry*>(static_cast<char*>(base) + 256);
+  t.max_entries = max_entries;
+  return t;
+}
+
+}  // namespace
+}  // namespace laep

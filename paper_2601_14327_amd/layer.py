@@ -1,0 +1,126 @@
+"""One MoE layer pass as a fixed chain of C-ABI calls on preallocated buffers.
+
+Forward (router path):
+    moe_route -> moe_expert_counts
+      [-> laep_prune_mask -> moe_route(alive) -> moe_expert_counts]   (pruning)
+    -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
+Forward (given routing, one device's expert shard with k = 1):
+    moe_expert_counts -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
+Backward:
+    moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
+
+All buffers are allocated once, so a pass makes no allocation and no host
+synchronisation; every step runs in the library's kernels on the current
+stream.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional
+
+import torch
+
+from . import api
+from ._lib import LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD
+
+
+class MoELayerPlan:
+    def __init__(self, T: int, d_model: int, E: int, k: int, d_ff: int,
+                 dtype: torch.dtype = torch.bfloat16, device="cuda", backward: bool = False):
+        self.T, self.d, self.E, self.k, self.f = T, d_model, E, k, d_ff
+        self.R = T * k
+        self.dtype = dtype
+        dev = torch.device(device)
+        self.device = dev
+        i32 = torch.int32
+        R = self.R
+        self.topk_idx = torch.empty((T, k), dtype=i32, device=dev)
+        self.topk_gate = torch.empty((T, k), dtype=torch.float32, device=dev)
+        self.counts = torch.empty(E, dtype=i32, device=dev)
+        self.offsets = torch.empty(E + 1, dtype=i32, device=dev)
+        self.dest_row = torch.empty(R, dtype=i32, device=dev)
+        self.alive = torch.empty(E, dtype=torch.uint8, device=dev)
+        self.n_pruned = torch.empty(1, dtype=i32, device=dev)
+        self.x_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
+        self.y_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
+        self.act_save = torch.empty((R, 2 * d_ff), dtype=dtype, device=dev)
+        self.out = torch.empty((T, d_model), dtype=dtype, device=dev)
+        self.ws_counts = torch.empty(max(1, api.workspace_bytes(LAEP_CALL_COUNTS, T, k, E)),
+                                     dtype=torch.uint8, device=dev)
+        self.ws_ffn = torch.empty(api.workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff),
+                                  dtype=torch.uint8, device=dev)
+        if backward:
+            self.dy_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
+            self.dx_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
+            self.dgate = torch.empty((T, k), dtype=torch.float32, device=dev)
+            self.dx = torch.empty((T, d_model), dtype=dtype, device=dev)
+            self.ws_bwd = torch.empty(
+                api.workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d_model, d_ff),
+                dtype=torch.uint8, device=dev)
+            self.dw_gate_up = None
+            self.dw_down = None
+
+    # -- pieces --------------------------------------------------------------
+    def route(self, x, w_router, bias=None, alive=None, renorm=True):
+        api.moe_route(x, w_router, self.k, bias=bias, alive=alive, renorm=renorm,
+                      topk_idx=self.topk_idx, topk_gate=self.topk_gate)
+
+    def count(self, etn_accum=None):
+        api.moe_expert_counts(self.topk_idx, self.E, ws=self.ws_counts, counts=self.counts,
+                              offsets=self.offsets, dest_row=self.dest_row,
+                              etn_accum=etn_accum)
+
+    def prune(self, beta: float, alpha: float = math.inf):
+        api.laep_prune_mask(self.counts, self.T * self.k, alpha, beta, alive=self.alive,
+                            n_pruned=self.n_pruned)
+
+    def experts_and_combine(self, x, w_gate_up, w_down, expert_map=None):
+        api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
+        api.moe_grouped_ffn_fwd(self.x_perm, w_gate_up, w_down, self.offsets,
+                                expert_map=expert_map, ws=self.ws_ffn, y_perm=self.y_perm,
+                                act_save=self.act_save)
+        api.moe_combine(self.y_perm, self.topk_gate, self.dest_row, out=self.out)
+        return self.out
+
+    # -- whole passes ----------------------------------------------------------
+    def forward(self, x, w_router, w_gate_up, w_down, bias=None, renorm=True,
+                prune_beta: Optional[float] = None, prune_alpha: float = math.inf):
+        self.route(x, w_router, bias=bias, renorm=renorm)
+        self.count()
+        if prune_beta is not None:
+            self.prune(prune_beta, prune_alpha)
+            self.route(x, w_router, bias=bias, alive=self.alive, renorm=renorm)
+            self.count()
+        return self.experts_and_combine(x, w_gate_up, w_down)
+
+    def forward_given_routing(self, x, topk_idx, topk_gate, w_gate_up, w_down):
+        self.topk_idx.copy_(topk_idx)
+        self.topk_gate.copy_(topk_gate)
+        self.count()
+        return self.experts_and_combine(x, w_gate_up, w_down)
+
+    def backward(self, dout, w_gate_up, w_down, expert_map=None, accumulate=False):
+        api.moe_combine_bwd(dout, self.y_perm, self.topk_gate, self.dest_row,
+                            dy_perm=self.dy_perm, dgate=self.dgate)
+        if self.dw_gate_up is None:
+            self.dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32,
+                                          device=self.device)
+            self.dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=self.device)
+        api.moe_grouped_ffn_bwd(self.dy_perm, self.x_perm, self.act_save, w_gate_up, w_down,
+                                self.offsets, expert_map=expert_map, dw_gate_up=self.dw_gate_up,
+                                dw_down=self.dw_down, accumulate=accumulate, ws=self.ws_bwd,
+                                dx_perm=self.dx_perm)
+        api.moe_permute_bwd(self.dx_perm, self.dest_row, self.T, self.k, out=self.dx)
+        return self.dx, self.dgate, self.dw_gate_up, self.dw_down
+
+
+def layer_forward(x, w_router, w_gate_up, w_down, k, bias=None, renorm=True,
+                  prune_beta=None, prune_alpha=math.inf):
+    """One forward pass with freshly allocated buffers; returns the plan."""
+    T, d = x.shape
+    E = w_router.shape[0]
+    f = w_down.shape[2]
+    plan = MoELayerPlan(T, d, E, k, f, dtype=x.dtype, device=x.device)
+    plan.forward(x, w_router, w_gate_up, w_down, bias=bias, renorm=renorm,
+                 prune_beta=prune_beta, prune_alpha=prune_alpha)
+    return plan

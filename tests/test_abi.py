@@ -1,0 +1,148 @@
+"""C-ABI contract tests that need no GPU: the library loads, exports every
+symbol the header declares, rejects invalid arguments on the host before any
+HIP call, and its host rearrangement utility matches the oracle."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "laep_moe.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2601_14327_amd as laep
+
+    if not os.path.exists(laep.LIB_PATH):
+        from paper_2601_14327_amd import build
+
+        build.build()
+    return laep.lib()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_hot_path_calls():
+    names = _declared_functions()
+    for n in ["moe_route", "moe_expert_counts", "laep_prune_mask", "moe_permute",
+              "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_combine", "moe_combine_bwd",
+              "moe_permute_bwd", "moe_workspace_bytes", "laep_rearrange", "laep_last_error"]:
+        assert n in names, n
+
+
+def test_library_exports_every_declared_symbol(L):
+    for n in _declared_functions():
+        assert hasattr(L, n), f"{n} declared in laep_moe.h but not exported"
+
+
+def test_binding_covers_every_declared_symbol():
+    from paper_2601_14327_amd._lib import SIGNATURES
+
+    assert set(_declared_functions()) == set(SIGNATURES)
+
+
+P = ctypes.c_void_p
+
+
+def _fake(n=1):
+    # host memory stands in for device pointers: validation must reject the
+    # call before touching it
+    buf = (ctypes.c_uint8 * (64 * n))()
+    addr = ctypes.addressof(buf)
+    return buf, (addr + 15) & ~15
+
+
+def _err(L):
+    return L.laep_last_error().decode()
+
+
+def test_route_validation(L):
+    keep, p = _fake()
+    assert L.moe_route(p, p, None, None, 7, 16, 64, 8, 2, 1, None, p, p, None, 0, None) == 2
+    assert "dtype" in _err(L)
+    assert L.moe_route(p, p, None, None, 1, 16, 64, 8, 9, 1, None, p, p, None, 0, None) == 1
+    assert "k=9" in _err(L)
+    assert L.moe_route(p, p, None, None, 1, 16, 64, 300, 2, 1, None, p, p, None, 0, None) == 1
+    assert L.moe_route(p, p, None, None, 1, 16, 60, 8, 2, 1, None, p, p, None, 0, None) == 1
+    assert L.moe_route(None, p, None, None, 1, 16, 64, 8, 2, 1, None, p, p, None, 0, None) == 1
+    assert L.moe_route(p + 2, p, None, None, 1, 16, 64, 8, 2, 1, None, p, p, None, 0, None) == 1
+    assert "aligned" in _err(L)
+    # empty input is a valid no-op that launches nothing
+    assert L.moe_route(None, None, None, None, 1, 0, 64, 8, 2, 1, None, None, None, None, 0, None) == 0
+
+
+def test_counts_validation_and_workspace(L):
+    keep, p = _fake()
+    need = L.moe_workspace_bytes(1, 1000, 8, 64, 0, 0)
+    assert need > 0
+    assert L.moe_expert_counts(p, 1000, 8, 64, p, p, p, None, None, p, need - 1, None) == 3
+    assert "workspace" in _err(L)
+    assert L.moe_expert_counts(p, 1000, 8, 64, None, p, p, None, None, p, need, None) == 1
+
+
+def test_prune_validation(L):
+    keep, p = _fake()
+    assert L.laep_prune_mask(p, 0, 100, math.inf, 0.1, p, p, None) == 1
+    assert L.laep_prune_mask(p, 8, -1, math.inf, 0.1, p, p, None) == 1
+    assert L.laep_prune_mask(p, 8, 100, math.nan, 0.1, p, p, None) == 1
+    assert L.laep_prune_mask(None, 8, 100, math.inf, 0.1, p, p, None) == 1
+
+
+def test_ffn_validation(L):
+    keep, p = _fake()
+    # d_model not a multiple of 64
+    assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 96, 128, 64, p, None, p, 1 << 30, None) == 2
+    assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 128, 128, 64, p, None, p, 16, None) == 3
+    assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 5, 8, 128, 128, 64, p, None, p, 1 << 30, None) == 2
+    # backward: only bf16
+    assert L.moe_grouped_ffn_bwd(p, p, p, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0, p,
+                                 1 << 30, None) == 2
+    assert "LAEP_BF16" in _err(L)
+
+
+def test_rowop_validation(L):
+    keep, p = _fake()
+    assert L.moe_permute(p, 1, p, 10, 2, 12, p, None) == 1
+    assert L.moe_combine(p, p, p, 10, 0, 64, 1, p, None) == 1
+    assert L.moe_combine_bwd(p, p, p, p, 10, 2, 64, 3, p, p, None) == 2
+    assert L.moe_permute_bwd(p, None, 10, 2, 64, 1, p, None) == 1
+
+
+def test_workspace_sizes_are_monotone(L):
+    a = L.moe_workspace_bytes(2, 1024, 1, 16, 256, 256)
+    b = L.moe_workspace_bytes(2, 4096, 1, 16, 256, 256)
+    assert 0 < a < b
+    assert L.moe_workspace_bytes(3, 1024, 1, 16, 256, 256) > 0
+    assert L.moe_workspace_bytes(0, 1024, 1, 16, 256, 256) == 0
+
+
+def test_rearrange_matches_oracle(L):
+    from oracle import laep as olaep
+    from paper_2601_14327_amd import laep_rearrange
+
+    rng = np.random.default_rng(0)
+    cases = [([40, 30, 20, 10, 5, 5], 2), ([100, 1, 1, 1], 2), ([9, 8, 7, 6, 5], 2)]
+    for _ in range(200):
+        n = int(rng.integers(1, 80))
+        cases.append((rng.integers(0, 1000, n).astype(float).tolist(), int(rng.integers(1, n + 1))))
+    for loads, ng in cases:
+        got = laep_rearrange(loads, ng)
+        want = olaep.rearrange(loads, ng)
+        np.testing.assert_array_equal(got["group_of"], want["group_of"])
+        np.testing.assert_array_equal(got["order"], want["order"])
+        np.testing.assert_array_equal(got["sums"], want["sums"])
+
+
+def test_rearrange_errors(L):
+    from paper_2601_14327_amd import LaepError, laep_rearrange
+
+    with pytest.raises(LaepError):
+        laep_rearrange([1.0, 2.0], 0)

@@ -1,0 +1,214 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (MoELayerPlan).  Integer outputs are checked completely;
+floating-point outputs on sampled rows the oracle computes one by one
+(rows are independent, so a row subset is exact)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.laep as ol
+import oracle.moe as om
+import paper_2601_14327_amd as laep
+from workloads import WORKLOADS, cached
+from _gpu import TOL_BF16, TOL_F32, case, check_routing, dev, rownorm_err
+
+pytestmark = pytest.mark.gpu
+BF = torch.bfloat16
+
+
+def h32(t):
+    return t.detach().float().cpu().numpy()
+
+
+def hint(t):
+    return t.detach().cpu().numpy()
+
+
+def _sample_rows(offsets, per_expert=3, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = []
+    for e in range(len(offsets) - 1):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi > lo:
+            rows += [lo, hi - 1] + rng.integers(lo, hi, size=per_expert).tolist()
+    return np.unique(np.array(rows, np.int64))
+
+
+def _expert_of_rows(rows, offsets):
+    return np.searchsorted(offsets, rows, side="right") - 1
+
+
+def _check_ffn_rows(plan, c, rows, w_gu_h, w_d_h):
+    offsets = hint(plan.offsets).astype(np.int64)
+    xp = h32(plan.x_perm[torch.from_numpy(rows).cuda()])
+    y = h32(plan.y_perm[torch.from_numpy(rows).cuda()])
+    act = h32(plan.act_save[torch.from_numpy(rows).cuda()])
+    ex = _expert_of_rows(rows, offsets)
+    ry = np.zeros_like(y, dtype=np.float64)
+    ract = np.zeros_like(act, dtype=np.float64)
+    for e in np.unique(ex):
+        sel = ex == e
+        ry[sel], ract[sel], _ = om.expert_ffn(xp[sel], w_gu_h[e], w_d_h[e], "bf16")
+    assert rownorm_err(y, ry) <= TOL_BF16
+    assert rownorm_err(act, ract) <= TOL_BF16
+
+
+def _check_combine_tokens(plan, toks):
+    k = plan.k
+    dest = hint(plan.dest_row).reshape(-1, k)[toks]
+    gate = hint(plan.topk_gate)[toks]
+    rows = np.unique(dest[dest >= 0]).astype(np.int64)
+    remap = {int(r): i for i, r in enumerate(rows)}
+    y = h32(plan.y_perm[torch.from_numpy(rows).cuda()])
+    dloc = np.vectorize(lambda r: remap.get(int(r), -1))(dest).reshape(-1)
+    ref = om.combine(y, gate, dloc, k, dtype="bf16")
+    assert rownorm_err(h32(plan.out)[toks], ref) <= TOL_BF16
+
+
+def _routed_plan(name):
+    w = WORKLOADS[name]
+    c = cached(name)
+    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda")
+    x, wr = dev(c["x"], BF), dev(c["w_router"], BF)
+    wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
+    bias = dev(c["bias"], torch.float32) if "bias" in c else None
+    return w, c, plan, x, wr, wgu, wd, bias
+
+
+@pytest.mark.parametrize("name", ["balanced", "skewed", "skewed_mild"])
+def test_router_layer_full_size(name):
+    w, c, plan, x, wr, wgu, wd, bias = _routed_plan(name)
+    case(f"full-size layer {name}: first routing pass")
+    plan.route(x, wr, bias=bias, renorm=w.renorm)
+    plan.count()
+    torch.cuda.synchronize()
+    ridx, rgate, margin, _ = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
+                                     renorm=w.renorm)
+    idx = hint(plan.topk_idx)
+    n_diff, _ = check_routing(idx, hint(plan.topk_gate), ridx, rgate, margin, w.k)
+    print(f"  near-tie tokens routed differently: {n_diff} of {w.T}")
+    rc, ro, rd = om.expert_counts(idx, w.E)
+    np.testing.assert_array_equal(hint(plan.counts), rc)
+    np.testing.assert_array_equal(hint(plan.offsets), ro)
+    np.testing.assert_array_equal(hint(plan.dest_row), rd)
+    alive = None
+    if w.prune_beta is not None:
+        case(f"full-size layer {name}: prune + second routing pass")
+        plan.prune(w.prune_beta, w.prune_alpha)
+        plan.route(x, wr, bias=bias, alive=plan.alive, renorm=w.renorm)
+        plan.count()
+        torch.cuda.synchronize()
+        ra, rn, _ = ol.prune_mask(rc, w.T * w.k, w.prune_alpha, w.prune_beta)
+        alive = hint(plan.alive).astype(bool)
+        np.testing.assert_array_equal(alive, ra)
+        assert int(hint(plan.n_pruned)[0]) == rn
+        print(f"  pruned {rn} of {w.E} experts (beta={w.prune_beta})")
+        ridx, rgate, margin, _ = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
+                                         alive=alive, renorm=w.renorm)
+        idx = hint(plan.topk_idx)
+        check_routing(idx, hint(plan.topk_gate), ridx, rgate, margin, w.k)
+        rc, ro, rd = om.expert_counts(idx, w.E)
+        np.testing.assert_array_equal(hint(plan.counts), rc)
+        np.testing.assert_array_equal(hint(plan.dest_row), rd)
+        assert np.all(rc[~alive] == 0)
+    case(f"full-size layer {name}: permute / FFN / combine")
+    plan.experts_and_combine(x, wgu, wd)
+    torch.cuda.synchronize()
+    # permute is a copy: check every row
+    src = np.empty(w.T * w.k, np.int64)
+    src[rd] = np.arange(w.T * w.k) // w.k
+    xp = plan.x_perm.view(torch.int16).cpu().numpy()
+    xs = x.view(torch.int16).cpu().numpy()
+    assert np.array_equal(xp, xs[src])
+    rows = _sample_rows(ro, per_expert=2)
+    _check_ffn_rows(plan, c, rows, c["w_gate_up"], c["w_down"])
+    toks = np.random.default_rng(1).choice(w.T, 256, replace=False)
+    _check_combine_tokens(plan, toks)
+
+
+def _shard_plan(name, backward=False):
+    w = WORKLOADS[name]
+    c = cached(name)
+    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda",
+                             backward=backward)
+    x = dev(c["x"], BF)
+    wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
+    idx = dev(c["topk_idx"], torch.int32)
+    gate = dev(c["topk_gate"], torch.float32)
+    return w, c, plan, x, wgu, wd, idx, gate
+
+
+def test_shard_forward_full_size():
+    w, c, plan, x, wgu, wd, idx, gate = _shard_plan("shard")
+    case("full-size expert shard forward (16 experts, d=4096, f=2048, 32768 rows)")
+    plan.forward_given_routing(x, idx, gate, wgu, wd)
+    torch.cuda.synchronize()
+    rc, ro, rd = om.expert_counts(c["topk_idx"], w.E)
+    np.testing.assert_array_equal(hint(plan.counts), rc)
+    np.testing.assert_array_equal(hint(plan.dest_row), rd)
+    print(f"  rows per expert: {sorted(rc.tolist())}")
+    rows = _sample_rows(ro, per_expert=2, seed=3)
+    _check_ffn_rows(plan, c, rows, c["w_gate_up"], c["w_down"])
+    toks = np.random.default_rng(2).choice(w.T, 256, replace=False)
+    _check_combine_tokens(plan, toks)
+
+
+def test_shard_backward_full_size():
+    w, c, plan, x, wgu, wd, idx, gate = _shard_plan("shard_bwd", backward=True)
+    case("full-size expert shard forward + backward")
+    plan.forward_given_routing(x, idx, gate, wgu, wd)
+    dout = dev(c["dout"], BF)
+    plan.backward(dout, wgu, wd)
+    torch.cuda.synchronize()
+    R, d, f = w.T, w.d_model, w.d_ff
+    offsets = hint(plan.offsets).astype(np.int64)
+    dest = hint(plan.dest_row)
+    g = hint(plan.topk_gate)[:, 0].astype(np.float64)
+    rng = np.random.default_rng(5)
+    # combine backward on sampled routed rows
+    toks = rng.choice(R, 512, replace=False)
+    rows = dest[toks].astype(np.int64)
+    tr = torch.from_numpy(rows).cuda()
+    y = h32(plan.y_perm[tr]).astype(np.float64)
+    dq = h32(dout[torch.from_numpy(toks).cuda()]).astype(np.float64)
+    ref_dg = np.einsum("ij,ij->i", dq, y)
+    cond = np.abs(dq * y).sum(1)
+    assert np.all(np.abs(hint(plan.dgate)[toks, 0] - ref_dg) <= TOL_F32 * cond)
+    from oracle.numerics import round_bf16
+    assert rownorm_err(h32(plan.dy_perm[tr]), round_bf16(g[toks, None] * dq)) <= TOL_BF16
+    # dgrad on sampled rows, teacher-forced on the GPU's act_save / dY / dA
+    dA_ws, hb_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
+    srows = _sample_rows(offsets, per_expert=2, seed=6)
+    ts = torch.from_numpy(srows).cuda()
+    ex = _expert_of_rows(srows, offsets)
+    dy_s, act_s = h32(plan.dy_perm[ts]), h32(plan.act_save[ts])
+    dA_s, hb_s, dx_s = h32(dA_ws[ts]), h32(hb_ws[ts]), h32(plan.dx_perm[ts])
+    for e in np.unique(ex):
+        sel = ex == e
+        dH = dy_s[sel].astype(np.float64) @ c["w_down"][e].astype(np.float64)
+        rdA, rhb = om.swiglu_bwd(dH, act_s[sel], "bf16")
+        assert rownorm_err(dA_s[sel], rdA) <= TOL_BF16
+        assert rownorm_err(hb_s[sel], rhb) <= TOL_BF16
+        rdx = round_bf16(dA_s[sel].astype(np.float64) @ c["w_gate_up"][e].astype(np.float64))
+        assert rownorm_err(dx_s[sel], rdx) <= TOL_BF16
+    # wgrad on sampled output rows, teacher-forced on the GPU's dA / H_b
+    case("full-size wgrad checks")
+    dwgu, dwd = plan.dw_gate_up, plan.dw_down
+    for e in range(w.E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi == lo:
+            continue
+        tr = torch.arange(lo, hi, device="cuda")
+        i_d = rng.choice(d, 3, replace=False)
+        i_g = rng.choice(2 * f, 3, replace=False)
+        dy_e = h32(plan.dy_perm[tr][:, torch.from_numpy(i_d).cuda()]).astype(np.float64)
+        hb_e = h32(hb_ws[tr]).astype(np.float64)
+        ref_d = dy_e.T @ hb_e
+        assert rownorm_err(h32(dwd[e][torch.from_numpy(i_d).cuda()]), ref_d) <= TOL_F32
+        dA_e = h32(dA_ws[tr][:, torch.from_numpy(i_g).cuda()]).astype(np.float64)
+        x_e = h32(plan.x_perm[tr]).astype(np.float64)
+        ref_g = dA_e.T @ x_e
+        assert rownorm_err(h32(dwgu[e][torch.from_numpy(i_g).cuda()]), ref_g) <= TOL_F32
+    # permute backward (k = 1: a gather back to token order)
+    dx_tok = h32(plan.dx[torch.from_numpy(toks).cuda()])
+    assert np.array_equal(dx_tok, h32(plan.dx_perm[torch.from_numpy(rows).cuda()]))

@@ -1,0 +1,318 @@
+"""GPU parity of every step of the layer against the CPU oracle, through the
+C ABI, at sizes the oracle finishes in seconds (several tiles, ragged tails,
+edge cases).  Stages are teacher-forced: each GPU stage is fed the GPU's own
+upstream outputs and compared with the oracle on those same inputs."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.moe as om
+import oracle.laep as ol
+import paper_2601_14327_amd as laep
+from workloads import WORKLOADS, generate, random_case
+from _gpu import (TOL_BF16, TOL_F32, case, check_routing, dev, host, rownorm_err)
+
+pytestmark = pytest.mark.gpu
+
+TD = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def _route_case(c, k, dtype, renorm=True, alive=None):
+    td = TD[dtype]
+    x, wr = dev(c["x"], td), dev(c["w_router"], td)
+    bias = dev(c["bias"], torch.float32) if "bias" in c else None
+    alive_t = None if alive is None else dev(alive.astype(np.uint8), torch.uint8)
+    idx, gate, logits = laep.moe_route(x, wr, k, bias=bias, alive=alive_t, renorm=renorm,
+                                       want_logits=True)
+    torch.cuda.synchronize()
+    ridx, rgate, margin, rlog = om.route(c["x"], c["w_router"], k, bias=c.get("bias"),
+                                        alive=alive, renorm=renorm)
+    return host(idx), host(gate), host(logits), ridx, rgate, margin, rlog
+
+
+# ---------------------------------------------------------------------------
+# routing
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,d,E,k,dtype,renorm,bias", [
+    (256, 128, 8, 2, "f32", False, 0.0),      # tiny fp32 layer, top-2 of a softmax
+    (256, 128, 8, 2, "f32", True, 0.0),
+    (1000, 256, 64, 8, "bf16", True, 0.0),    # ragged token tail
+    (777, 512, 64, 8, "bf16", True, 2.0),     # biased router
+    (333, 192, 40, 5, "bf16", False, 0.0),    # E not a multiple of 32
+    (130, 64, 256, 16, "bf16", True, 0.5),    # largest expert count
+    (65, 136, 3, 3, "bf16", True, 0.0),       # k = E, d not a multiple of 16
+    (1, 64, 1, 1, "f32", True, 0.0),          # one token, one expert
+])
+def test_route_parity(T, d, E, k, dtype, renorm, bias):
+    case(f"route T={T} d={d} E={E} k={k} {dtype} renorm={renorm} bias={bias}")
+    c = random_case(T * 7 + E, T=T, d_model=d, E=E, k=k, d_ff=64, dtype=dtype, bias_std=bias,
+                    weight_std=0.05)
+    idx, gate, logits, ridx, rgate, margin, rlog = _route_case(c, k, dtype, renorm)
+    check_routing(idx, gate, ridx, rgate, margin, k)
+    assert rownorm_err(logits, rlog) <= TOL_F32
+
+
+def test_route_with_alive_mask_and_too_few_alive():
+    T, d, E, k = 300, 128, 16, 4
+    c = random_case(5, T=T, d_model=d, E=E, k=k, d_ff=64, dtype="bf16", weight_std=0.05)
+    alive = np.ones(E, bool)
+    alive[[0, 3, 4, 9, 15]] = False
+    case("route alive mask (11 of 16)")
+    idx, gate, logits, ridx, rgate, margin, rlog = _route_case(c, k, "bf16", True, alive)
+    check_routing(idx, gate, ridx, rgate, margin, k)
+    assert not np.isin(idx, np.nonzero(~alive)[0]).any()
+    assert np.all(np.isneginf(logits[:, ~alive]))
+    alive2 = np.zeros(E, bool)
+    alive2[[2, 7]] = True
+    case("route alive mask (2 of 16 < k)")
+    idx, gate, *_ = _route_case(c, k, "bf16", True, alive2)
+    assert np.all(idx[:, 2:] == -1) and np.all(gate[:, 2:] == 0)
+    assert np.all(np.sort(idx[:, :2], axis=1) == [2, 7])
+    np.testing.assert_allclose(gate[:, :2].sum(1), 1.0, rtol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# counts / offsets / dispatch permutation
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,E,k", [(1, 1, 1), (63, 8, 2), (64, 8, 2), (1000, 64, 8),
+                                   (4097, 256, 16), (2000, 16, 1), (500, 5, 5)])
+def test_counts_bit_exact(T, E, k):
+    rng = np.random.default_rng(T + E)
+    idx = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    case(f"counts T={T} E={E} k={k}")
+    etn = torch.full((E,), 5, dtype=torch.int64, device="cuda")
+    counts, offsets, dest, row_src = laep.moe_expert_counts(
+        dev(idx, torch.int32), E, want_row_src=True, etn_accum=etn)
+    torch.cuda.synchronize()
+    rc, ro, rd = om.expert_counts(idx, E)
+    np.testing.assert_array_equal(host(counts), rc)
+    np.testing.assert_array_equal(host(offsets), ro)
+    np.testing.assert_array_equal(host(dest), rd)
+    rs = host(row_src)
+    np.testing.assert_array_equal(rs[rd], np.arange(T * k))
+    np.testing.assert_array_equal(host(etn), rc + 5)
+
+
+def test_counts_skew_unrouted_and_empty_experts():
+    rng = np.random.default_rng(3)
+    T, E, k = 3000, 32, 4
+    idx = np.full((T, k), -1, np.int32)
+    for t in range(T):
+        m = rng.integers(1, k + 1)
+        idx[t, :m] = rng.choice([0, 1, 2, 5, 31], size=m, replace=False)
+    case("counts skewed with unrouted slots")
+    counts, offsets, dest = laep.moe_expert_counts(dev(idx, torch.int32), E)
+    torch.cuda.synchronize()
+    rc, ro, rd = om.expert_counts(idx, E)
+    np.testing.assert_array_equal(host(counts), rc)
+    np.testing.assert_array_equal(host(offsets), ro)
+    np.testing.assert_array_equal(host(dest), rd)
+
+
+def test_counts_zero_tokens():
+    case("counts T=0")
+    counts, offsets, dest = laep.moe_expert_counts(
+        torch.empty((0, 2), dtype=torch.int32, device="cuda"), 8)
+    torch.cuda.synchronize()
+    assert host(counts).tolist() == [0] * 8 and host(offsets).tolist() == [0] * 9
+
+
+# ---------------------------------------------------------------------------
+# LAEP prune mask
+# ---------------------------------------------------------------------------
+def test_prune_mask_parity():
+    rng = np.random.default_rng(21)
+    cases = [([35, 1, 20, 4, 2, 25, 3, 10], 100, math.inf, 0.1),
+             ([35, 1, 20, 4, 2, 25, 3, 10], 100, 0.2, 0.1),
+             ([5, 5, 5, 85], 100, math.inf, 0.1), ([5, 5, 90], 100, math.inf, 0.1),
+             ([0] * 64, 0, math.inf, 0.05)]
+    for _ in range(150):
+        E = int(rng.integers(1, 257))
+        counts = (rng.pareto(0.8, E) * 40).astype(np.int64)
+        total = int(counts.sum())
+        cases.append((counts.tolist(), total, float(rng.choice([math.inf, 0.2, 0.4, 1.5])),
+                      float(rng.choice([0.0, 0.05, 0.1, 0.3, 1.0]))))
+    case(f"prune {len(cases)} cases")
+    for counts, total, alpha, beta in cases:
+        alive, n = laep.laep_prune_mask(dev(np.array(counts, np.int32), torch.int32), total,
+                                        alpha, beta)
+        ra, rn, _ = ol.prune_mask(counts, total, alpha, beta)
+        np.testing.assert_array_equal(host(alive).astype(bool), ra)
+        assert int(host(n)[0]) == rn
+
+
+# ---------------------------------------------------------------------------
+# permute / combine / permute_bwd / combine_bwd
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("T,d,E,k", [(1000, 256, 16, 4), (37, 72, 5, 2), (300, 4096, 8, 1)])
+def test_rowops_parity(dtype, T, d, E, k):
+    rng = np.random.default_rng(T + d)
+    td = TD[dtype]
+    c = random_case(T, T=T, d_model=d, E=E, k=k, d_ff=64, dtype=dtype)
+    idx = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    if T > 10:
+        idx[5, -1] = -1   # an unrouted slot
+    gate = rng.uniform(0.05, 1, (T, k)).astype(np.float32)
+    rc, ro, rd = om.expert_counts(idx, E)
+    R = int(ro[E])
+    case(f"rowops {dtype} T={T} d={d} k={k}")
+    x = dev(c["x"], td)
+    dest = dev(rd.astype(np.int32), torch.int32)
+    xp = laep.moe_permute(x, dest, k, R)
+    torch.cuda.synchronize()
+    xq = host(x)
+    np.testing.assert_array_equal(host(xp), om.permute(xq, rd, k))    # bit-exact copy
+    y = dev(rng.standard_normal((R, d)).astype(np.float32), td)
+    g = dev(gate, torch.float32)
+    out = laep.moe_combine(y, g, dest)
+    dxp = laep.moe_permute_bwd(y, dest, T, k)
+    dout = dev(rng.standard_normal((T, d)).astype(np.float32), td)
+    dy, dgate = laep.moe_combine_bwd(dout, y, g, dest)
+    torch.cuda.synchronize()
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    yq, dq = host(y), host(dout)
+    assert rownorm_err(host(out), om.combine(yq, gate, rd, k, dtype=dtype)) <= tol
+    assert rownorm_err(host(dxp), om.permute_bwd(yq, rd, k, dtype=dtype)) <= tol
+    rdy, rdg = om.combine_bwd(dq, yq, gate, rd, k, dtype=dtype)
+    routed = rd >= 0
+    got_dy = host(dy)
+    assert rownorm_err(got_dy, rdy) <= tol
+    # dgate is a dot product: bound the error by its condition, sum |dout * y|
+    cond = np.zeros((T, k))
+    for t in range(T):
+        for j in range(k):
+            r = rd[t * k + j]
+            if r >= 0:
+                cond[t, j] = np.abs(dq[t] * yq[r]).sum()
+    assert np.all(np.abs(host(dgate) - rdg) <= TOL_F32 * cond + 1e-30)
+    if T > 10:
+        assert host(dgate)[5, -1] == 0.0
+
+
+# ---------------------------------------------------------------------------
+# grouped SwiGLU FFN
+# ---------------------------------------------------------------------------
+def _ffn_inputs(seed, counts, d, f, dtype, E_phys=None):
+    rng = np.random.default_rng(seed)
+    E = len(counts)
+    E_phys = E if E_phys is None else E_phys
+    R = int(sum(counts))
+    c = random_case(seed, T=R, d_model=d, E=E_phys, k=1, d_ff=f, dtype=dtype)
+    offsets = np.zeros(E + 1, np.int64)
+    offsets[1:] = np.cumsum(counts)
+    return c["x"], c["w_gate_up"], c["w_down"], offsets
+
+
+@pytest.mark.parametrize("dtype,counts,d,f", [
+    ("f32", [60, 0, 200, 5, 1, 130, 64, 52], 128, 256),          # tiny fp32 layer shape
+    ("bf16", [60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
+    ("bf16", [300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),       # ragged, f % 128 = 64
+    ("bf16", [0, 0, 0, 513], 320, 128),                           # one expert takes all
+    ("bf16", [64] * 16, 512, 512),
+])
+def test_ffn_fwd_parity(dtype, counts, d, f):
+    x, wgu, wd, offsets = _ffn_inputs(len(counts) * 31 + d, counts, d, f, dtype)
+    td = TD[dtype]
+    case(f"ffn fwd {dtype} counts={counts} d={d} f={f}")
+    y, act = laep.moe_grouped_ffn_fwd(dev(x, td), dev(wgu, td), dev(wd, td),
+                                      dev(offsets.astype(np.int32), torch.int32))
+    torch.cuda.synchronize()
+    ry, ract = om.grouped_ffn_fwd(x, wgu, wd, offsets, dtype=dtype)
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    assert rownorm_err(host(y), ry) <= tol
+    assert rownorm_err(host(act), ract) <= tol
+
+
+def test_ffn_fwd_expert_map_with_pruned_slots():
+    counts = [100, 0, 37, 0, 250]
+    d, f = 256, 128
+    x, wgu, wd, offsets = _ffn_inputs(9, counts, d, f, "bf16", E_phys=3)
+    emap = np.array([2, -1, 0, -1, 1], np.int32)
+    case("ffn fwd expert_map")
+    y, _ = laep.moe_grouped_ffn_fwd(dev(x, torch.bfloat16), dev(wgu, torch.bfloat16),
+                                    dev(wd, torch.bfloat16),
+                                    dev(offsets.astype(np.int32), torch.int32),
+                                    expert_map=dev(emap, torch.int32))
+    torch.cuda.synchronize()
+    ry, _ = om.grouped_ffn_fwd(x, wgu, wd, offsets, expert_map=emap, dtype="bf16")
+    assert rownorm_err(host(y), ry) <= TOL_BF16
+
+
+@pytest.mark.parametrize("counts,d,f", [
+    ([60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
+    ([300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),
+])
+def test_ffn_bwd_parity(counts, d, f):
+    x, wgu, wd, offsets = _ffn_inputs(len(counts) + d, counts, d, f, "bf16")
+    R = int(offsets[-1])
+    E = len(counts)
+    rng = np.random.default_rng(4)
+    bf = torch.bfloat16
+    xt, wgut, wdt = dev(x, bf), dev(wgu, bf), dev(wd, bf)
+    off = dev(offsets.astype(np.int32), torch.int32)
+    case(f"ffn bwd counts={counts} d={d} f={f}")
+    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off)
+    dy = dev(rng.standard_normal((R, d)).astype(np.float32), bf)
+    dwgu = torch.full(wgut.shape, 7.0, dtype=torch.float32, device="cuda")
+    dwd = torch.full(wdt.shape, 7.0, dtype=torch.float32, device="cuda")
+    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off,
+                                                 dw_gate_up=dwgu, dw_down=dwd, return_ws=True)
+    torch.cuda.synchronize()
+    dA_g, hb_g = laep.ffn_bwd_ws_views(ws, R, f, bf)
+    act_h, dy_h, dA_h, hb_h = host(act), host(dy), host(dA_g), host(hb_g)
+    # dgrad 1 + SwiGLU backward (teacher-forced on the GPU's act_save)
+    rdx, rdA, rhb = om.grouped_ffn_dgrad(dy_h, act_h, wgu, wd, offsets, dtype="bf16",
+                                         dA_given=dA_h)
+    assert rownorm_err(dA_h, rdA) <= TOL_BF16
+    assert rownorm_err(hb_h, rhb) <= TOL_BF16
+    assert rownorm_err(host(dx), rdx) <= TOL_BF16
+    # wgrad (teacher-forced on the GPU's dA and H_b), fp32
+    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, hb_h, offsets, E)
+    got_gu, got_d = host(dwgu), host(dwd)
+    for e in range(E):
+        assert rownorm_err(got_gu[e], rgu[e]) <= TOL_F32, e
+        assert rownorm_err(got_d[e], rd[e]) <= TOL_F32, e
+    # accumulate adds onto the existing gradient
+    case("ffn bwd accumulate")
+    laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, dw_gate_up=dwgu, dw_down=dwd,
+                             accumulate=True)
+    torch.cuda.synchronize()
+    assert rownorm_err(host(dwd).reshape(E, -1), (2 * rd).reshape(E, -1)) <= TOL_F32
+
+
+# ---------------------------------------------------------------------------
+# the whole layer, end to end, tiny fp32 workload
+# ---------------------------------------------------------------------------
+def test_tiny_layer_end_to_end():
+    w = WORKLOADS["tiny"]
+    c = generate(w)
+    td = torch.float32
+    case("tiny layer end to end (fp32)")
+    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=td, device="cuda")
+    out = plan.forward(dev(c["x"], td), dev(c["w_router"], td), dev(c["w_gate_up"], td),
+                       dev(c["w_down"], td), renorm=w.renorm)
+    torch.cuda.synchronize()
+    ref = om.layer_forward(c["x"], c["w_router"], c["w_gate_up"], c["w_down"], w.k,
+                           renorm=w.renorm, dtype="f32")
+    ok = np.all(host(plan.topk_idx) == ref["idx"], axis=1)
+    assert np.all(ok | (ref["margin"] < 1e-4))
+    assert rownorm_err(host(out)[ok], ref["out"][ok]) <= TOL_F32
+
+
+def test_determinism():
+    w = WORKLOADS["balanced"]
+    c = random_case(11, T=1500, d_model=512, E=64, k=8, d_ff=256, dtype="bf16")
+    bf = torch.bfloat16
+    args = (dev(c["x"], bf), dev(c["w_router"], bf), dev(c["w_gate_up"], bf),
+            dev(c["w_down"], bf))
+    case("determinism")
+    p1 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda")
+    p2 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda")
+    o1 = p1.forward(*args).clone()
+    o2 = p2.forward(*args)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    assert torch.equal(p1.act_save, p2.act_save)
