@@ -54,10 +54,13 @@ def _cpu_baseline(w, c, budget_s: float):
             om.combine(y, c["topk_gate"][:n], dest, 1, dtype="bf16")
         return time.perf_counter() - t0
 
+    # grow the sample until one run costs about half the budget (or is whole)
     n = min(256, w.T)
     dt = run(n)
-    if dt < budget_s / 3 and n < w.T:
-        n = int(min(w.T, n * max(1.0, (budget_s / 2) / max(dt, 1e-3))))
+    for _ in range(4):
+        if dt >= budget_s / 2 or n >= w.T:
+            break
+        n = int(min(w.T, max(2 * n, n * (budget_s * 0.6) / max(dt, 1e-3))))
         dt = run(n)
     unit = "tokens/s" if w.routed else "rows/s"
     return {"value": n / dt, "unit": unit, "cores": threads, "kind": "oracle",

@@ -21,25 +21,23 @@ constexpr int kWave = 64;
 
 // ---------------------------------------------------------------------------
 // bf16 <-> fp32.  bf16 keeps the sign, the 8 exponent bits and the top 7
-// fraction bits of binary32.  Narrowing rounds to nearest, ties to even:
-// add 0x7FFF plus the lowest kept bit, then truncate.  NaN stays a quiet NaN.
+// fraction bits of binary32.  Narrowing uses gfx950's v_cvt_pk_bf16_f32
+// (round to nearest, ties to even; NaN stays NaN), which the compiler emits
+// for a float -> __bf16 conversion; it is branch-free.
 // ---------------------------------------------------------------------------
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) {
   return __uint_as_float(b << 16);
 }
 
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu))
-    return (u >> 16) | 0x40u;  // quiet NaN
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
 // two floats -> packed bf16x2 (lo in bits 0..15)
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
+
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) { return pack_bf16x2(f, 0.0f) & 0xFFFFu; }
 
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -98,7 +96,11 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-__device__ __forceinline__ float fast_silu(float a) { return a / (1.0f + __expf(-a)); }
-__device__ __forceinline__ float fast_sigmoid(float a) { return 1.0f / (1.0f + __expf(-a)); }
+// sigmoid / SiLU for bf16 outputs: hardware exp2 and reciprocal (about 1 ulp
+// each in fp32, far below bf16 resolution)
+__device__ __forceinline__ float fast_sigmoid(float a) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-a));
+}
+__device__ __forceinline__ float fast_silu(float a) { return a * fast_sigmoid(a); }
 
 }  // namespace laep

@@ -28,6 +28,9 @@
 #include "internal.hpp"
 #include "tiles.hpp"
 
+#include <cstdlib>
+#include <cstring>
+
 namespace laep {
 namespace {
 
@@ -378,6 +381,297 @@ __global__ __launch_bounds__(64 * NWM * NWN) void grouped_gemm_kernel(GemmParams
 }
 
 // ---------------------------------------------------------------------------
+// Forward products (both operands K-contiguous): deep LDS-DMA pipeline.
+//
+// Global -> LDS moves use global_load_lds_dwordx4 (no register staging):
+// every wave instruction fills 1 KB of LDS contiguously, lane i at +16*i, so
+// the swizzle is applied on the global side (each lane fetches the chunk
+// that belongs in its LDS slot).  BK = 32: an LDS row is 64 bytes (4 chunks)
+// and chunk c of row r is stored at c ^ ((r >> 2) & 3).  With that layout the
+// fragment reads (lane -> row lane % 32, chunk lane / 32) measured zero LDS
+// bank-conflict cycles on gfx950 (SQ_LDS_BANK_CONFLICT), where the unswizzled
+// layout costs 3 extra cycles per ds_read_b128.
+// NS stages are in flight; one s_barrier per k-tile.  The wait before it is
+// an explicit vmcnt on this thread's outstanding LDS-DMA loads, then the
+// barrier makes every thread's loads visible.
+// ---------------------------------------------------------------------------
+constexpr int PBK = 32;          // k per pipeline stage
+constexpr int PROW = PBK * 2;    // bytes per LDS row
+
+__device__ __forceinline__ int pswz(int row) { return (row >> 2) & 3; }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt lgkmcnt(0) only (vmcnt field at its maximum, 63)
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// One k-tile of LDS-DMA loads for this thread: A chunks then B chunks.  (A
+// device function, not a lambda: the host pass of a kernel must not see the
+// LDS-DMA builtin inside a lambda, or the kernel's launch stub is dropped.)
+template <int NA, int NB, int NT, int A_BYTES>
+__device__ __forceinline__ void dma_tile(char* st, const bf16_t* const* a_src,
+                                         const bf16_t* const* b_src, int k0, int wave) {
+#pragma unroll
+  for (int i = 0; i < NA; ++i)
+    __builtin_amdgcn_global_load_lds(a_src[i] + k0, (lds_void_t*)(st + (i * NT + wave * 64) * 16),
+                                     16, 0, 0);
+#pragma unroll
+  for (int i = 0; i < NB; ++i)
+    __builtin_amdgcn_global_load_lds(b_src[i] + k0,
+                                     (lds_void_t*)(st + A_BYTES + (i * NT + wave * 64) * 16), 16,
+                                     0, 0);
+}
+
+template <int BM, int BN, int NWM, int NWN, int NS, int EPI, bool GU_ROWS>
+__global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_pipe_kernel(GemmParams p) {
+  constexpr int NT = 64 * NWM * NWN;
+  static_assert((BM * 4) % NT == 0 && (BN * 4) % NT == 0, "chunks must divide over the threads");
+  static_assert(NS >= 3, "at least three stages");
+  constexpr int WTM = BM / NWM, WTN = BN / NWN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * PROW, B_BYTES = BN * PROW;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int NA = BM * 4 / NT, NB = BN * 4 / NT;  // 16-byte chunks per thread
+  constexpr int NLD = NA + NB;                        // loads per thread per k-tile
+  constexpr int NFR = TM + TN;                        // fragment reads per k16 step
+  static_assert(EPI != EPI_GU || (TN % 2 == 0), "SwiGLU epilogue pairs gate/up blocks");
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+
+  // ---- tile schedule (XCD-contiguous) --------------------------------------
+  const int n_valid = (*p.n_entries) * p.tiles_per_entry;
+  const int per = (n_valid + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per) return;
+  const int L = (blockIdx.x & 7) * per + slot;
+  if (L >= n_valid) return;
+  const TileEntry te = p.table[L / p.tiles_per_entry];
+  const int nt = L % p.tiles_per_entry;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / NWN, wn = wave % NWN;
+
+  // ---- per-thread global source of each LDS chunk it fills ------------------
+  const bf16_t* a_src[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int q = i * NT + tid;
+    const int r = q >> 2;
+    const int lc = (q & 3) ^ pswz(r);
+    const int rr = r < te.rows ? r : te.rows - 1;   // rows past the expert: any valid row
+    a_src[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
+  }
+  const bf16_t* Bw = p.B + (long long)te.phys * p.strideB;
+  const bf16_t* b_src[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int q = i * NT + tid;
+    const int r = q >> 2;
+    const int lc = (q & 3) ^ pswz(r);
+    int row;
+    if (GU_ROWS) {
+      const int grp = r >> 6, w = r & 63;
+      int fcol = nt * (BN / 2) + grp * 32 + (w & 31);
+      fcol = fcol < p.f ? fcol : p.f - 1;
+      row = (w < 32) ? fcol : p.f + fcol;
+    } else {
+      row = nt * BN + r;
+      row = row < p.N ? row : p.N - 1;
+    }
+    b_src[i] = Bw + (long long)row * p.ldb + lc * 8;
+  }
+  auto issue = [&](int kt) {
+    dma_tile<NA, NB, NT, A_BYTES>(smem + (kt % NS) * STAGE, a_src, b_src, kt * PBK, wave);
+  };
+  // fragment LDS byte offsets within a stage for k16 step 0; step 1 is ^32
+  int a_off[TM], b_off[TN];
+  const int lc0 = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + (lane & 31);
+    a_off[i] = r * PROW + ((lc0 ^ pswz(r)) << 4);
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int r = wn * WTN + j * 32 + (lane & 31);
+    b_off[j] = A_BYTES + r * PROW + ((lc0 ^ pswz(r)) << 4);
+  }
+  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+  auto read_frags = [&](const char* st, int flip, u32x4_t* fa, u32x4_t* fb) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(st + (a_off[i] ^ flip));
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const u32x4_t*>(st + (b_off[j] ^ flip));
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
+            0, 0, 0);
+  };
+  // interleave the fragment reads of the next step with this step's MFMAs
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < NFR; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - NFR, 0);
+  };
+
+  const int nk = p.K / PBK;
+  // Every iteration issues exactly one k-tile of LDS-DMA loads (past the end
+  // the last k-tile is loaded again into the free stage), so the number of
+  // loads in flight is the same at every wait and one constant vmcnt
+  // suffices: the loop body is straight-line code, which lets the compiler
+  // keep exact LDS wait counts across the barrier.
+  // prologue: tiles 0 .. NS-2 in flight (stage NS-1 stays free for the first
+  // refill), tile 0 landed, its step-0 fragments read
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t) issue(t < nk ? t : nk - 1);
+  wait_vmcnt<(NS - 2) * NLD>();
+  __builtin_amdgcn_s_barrier();
+  read_frags(smem, 0, fa0, fb0);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const char* st = smem + (kt % NS) * STAGE;
+    // first half: MFMAs of step 0, fragment reads of step 1 of the same tile
+    read_frags(st, 32, fa1, fb1);
+    mma_step(fa0, fb0);
+    interleave();
+    // tile boundary: tile kt+1 has landed for every thread, and every wave is
+    // done with stage (kt-1) % NS, which receives tile kt+NS-1
+    wait_vmcnt<(NS - 3) * NLD>();
+    __builtin_amdgcn_s_barrier();
+    {
+      const int t = kt + NS - 1;
+      dma_tile<NA, NB, NT, A_BYTES>(smem + (t % NS) * STAGE, a_src, b_src,
+                                    (t < nk ? t : nk - 1) * PBK, wave);
+    }
+    read_frags(smem + ((kt + 1) % NS) * STAGE, 0, fa0, fb0);
+    // second half: MFMAs of step 1, step-0 fragment reads of the next tile
+    mma_step(fa1, fb1);
+    interleave();
+  }
+  // no LDS-DMA may still be writing when the workgroup retires
+  wait_vmcnt<0>();
+
+  // ---- epilogues: stage the tile in LDS, then write whole rows -----------------
+  // Each lane holds one row and 4 consecutive columns per register quad, so a
+  // direct store scatters 16 bytes into each of 32 rows.  Staging through the
+  // (now idle) LDS lets every store instruction write 4 rows of 256 contiguous
+  // bytes instead.
+  wait_lgkm0();  // all LDS reads done
+  __builtin_amdgcn_s_barrier();
+  const int lrow = lane & 31;
+  const int lcol = (lane >> 5) * 4;
+  constexpr int SCOLS = (EPI == EPI_GU) ? BN : BN;  // staged columns per pass
+  constexpr int PITCH = SCOLS * 2 + 16;               // bytes per staged row
+  static_assert(BM * PITCH <= NS * STAGE, "staging tile must fit in LDS");
+  // write the staged [BM][SCOLS] tile to global rows: columns [0, ncols) of
+  // the staged tile go to dst + row * ld + col (bf16), rows < te.rows only
+  auto flush = [&](bf16_t* dst, long long ld, int ncols, int scol0) {
+    const int chunks_per_row = ncols / 8;
+    const int total = BM * chunks_per_row;
+    for (int c = tid; c < total; c += NT) {
+      const int r = c / chunks_per_row, cc = c % chunks_per_row;
+      if (r < te.rows) {
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(smem + r * PITCH + (scol0 + cc * 8) * 2);
+        *reinterpret_cast<u32x4_t*>(dst + (te.row0 + r) * ld + cc * 8) = v;
+      }
+    }
+  };
+  auto stage = [&](int row, int col, float a, float b, float c, float d) {
+    u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
+    *reinterpret_cast<u32x2_t*>(smem + row * PITCH + col * 2) = w;
+  };
+  if (EPI == EPI_GU) {
+    // staged columns: [0, BN/2) = gate f-columns, [BN/2, BN) = up f-columns
+    const int f = p.f;
+    const int fbase = nt * (BN / 2);
+    const int fcols = min(BN / 2, f - fbase);
+    if (p.out2) {  // pass 1: act_save (gate and up pre-activations)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = wm * WTM + i * 32 + lrow;
+#pragma unroll
+        for (int pp = 0; pp < TN / 2; ++pp) {
+          const int grp = (wn * WTN) / 64 + pp;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int c = grp * 32 + q * 8 + lcol;
+            stage(r, c, acc[i][2 * pp][q * 4], acc[i][2 * pp][q * 4 + 1],
+                  acc[i][2 * pp][q * 4 + 2], acc[i][2 * pp][q * 4 + 3]);
+            stage(r, BN / 2 + c, acc[i][2 * pp + 1][q * 4], acc[i][2 * pp + 1][q * 4 + 1],
+                  acc[i][2 * pp + 1][q * 4 + 2], acc[i][2 * pp + 1][q * 4 + 3]);
+          }
+        }
+      }
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      flush(p.out2 + fbase, 2LL * f, fcols, 0);
+      flush(p.out2 + f + fbase, 2LL * f, fcols, BN / 2);
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+    }
+    // pass 2: H = silu(gate) * up
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int pp = 0; pp < TN / 2; ++pp) {
+        const int grp = (wn * WTN) / 64 + pp;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float h[4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            h[c] = fast_silu(acc[i][2 * pp][q * 4 + c]) * acc[i][2 * pp + 1][q * 4 + c];
+          stage(r, grp * 32 + q * 8 + lcol, h[0], h[1], h[2], h[3]);
+        }
+      }
+    }
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+    flush(p.out + fbase, f, fcols, 0);
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          stage(r, wn * WTN + j * 32 + q * 8 + lcol, acc[i][j][q * 4], acc[i][j][q * 4 + 1],
+                acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
+    }
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+    flush(p.out + nt * BN, p.ldo, min(BN, p.N - nt * BN), 0);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
 constexpr int kBM = 128, kBN = 128, kNWM = 2, kNWN = 2;
@@ -396,6 +690,74 @@ hipError_t launch_gemm(const GemmParams& p, int grid, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Forward tile shapes.  The default is 256 x 256 with 8 waves (2 x 4, each
+// 128 x 64, two waves per SIMD so one wave's MFMAs cover the other's waits).
+// 256 x 256 with 4 waves and 128 x 512 with 4 waves remain selectable through
+// LAEP_GEMM_TILE=256x256 / 128x512 for tuning comparisons.
+enum FwdTile { TILE_128x512 = 0, TILE_256x256 = 1, TILE_256x256_W8 = 2 };
+
+FwdTile pick_fwd_tile(int64_t R, int E) {
+  static const char* env = getenv("LAEP_GEMM_TILE");
+  if (env && strcmp(env, "128x512") == 0) return TILE_128x512;
+  if (env && strcmp(env, "256x256") == 0) return TILE_256x256;
+  if (env && strcmp(env, "256x256w8") == 0) return TILE_256x256_W8;
+  (void)R;
+  (void)E;
+  return TILE_256x256_W8;
+}
+
+template <int BM, int BN, int NWM, int NWN, int NS, int EPI, bool GU>
+hipError_t launch_pipe(const GemmParams& p, int grid, hipStream_t s) {
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_nt_pipe_kernel<BM, BN, NWM, NWN, NS, EPI, GU>), dim3(round8(grid)),
+                     dim3(64 * NWM * NWN), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int NWM, int NWN, int NS>
+hipError_t ffn_fwd_pipe(const void* x_perm, const void* w_gu, const void* w_d,
+                        const int32_t* offsets, const int32_t* expert_map, int E, int d, int f,
+                        int64_t R, void* y_perm, void* act_save, void* ws, hipStream_t s) {
+  bf16_t* H = static_cast<bf16_t*>(ws);
+  const int max_entries = ceil_div(R, BM) + E;
+  TableWs tw = carve_table(static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256), max_entries);
+  hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
+                     E, BM, 0, max_entries, tw.n_entries, tw.table);
+  GemmParams g = {};
+  g.table = tw.table;
+  g.n_entries = tw.n_entries;
+  g.f = f;
+  // gate/up + SwiGLU: B rows interleaved gate/up per 32, BN/2 f-columns per tile
+  g.A = static_cast<const bf16_t*>(x_perm);
+  g.lda = d;
+  g.B = static_cast<const bf16_t*>(w_gu);
+  g.ldb = d;
+  g.strideB = (long long)2 * f * d;
+  g.N = 2 * f;
+  g.K = d;
+  g.n_tiles_n = ceil_div(f, BN / 2);
+  g.tiles_per_entry = g.n_tiles_n;
+  g.out = H;
+  g.ldo = f;
+  g.out2 = static_cast<bf16_t*>(act_save);
+  hipError_t err = launch_pipe<BM, BN, NWM, NWN, NS, EPI_GU, true>(g, max_entries * g.n_tiles_n, s);
+  if (err != hipSuccess) return err;
+  // down projection
+  g.A = H;
+  g.lda = f;
+  g.B = static_cast<const bf16_t*>(w_d);
+  g.ldb = f;
+  g.strideB = (long long)d * f;
+  g.N = d;
+  g.K = f;
+  g.n_tiles_n = ceil_div(d, BN);
+  g.tiles_per_entry = g.n_tiles_n;
+  g.out = static_cast<bf16_t*>(y_perm);
+  g.ldo = d;
+  g.out2 = nullptr;
+  return launch_pipe<BM, BN, NWM, NWN, NS, EPI_STORE, false>(g, max_entries * g.n_tiles_n, s);
+}
+
 }  // namespace
 
 size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
@@ -409,45 +771,15 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
                                hipStream_t s) {
-  bf16_t* H = static_cast<bf16_t*>(ws);
-  const int max_entries = ragged_max_entries(R, E);
-  TableWs tw = carve_table(static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256), max_entries);
-  hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
-                     E, kBM, 0, max_entries, tw.n_entries, tw.table);
-
-  GemmParams g = {};
-  g.table = tw.table;
-  g.n_entries = tw.n_entries;
-  g.f = f;
-  // gate/up + SwiGLU: N = 2f (interleaved), K = d
-  g.A = static_cast<const bf16_t*>(x_perm);
-  g.lda = d;
-  g.B = static_cast<const bf16_t*>(w_gu);
-  g.ldb = d;
-  g.strideB = (long long)2 * f * d;
-  g.N = 2 * f;
-  g.K = d;
-  g.n_tiles_n = ceil_div(2 * f, kBN);
-  g.tiles_per_entry = g.n_tiles_n;
-  g.out = H;
-  g.ldo = f;
-  g.out2 = static_cast<bf16_t*>(act_save);
-  hipError_t err = launch_gemm<EPI_GU, false, false, true>(g, max_entries * g.n_tiles_n, s);
-  if (err != hipSuccess) return err;
-  // down: N = d, K = f
-  g.A = H;
-  g.lda = f;
-  g.B = static_cast<const bf16_t*>(w_d);
-  g.ldb = f;
-  g.strideB = (long long)d * f;
-  g.N = d;
-  g.K = f;
-  g.n_tiles_n = ceil_div(d, kBN);
-  g.tiles_per_entry = g.n_tiles_n;
-  g.out = static_cast<bf16_t*>(y_perm);
-  g.ldo = d;
-  g.out2 = nullptr;
-  return launch_gemm<EPI_STORE, false, false, false>(g, max_entries * g.n_tiles_n, s);
+  const FwdTile tile = pick_fwd_tile(R, E);
+  if (tile == TILE_256x256_W8)
+    return ffn_fwd_pipe<256, 256, 2, 4, 5>(x_perm, w_gu, w_d, offsets, expert_map, E, d, f, R,
+                                           y_perm, act_save, ws, s);
+  if (tile == TILE_256x256)
+    return ffn_fwd_pipe<256, 256, 2, 2, 5>(x_perm, w_gu, w_d, offsets, expert_map, E, d, f, R,
+                                        y_perm, act_save, ws, s);
+  return ffn_fwd_pipe<128, 512, 1, 4, 4>(x_perm, w_gu, w_d, offsets, expert_map, E, d, f, R, y_perm,
+                                      act_save, ws, s);
 }
 
 size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype) {

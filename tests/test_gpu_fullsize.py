@@ -82,10 +82,10 @@ def test_router_layer_full_size(name):
     plan.route(x, wr, bias=bias, renorm=w.renorm)
     plan.count()
     torch.cuda.synchronize()
-    ridx, rgate, margin, _ = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
-                                     renorm=w.renorm)
+    ridx, rgate, margin, rlog = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
+                                        renorm=w.renorm)
     idx = hint(plan.topk_idx)
-    n_diff, _ = check_routing(idx, hint(plan.topk_gate), ridx, rgate, margin, w.k)
+    n_diff, _ = check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k)
     print(f"  near-tie tokens routed differently: {n_diff} of {w.T}")
     rc, ro, rd = om.expert_counts(idx, w.E)
     np.testing.assert_array_equal(hint(plan.counts), rc)
@@ -103,10 +103,10 @@ def test_router_layer_full_size(name):
         np.testing.assert_array_equal(alive, ra)
         assert int(hint(plan.n_pruned)[0]) == rn
         print(f"  pruned {rn} of {w.E} experts (beta={w.prune_beta})")
-        ridx, rgate, margin, _ = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
-                                         alive=alive, renorm=w.renorm)
+        ridx, rgate, margin, rlog = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
+                                            alive=alive, renorm=w.renorm)
         idx = hint(plan.topk_idx)
-        check_routing(idx, hint(plan.topk_gate), ridx, rgate, margin, w.k)
+        check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k, alive)
         rc, ro, rd = om.expert_counts(idx, w.E)
         np.testing.assert_array_equal(hint(plan.counts), rc)
         np.testing.assert_array_equal(hint(plan.dest_row), rd)
