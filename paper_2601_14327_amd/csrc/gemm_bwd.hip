@@ -1,0 +1,527 @@
+// Backward grouped GEMMs of the SwiGLU expert FFN (moe_grouped_ffn_bwd) on
+// the gfx950 matrix cores:
+//   dgrad 1   dH = dY W_d[p]        (A = dY rows, K contiguous; B = W_d [K=d][N=f])
+//             -> SwiGLU backward epilogue at the saved pre-activations: dA, H_b
+//   dgrad 2   dX = dA W_gu[p]       (A = dA rows; B = W_gu [K=2f][N=d])
+//   wgrad     dW_d[p]  = dY^T H_b   (both operands [K = routed rows][features])
+//             dW_gu[p] = dA^T X     -> fp32 weight gradients, one tile per expert
+//             and output block, the reduction running over the expert's rows.
+//
+// Same pipeline as the forward kernels: 256 x 256 tiles, 8 waves (2 x 4),
+// k-tiles of 32 moved by LDS-DMA through NS stages, one barrier per k-tile.
+// Operands whose K is the strided global dimension are stored in LDS as
+// [32 k][256 features] rows (512 contiguous bytes per global row segment) and
+// turned into MFMA operands with ds_read_b64_tr_b16: within each 16-lane
+// group, lane j receives feature j of four consecutive k-rows, so two such
+// reads give a lane the same 8 consecutive k values a ds_read_b128 gives for
+// a K-contiguous operand.  The 32-byte block b of k-row r is stored at
+// b ^ ((r & 7) << 1), so the four k-rows a group reads fall in different
+// banks.  Rows past the end of an expert (the ragged reduction of the weight
+// gradient) are loaded from a zero page.
+#include "gemm_common.hpp"
+
+namespace laep {
+namespace {
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// One operand's LDS tile for one stage (32 k).
+//   TR == false: [ROWS][32] bf16, 64-byte rows, chunk c of row r at c ^ pswz(r)
+//   TR == true : [32][ROWS] bf16, 2*ROWS-byte rows, 32-byte block b of row r at
+//                b ^ ((r & 7) << 1)
+template <int ROWS, int NT, bool TR>
+struct OperandTile {
+  static constexpr int BYTES = ROWS * 64;
+  static constexpr int NC = ROWS * 4 / NT;    // 16-byte chunks per thread per stage
+  static constexpr int CPR = ROWS / 8;        // 16-byte chunks per k-row (TR)
+  static constexpr int RB = ROWS * 2;         // bytes per k-row (TR)
+  static_assert(!TR || ROWS == 256, "transposed tiles are 256 features wide");
+  static_assert((ROWS * 4) % NT == 0, "chunks must divide over the threads");
+};
+
+// LDS slot q of a TR tile -> (k-row, element column within the tile)
+__device__ __forceinline__ void tr_slot(int q, int cpr, int& r, int& col) {
+  r = q / cpr;
+  const int pc = q % cpr;
+  const int lblock = (pc >> 1) ^ ((r & 7) << 1);
+  col = lblock * 16 + (pc & 1) * 8;
+}
+
+// byte offset, within a TR tile, of the 8 bytes a lane reads in a
+// ds_read_b64_tr_b16 for k-row r (fragment column base mf, lane in group i,
+// group column half gh)
+__device__ __forceinline__ int tr_off(int r, int mf, int gh, int i) {
+  const int lblock = (mf >> 4) + gh;
+  return r * 512 + ((lblock ^ ((r & 7) << 1)) << 5) + ((i & 3) << 3);
+}
+
+__device__ __forceinline__ u32x4_t read_tr_frag(const char* st, int off1, int off2) {
+  const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(st + off1));
+  const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(st + off2));
+  const u32x2_t ua = __builtin_bit_cast(u32x2_t, a);
+  const u32x2_t ub = __builtin_bit_cast(u32x2_t, b);
+  u32x4_t v = {ua[0], ua[1], ub[0], ub[1]};
+  return v;
+}
+
+// One k-tile of LDS-DMA loads of one operand.  base[i] is chunk i's global
+// address at k-tile 0; kstep the element stride between k-tiles; for TR
+// operands rows at or past kvalid come from the zero page.
+template <int NC, int NT, bool TR>
+__device__ __forceinline__ void dma_operand(char* st, const bf16_t* const* base, const int* krow,
+                                            long long kstep, int kt, int kvalid,
+                                            const bf16_t* zero, int wave) {
+#pragma unroll
+  for (int i = 0; i < NC; ++i) {
+    const bf16_t* src = base[i] + kstep * kt;
+    if (TR && kt * 32 + krow[i] >= kvalid) src = zero;
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(st + (i * NT + wave * 64) * 16), 16, 0, 0);
+  }
+}
+
+template <int BM, int BN, int NWM, int NWN, int NS, int EPI, bool A_TR, bool B_TR>
+__global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) {
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int WTM = BM / NWM, WTN = BN / NWN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  using OA = OperandTile<BM, NT, A_TR>;
+  using OB = OperandTile<BN, NT, B_TR>;
+  constexpr int A_BYTES = OA::BYTES;
+  constexpr int STAGE = OA::BYTES + OB::BYTES;
+  constexpr int NLD = OA::NC + OB::NC;
+  static_assert(NS >= 3, "at least three stages");
+  static_assert(NWM == 2 && BM == 256, "the staged epilogues process one wave row per pass");
+  constexpr int PITCH16 = BN * 2 + 16;   // bf16 staging pitch
+  constexpr int PITCH32 = BN * 4 + 16;   // fp32 staging pitch
+  constexpr int EPI_BYTES = (EPI == EPI_WGRAD)  ? 128 * PITCH32
+                            : (EPI == EPI_GU_BWD) ? 3 * 64 * PITCH16
+                                                  : BM * PITCH16;
+  constexpr int SMEM = NS * STAGE > EPI_BYTES ? NS * STAGE : EPI_BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  // ---- tile schedule (XCD-contiguous) --------------------------------------
+  const int n_valid = (*p.n_entries) * p.tiles_per_entry;
+  const int per = (n_valid + 7) >> 3;
+  const int slot = blockIdx.x >> 3;
+  if (slot >= per) return;
+  const int L = (blockIdx.x & 7) * per + slot;
+  if (L >= n_valid) return;
+  const TileEntry te = p.table[L / p.tiles_per_entry];
+  const int rem = L % p.tiles_per_entry;
+  const int mt = (EPI == EPI_WGRAD) ? rem / p.n_tiles_n : 0;
+  const int nt = (EPI == EPI_WGRAD) ? rem % p.n_tiles_n : rem;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / NWN, wn = wave % NWN;
+
+  // reduction extent of this tile
+  const int kext = (EPI == EPI_WGRAD) ? te.rows : p.K;
+  const int nk = (kext + 31) / 32;
+
+  // ---- per-thread DMA sources ---------------------------------------------------
+  const bf16_t* a_base[OA::NC];
+  int a_krow[OA::NC];
+  long long a_kstep;
+#pragma unroll
+  for (int i = 0; i < OA::NC; ++i) {
+    const int q = i * NT + tid;
+    if (A_TR) {  // weight gradient: [routed rows][Mw], k = row, feature = mt*BM + col
+      int r, col;
+      tr_slot(q, OA::CPR, r, col);
+      int c = mt * BM + col;
+      c = c < p.Mw ? c : p.Mw - 8;  // columns past Mw: any valid column (not stored)
+      a_krow[i] = r;
+      a_base[i] = p.A + (long long)(te.row0 + r) * p.lda + c;
+    } else {     // data gradient: expert rows, K contiguous
+      const int r = q >> 2;
+      const int lc = (q & 3) ^ pswz(r);
+      const int rr = r < te.rows ? r : te.rows - 1;
+      a_krow[i] = 0;
+      a_base[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
+    }
+  }
+  a_kstep = A_TR ? 32LL * p.lda : 32LL;
+  const bf16_t* b_base[OB::NC];
+  int b_krow[OB::NC];
+  long long b_kstep;
+  const bf16_t* Bw = (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb
+                                        : p.B + (long long)te.phys * p.strideB;
+#pragma unroll
+  for (int i = 0; i < OB::NC; ++i) {
+    const int q = i * NT + tid;
+    if (B_TR) {  // [K][N] rows, feature = nt*BN + col (clamped to the last valid column block)
+      int r, col;
+      tr_slot(q, OB::CPR, r, col);
+      int c = nt * BN + col;
+      c = c < p.N ? c : p.N - 8;
+      b_krow[i] = r;
+      b_base[i] = Bw + (long long)r * p.ldb + c;
+    } else {
+      const int r = q >> 2;
+      const int lc = (q & 3) ^ pswz(r);
+      int row = nt * BN + r;
+      row = row < p.N ? row : p.N - 1;
+      b_krow[i] = 0;
+      b_base[i] = Bw + (long long)row * p.ldb + lc * 8;
+    }
+  }
+  b_kstep = B_TR ? 32LL * p.ldb : 32LL;
+  const int kvalid_a = A_TR ? kext : (1 << 30);
+  const int kvalid_b = (B_TR && EPI == EPI_WGRAD) ? kext : (1 << 30);
+
+  // ---- fragment offsets -------------------------------------------------------------
+  const int lc0 = lane >> 5;
+  const int gh = (lane >> 4) & 1;
+  const int li = lane & 15;
+  const int rk = (lane >> 5) * 8 + (li >> 2);  // first k-row of the lane's TR reads
+  int a_o1[TM], a_o2[TM], b_o1[TN], b_o2[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    if (A_TR) {
+      const int mf = wm * WTM + i * 32;
+      a_o1[i] = tr_off(rk, mf, gh, li);
+      a_o2[i] = tr_off(rk + 4, mf, gh, li);
+    } else {
+      const int r = wm * WTM + i * 32 + (lane & 31);
+      a_o1[i] = r * PROW + ((lc0 ^ pswz(r)) << 4);
+      a_o2[i] = 0;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    if (B_TR) {
+      const int mf = wn * WTN + j * 32;
+      b_o1[j] = A_BYTES + tr_off(rk, mf, gh, li);
+      b_o2[j] = A_BYTES + tr_off(rk + 4, mf, gh, li);
+    } else {
+      const int r = wn * WTN + j * 32 + (lane & 31);
+      b_o1[j] = A_BYTES + r * PROW + ((lc0 ^ pswz(r)) << 4);
+      b_o2[j] = 0;
+    }
+  }
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+
+  if (nk > 0) {
+    auto issue = [&](int kt) {
+      char* st = smem + (kt % NS) * STAGE;
+      const int kk = kt < nk ? kt : nk - 1;
+      dma_operand<OA::NC, NT, A_TR>(st, a_base, a_krow, a_kstep, kk, kvalid_a, p.zero, wave);
+      dma_operand<OB::NC, NT, B_TR>(st + A_BYTES, b_base, b_krow, b_kstep, kk, kvalid_b, p.zero,
+                                    wave);
+    };
+    // k16 step s of a stage: normal operands flip the logical chunk by 2
+    // (byte offset ^ 32 s); TR operands move down 16 k-rows (+ 16 * 512 s)
+    auto read_step = [&](const char* st, int s, u32x4_t* fa, u32x4_t* fb) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        if (A_TR) fa[i] = read_tr_frag(st, a_o1[i] + s * 8192, a_o2[i] + s * 8192);
+        else fa[i] = *reinterpret_cast<const u32x4_t*>(st + (a_o1[i] ^ (s << 5)));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        if (B_TR) fb[j] = read_tr_frag(st, b_o1[j] + s * 8192, b_o2[j] + s * 8192);
+        else fb[j] = *reinterpret_cast<const u32x4_t*>(st + (b_o1[j] ^ (s << 5)));
+      }
+    };
+    auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
+              0, 0, 0);
+    };
+#pragma unroll
+    for (int t = 0; t < NS - 1; ++t) issue(t);
+    wait_vmcnt<(NS - 2) * NLD>();
+    __builtin_amdgcn_s_barrier();
+    read_step(smem, 0, fa0, fb0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const char* st = smem + (kt % NS) * STAGE;
+      read_step(st, 1, fa1, fb1);
+      mma_step(fa0, fb0);
+      wait_vmcnt<(NS - 3) * NLD>();
+      __builtin_amdgcn_s_barrier();
+      issue(kt + NS - 1);
+      read_step(smem + ((kt + 1) % NS) * STAGE, 0, fa0, fb0);
+      mma_step(fa1, fb1);
+    }
+    wait_vmcnt<0>();
+  }
+
+  // ---- epilogues (staged through LDS) -------------------------------------------
+  wait_lgkm0();
+  __builtin_amdgcn_s_barrier();
+  const int lrow = lane & 31;
+  const int lcol = (lane >> 5) * 4;
+
+  if (EPI == EPI_WGRAD) {
+    // fp32 dW tile, 128 rows (one wave row) per pass
+    float* W = p.wout + (long long)te.phys * p.strideW;
+    const int ncols = min(BN, p.N - nt * BN);
+    for (int pass = 0; pass < 2; ++pass) {
+      if (wm == pass) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = i * 32 + lrow;
+              const int c = wn * WTN + j * 32 + q * 8 + lcol;
+              f32x4_t v = {acc[i][j][q * 4], acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2],
+                           acc[i][j][q * 4 + 3]};
+              *reinterpret_cast<f32x4_t*>(smem + r * PITCH32 + c * 4) = v;
+            }
+      }
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+      const int cpr = ncols / 4;
+      for (int c = tid; c < 128 * cpr; c += NT) {
+        const int r = c / cpr, cc = c % cpr;
+        const int row = mt * BM + pass * 128 + r;
+        if (row < p.Mw) {
+          f32x4_t v = *reinterpret_cast<const f32x4_t*>(smem + r * PITCH32 + cc * 16);
+          f32x4_t* dst = reinterpret_cast<f32x4_t*>(W + (long long)row * p.N + nt * BN + cc * 4);
+          if (p.accumulate) v += *dst;
+          *dst = v;
+        }
+      }
+      wait_lgkm0();
+      __builtin_amdgcn_s_barrier();
+    }
+  } else if (EPI == EPI_GU_BWD) {
+    // dH tile (columns = f-columns nt*BN ...), 64 rows per pass (half of one
+    // wave row).  Stage the saved pre-activations of those rows, compute
+    // dA_g, dA_u and H_b, and write all three back with whole-row stores.
+    const int f = p.f;
+    const int ncols = min(BN, f - nt * BN);
+    const int cpr = ncols / 8;
+    char* G = smem;
+    char* U = smem + 64 * PITCH16;
+    char* Hs = smem + 128 * PITCH16;
+    for (int pass = 0; pass < 4; ++pass) {
+      const int prow0 = pass * 64;
+      const int prows = min(64, te.rows - prow0);
+      for (int c = tid; c < 64 * cpr; c += NT) {  // stage A_g and A_u
+        const int r = c / cpr, cc = c % cpr;
+        if (r < prows) {
+          const bf16_t* src = p.aux + (long long)(te.row0 + prow0 + r) * 2 * f + nt * BN + cc * 8;
+          *reinterpret_cast<u32x4_t*>(G + r * PITCH16 + cc * 16) = *reinterpret_cast<const u32x4_t*>(src);
+          *reinterpret_cast<u32x4_t*>(U + r * PITCH16 + cc * 16) = *reinterpret_cast<const u32x4_t*>(src + f);
+        }
+      }
+      wait_lgkm0();
+      __syncthreads();
+      if (wm == (pass >> 1)) {
+        const int i0 = (pass & 1) * (TM / 2);
+#pragma unroll
+        for (int ii = 0; ii < TM / 2; ++ii)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int i = i0 + ii;
+              const int r = ii * 32 + lrow;
+              const int c = wn * WTN + j * 32 + q * 8 + lcol;
+              const u32x2_t gw = *reinterpret_cast<const u32x2_t*>(G + r * PITCH16 + c * 2);
+              const u32x2_t uw = *reinterpret_cast<const u32x2_t*>(U + r * PITCH16 + c * 2);
+              const float ag[4] = {lo_bf16(gw[0]), hi_bf16(gw[0]), lo_bf16(gw[1]), hi_bf16(gw[1])};
+              const float au[4] = {lo_bf16(uw[0]), hi_bf16(uw[0]), lo_bf16(uw[1]), hi_bf16(uw[1])};
+              float dag[4], dau[4], hb[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const float dh = acc[i][j][q * 4 + e];
+                const float s = fast_sigmoid(ag[e]);
+                const float sl = ag[e] * s;
+                dag[e] = dh * au[e] * s * (1.0f + ag[e] * (1.0f - s));
+                dau[e] = dh * sl;
+                hb[e] = sl * au[e];
+              }
+              u32x2_t wg = {pack_bf16x2(dag[0], dag[1]), pack_bf16x2(dag[2], dag[3])};
+              u32x2_t wu = {pack_bf16x2(dau[0], dau[1]), pack_bf16x2(dau[2], dau[3])};
+              u32x2_t wh = {pack_bf16x2(hb[0], hb[1]), pack_bf16x2(hb[2], hb[3])};
+              *reinterpret_cast<u32x2_t*>(G + r * PITCH16 + c * 2) = wg;
+              *reinterpret_cast<u32x2_t*>(U + r * PITCH16 + c * 2) = wu;
+              *reinterpret_cast<u32x2_t*>(Hs + r * PITCH16 + c * 2) = wh;
+            }
+      }
+      wait_lgkm0();
+      __syncthreads();
+      for (int c = tid; c < 64 * cpr; c += NT) {  // dA (gate and up halves) and H_b
+        const int r = c / cpr, cc = c % cpr;
+        if (r < prows) {
+          const long long row = te.row0 + prow0 + r;
+          bf16_t* dst = p.out + row * 2 * f + nt * BN + cc * 8;
+          *reinterpret_cast<u32x4_t*>(dst) = *reinterpret_cast<const u32x4_t*>(G + r * PITCH16 + cc * 16);
+          *reinterpret_cast<u32x4_t*>(dst + f) = *reinterpret_cast<const u32x4_t*>(U + r * PITCH16 + cc * 16);
+          *reinterpret_cast<u32x4_t*>(p.out2 + row * f + nt * BN + cc * 8) =
+              *reinterpret_cast<const u32x4_t*>(Hs + r * PITCH16 + cc * 16);
+        }
+      }
+      wait_lgkm0();
+      __syncthreads();
+    }
+  } else {  // EPI_STORE (bf16 rows, dX)
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = wn * WTN + j * 32 + q * 8 + lcol;
+          u32x2_t w = {pack_bf16x2(acc[i][j][q * 4], acc[i][j][q * 4 + 1]),
+                       pack_bf16x2(acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3])};
+          *reinterpret_cast<u32x2_t*>(smem + r * PITCH16 + c * 2) = w;
+        }
+    }
+    wait_lgkm0();
+    __syncthreads();
+    const int ncols = min(BN, p.N - nt * BN);
+    const int cpr = ncols / 8;
+    for (int c = tid; c < BM * cpr; c += NT) {
+      const int r = c / cpr, cc = c % cpr;
+      if (r < te.rows) {
+        bf16_t* dst = p.out + (long long)(te.row0 + r) * p.ldo + nt * BN + cc * 8;
+        *reinterpret_cast<u32x4_t*>(dst) = *reinterpret_cast<const u32x4_t*>(smem + r * PITCH16 + cc * 16);
+      }
+    }
+  }
+}
+
+// zero page for the ragged-K loads, and the tile tables
+__global__ void zero_page_kernel(uint32_t* z, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) z[i] = 0u;
+}
+
+constexpr int kBwdBM = 256, kBwdBN = 256;
+constexpr int kZeroBytes = 1024;
+
+template <int EPI, bool A_TR, bool B_TR>
+hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, 5, EPI, A_TR, B_TR>),
+                     dim3(round8(grid)), dim3(512), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype) {
+  const size_t elem = dtype == kDtypeBf16 ? 2 : 4;
+  return align_up((size_t)R * 2 * f * elem, 256);
+}
+
+size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
+  (void)d;
+  const size_t elem = dtype == kDtypeBf16 ? 2 : 4;
+  return ffn_bwd_hb_offset(R, f, dtype) + align_up((size_t)R * f * elem, 256) +
+         table_bytes(ceil_div(R, kBwdBM) + E) + table_bytes(E) + kZeroBytes;
+}
+
+hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
+                               const void* w_gu, const void* w_d, const int32_t* offsets,
+                               const int32_t* expert_map, int E, int d, int f, int64_t R,
+                               void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
+                               void* ws, hipStream_t s) {
+  char* base = static_cast<char*>(ws);
+  bf16_t* dA = reinterpret_cast<bf16_t*>(base);
+  bf16_t* Hb = reinterpret_cast<bf16_t*>(base + ffn_bwd_hb_offset(R, f, kDtypeBf16));
+  char* tables = base + ffn_bwd_hb_offset(R, f, kDtypeBf16) + align_up((size_t)R * f * 2, 256);
+  const int max_ragged = ceil_div(R, kBwdBM) + E;
+  TableWs tr = carve_table(tables, max_ragged);
+  TableWs te = carve_table(tables + table_bytes(max_ragged), E);
+  bf16_t* zero = reinterpret_cast<bf16_t*>(tables + table_bytes(max_ragged) + table_bytes(E));
+  hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
+                     E, kBwdBM, 0, max_ragged, tr.n_entries, tr.table);
+  hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
+                     E, kBwdBM, 1, E, te.n_entries, te.table);
+  hipLaunchKernelGGL(zero_page_kernel, dim3(1), dim3(256), 0, s, reinterpret_cast<uint32_t*>(zero),
+                     kZeroBytes / 4);
+
+  // dgrad 1: dH = dY W_d, SwiGLU backward epilogue -> dA, H_b
+  GemmParams g = {};
+  g.table = tr.table;
+  g.n_entries = tr.n_entries;
+  g.f = f;
+  g.zero = zero;
+  g.A = static_cast<const bf16_t*>(dy);
+  g.lda = d;
+  g.B = static_cast<const bf16_t*>(w_d);
+  g.ldb = f;
+  g.strideB = (long long)d * f;
+  g.N = f;
+  g.K = d;
+  g.n_tiles_n = ceil_div(f, kBwdBN);
+  g.tiles_per_entry = g.n_tiles_n;
+  g.out = dA;
+  g.out2 = Hb;
+  g.aux = static_cast<const bf16_t*>(act_save);
+  hipError_t err = launch_bwd<EPI_GU_BWD, false, true>(g, max_ragged * g.n_tiles_n, s);
+  if (err != hipSuccess) return err;
+
+  // dgrad 2: dX = dA W_gu
+  g.A = dA;
+  g.lda = 2 * f;
+  g.B = static_cast<const bf16_t*>(w_gu);
+  g.ldb = d;
+  g.strideB = (long long)2 * f * d;
+  g.N = d;
+  g.K = 2 * f;
+  g.n_tiles_n = ceil_div(d, kBwdBN);
+  g.tiles_per_entry = g.n_tiles_n;
+  g.out = static_cast<bf16_t*>(dx_perm);
+  g.ldo = d;
+  g.out2 = nullptr;
+  g.aux = nullptr;
+  err = launch_bwd<EPI_STORE, false, true>(g, max_ragged * g.n_tiles_n, s);
+  if (err != hipSuccess) return err;
+
+  // wgrad W_d: dW_d[p] [d, f] = dY^T H_b over the expert's rows
+  GemmParams w = {};
+  w.table = te.table;
+  w.n_entries = te.n_entries;
+  w.f = f;
+  w.zero = zero;
+  w.A = static_cast<const bf16_t*>(dy);
+  w.lda = d;
+  w.B = Hb;
+  w.ldb = f;
+  w.Mw = d;
+  w.N = f;
+  w.n_tiles_n = ceil_div(f, kBwdBN);
+  w.tiles_per_entry = ceil_div(d, kBwdBM) * w.n_tiles_n;
+  w.wout = dw_d;
+  w.strideW = (long long)d * f;
+  w.accumulate = accumulate;
+  err = launch_bwd<EPI_WGRAD, true, true>(w, E * w.tiles_per_entry, s);
+  if (err != hipSuccess) return err;
+
+  // wgrad W_gu: dW_gu[p] [2f, d] = dA^T X
+  w.A = dA;
+  w.lda = 2 * f;
+  w.B = static_cast<const bf16_t*>(x_perm);
+  w.ldb = d;
+  w.Mw = 2 * f;
+  w.N = d;
+  w.n_tiles_n = ceil_div(d, kBwdBN);
+  w.tiles_per_entry = ceil_div(2 * f, kBwdBM) * w.n_tiles_n;
+  w.wout = dw_gu;
+  w.strideW = (long long)2 * f * d;
+  return launch_bwd<EPI_WGRAD, true, true>(w, E * w.tiles_per_entry, s);
+}
+
+}  // namespace laep

@@ -1,0 +1,73 @@
+// Shared pieces of the grouped bf16 GEMM kernels (forward and backward).
+#pragma once
+
+#include "common.hpp"
+#include "internal.hpp"
+#include "tiles.hpp"
+
+namespace laep {
+namespace {
+
+enum { EPI_GU = 0, EPI_STORE = 1, EPI_GU_BWD = 2, EPI_WGRAD = 3 };
+
+struct GemmParams {
+  const bf16_t* A;
+  long long lda;
+  const bf16_t* B;
+  long long ldb;
+  long long strideB;  // elements between weight slots
+  int N;              // output columns
+  int K;              // reduction length (ragged-M products)
+  int Mw;             // output rows (wgrad)
+  int f;              // d_ff
+  const TileEntry* table;
+  const int* n_entries;
+  int tiles_per_entry;
+  int n_tiles_n;
+  bf16_t* out;
+  long long ldo;
+  bf16_t* out2;
+  const bf16_t* aux;
+  float* wout;
+  long long strideW;
+  int accumulate;
+  const bf16_t* zero;  // >= 1 KB of zeros (ragged-K tail loads of the weight gradient)
+};
+
+__device__ __forceinline__ void store_bf16x4(bf16_t* p, float a, float b, float c, float d) {
+  u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
+  *reinterpret_cast<u32x2_t*>(p) = w;
+}
+
+__device__ __forceinline__ void load_bf16x4(const bf16_t* p, float v[4]) {
+  const u32x2_t w = *reinterpret_cast<const u32x2_t*>(p);
+  v[0] = lo_bf16(w[0]);
+  v[1] = hi_bf16(w[0]);
+  v[2] = lo_bf16(w[1]);
+  v[3] = hi_bf16(w[1]);
+}
+
+constexpr int PBK = 32;          // k per pipeline stage
+constexpr int PROW = PBK * 2;    // bytes per LDS row
+
+__device__ __forceinline__ int pswz(int row) { return (row >> 2) & 3; }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt lgkmcnt(0) only (vmcnt field at its maximum, 63)
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+
+inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+inline int round8(int v) { return (v + 7) & ~7; }
+
+}  // namespace
+}  // namespace laep
