@@ -100,12 +100,22 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   constexpr int SMEM = NS * STAGE > EPI_BYTES ? NS * STAGE : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
-  // ---- tile schedule (XCD-contiguous) --------------------------------------
+  // ---- tile schedule --------------------------------------------------------
+  // Row-tile products: tiles of one expert share weight blocks, so each XCD
+  // takes a contiguous range of the table.  Weight gradients: the table is
+  // ordered longest expert first and tile costs follow the expert's rows, so
+  // the tiles of each expert are dealt round-robin over the XCDs (block i
+  // runs on XCD i % 8) to keep the eight XCDs equally loaded.
   const int n_valid = (*p.n_entries) * p.tiles_per_entry;
-  const int per = (n_valid + 7) >> 3;
-  const int slot = blockIdx.x >> 3;
-  if (slot >= per) return;
-  const int L = (blockIdx.x & 7) * per + slot;
+  int L;
+  if (EPI == EPI_WGRAD) {
+    L = blockIdx.x;
+  } else {
+    const int per = (n_valid + 7) >> 3;
+    const int slot = blockIdx.x >> 3;
+    if (slot >= per) return;
+    L = (blockIdx.x & 7) * per + slot;
+  }
   if (L >= n_valid) return;
   const TileEntry te = p.table[L / p.tiles_per_entry];
   const int rem = L % p.tiles_per_entry;
