@@ -1,11 +1,11 @@
 // Router scoring and top-k gating (moe_route).
 //
-// One workgroup of 256 threads handles 32 tokens.
+// One workgroup of 512 threads handles 32 tokens.
 //  1. logits[32 x EP] = x_tile . W_r^T on the matrix cores.  The reduction
-//     dimension is split over the 4 waves (16-wide k-steps dealt round
-//     robin); each wave holds a 32 x 32 fp32 block per 32 experts.  The four
-//     partial blocks are summed through LDS in wave order, so the result is
-//     deterministic.
+//     dimension is split over the 8 waves (chunks of consecutive 16-wide
+//     k-steps dealt round robin); each wave holds a 32 x 32 fp32 block per 32
+//     experts.  The eight partial blocks are summed through LDS in wave
+//     order, so the result is deterministic.
 //  2. top-k: 8 lanes per token, each lane owning experts e = 8q + lane.  k
 //     passes of a (value desc, index asc) arg-max across the 8 lanes.  The
 //     slot order is descending logit, ties to the lower expert index.
@@ -18,7 +18,9 @@ namespace laep {
 namespace {
 
 constexpr int kRouteTokens = 32;
-constexpr int kRouteThreads = 256;
+constexpr int kRouteWaves = 8;
+constexpr int kRouteThreads = 64 * kRouteWaves;
+constexpr int kTopkThreads = 8 * kRouteTokens;  // 8 lanes per token
 
 // One k-step of the router GEMM for element type T.
 //   bf16: 16 k per step; lane loads 8 consecutive k (16 bytes) of its row.
@@ -90,20 +92,33 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   const bool tok_ok = tok < n_tok;
   const T* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
   const int n_steps = (d + Step::kK - 1) / Step::kK;
-  for (int s = wave; s < n_steps; s += 4) {
-    const int kk = s * Step::kK + kh * Step::kLaneK;
-    const bool k_ok = kk < d;  // d % 8 == 0: a lane's k-group is all in or all out
-    u32x4_t a = load16_or_zero(xrow + kk, tok_ok && k_ok);
+  // The reduction is cut into chunks of U consecutive k-steps dealt round
+  // robin to the waves.  A chunk's loads are all issued before its MFMAs,
+  // so each wave keeps U row loads of x in flight (the router GEMM is
+  // bound by reading x once from HBM).
+  constexpr int U = NB >= 8 ? 2 : (NB >= 4 ? 4 : 8);
+  for (int c = wave; c * U < n_steps; c += kRouteWaves) {
+    u32x4_t a[U];
+    u32x4_t b[U][NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int e = nb * 32 + row;
-      u32x4_t b = load16_or_zero(w + (size_t)(e < E ? e : 0) * d + kk, k_ok && e < E);
-      Step::mma(acc[nb], a, b);
+    for (int i = 0; i < U; ++i) {
+      const int kk = (c * U + i) * Step::kK + kh * Step::kLaneK;
+      const bool k_ok = kk < d;  // d % 8 == 0: a lane's k-group is all in or all out
+      a[i] = load16_or_zero(xrow + kk, tok_ok && k_ok);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int e = nb * 32 + row;
+        b[i][nb] = load16_or_zero(w + (size_t)(e < E ? e : 0) * d + kk, k_ok && e < E);
+      }
     }
+#pragma unroll
+    for (int i = 0; i < U; ++i)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) Step::mma(acc[nb], a[i], b[i][nb]);
   }
 
   // acc[nb][r]: token (r/4)*8 + kh*4 + r%4, expert nb*32 + row.
-  for (int wv = 0; wv < 4; ++wv) {
+  for (int wv = 0; wv < kRouteWaves; ++wv) {
     __syncthreads();
     if (wave == wv) {
 #pragma unroll
@@ -133,14 +148,15 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     }
   }
 
-  // ---- 2. top-k -------------------------------------------------------------
-  const int ti = tid >> 3;  // token within the tile
-  const int g = tid & 7;    // lane within the token's group of 8
+  // ---- 2. top-k (the first 256 threads; the others idle through it) -----------
+  const bool tk = tid < kTopkThreads;
+  const int ti = tk ? (tid >> 3) : 0;  // token within the tile
+  const int g = tid & 7;               // lane within the token's group of 8
   float v[EPL];
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
     const int e = q * 8 + g;
-    v[q] = s_alive[e] ? s_log[ti * LD + e] : -INFINITY;
+    v[q] = (tk && s_alive[e]) ? s_log[ti * LD + e] : -INFINITY;
   }
   __syncthreads();  // s_log is reused below for the gate numerators
 
@@ -162,7 +178,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
 
   float* s_ex = s_log;  // [32][k] gate numerators (k <= E <= EP < LD)
   const int t_glob = t0 + ti;
-  const bool write_ok = t_glob < n_tok;
+  const bool write_ok = tk && t_glob < n_tok;
   float s_sel = 0.0f;
   for (int j = 0; j < k; ++j) {
     float bv = -INFINITY;
@@ -186,7 +202,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     }
     const float ex = found ? expf(bv - vmax) : 0.0f;
     s_sel += ex;
-    if (g == 0) {
+    if (tk && g == 0) {
       s_ex[ti * k + j] = ex;
       if (write_ok) idx_out[(size_t)t_glob * k + j] = found ? be : -1;
     }

@@ -50,15 +50,34 @@ __global__ __launch_bounds__(kRowThreads) void combine_kernel(
     float acc[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
-    for (int j = 0; j < k; ++j) {
-      const size_t s = (size_t)t * k + j;
-      const int r = dest_row[s];
-      if (r < 0) continue;
-      const float g = GATED ? gate[s] : 1.0f;
-      float val[8];
-      Elem<T>::load8(y + (size_t)r * d + (size_t)v * 8, val);
+    // slots in groups of 8: every row load of a group is issued before the
+    // sums, which still run in slot order
+    for (int j0 = 0; j0 < k; j0 += 8) {
+      int r[8];
+      float g[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) acc[q] += g * val[q];
+      for (int q = 0; q < 8; ++q) {
+        const int j = j0 + q;
+        const size_t s = (size_t)t * k + j;
+        r[q] = j < k ? dest_row[s] : -1;
+        g[q] = (GATED && j < k) ? gate[s] : 1.0f;
+      }
+      float val[8][8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (r[q] >= 0) {
+          Elem<T>::load8(y + (size_t)r[q] * d + (size_t)v * 8, val[q]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) val[q][e] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (r[q] >= 0) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] += g[q] * val[q][e];
+        }
     }
     Elem<T>::store8(out + (size_t)t * d + (size_t)v * 8, acc);
   }

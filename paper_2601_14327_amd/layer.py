@@ -26,7 +26,8 @@ from ._lib import LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD
 
 class MoELayerPlan:
     def __init__(self, T: int, d_model: int, E: int, k: int, d_ff: int,
-                 dtype: torch.dtype = torch.bfloat16, device="cuda", backward: bool = False):
+                 dtype: torch.dtype = torch.bfloat16, device="cuda", backward: bool = False,
+                 save_act: Optional[bool] = None):
         self.T, self.d, self.E, self.k, self.f = T, d_model, E, k, d_ff
         self.R = T * k
         self.dtype = dtype
@@ -43,7 +44,10 @@ class MoELayerPlan:
         self.n_pruned = torch.empty(1, dtype=i32, device=dev)
         self.x_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
         self.y_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
-        self.act_save = torch.empty((R, 2 * d_ff), dtype=dtype, device=dev)
+        # pre-activations are kept when a backward pass will read them (or on request)
+        save_act = backward if save_act is None else save_act
+        self.act_save = (torch.empty((R, 2 * d_ff), dtype=dtype, device=dev) if save_act
+                         else None)
         self.out = torch.empty((T, d_model), dtype=dtype, device=dev)
         self.ws_counts = torch.empty(max(1, api.workspace_bytes(LAEP_CALL_COUNTS, T, k, E)),
                                      dtype=torch.uint8, device=dev)

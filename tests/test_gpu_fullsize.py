@@ -68,7 +68,8 @@ def _check_combine_tokens(plan, toks):
 def _routed_plan(name):
     w = WORKLOADS[name]
     c = cached(name)
-    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda")
+    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda",
+                             save_act=True)
     x, wr = dev(c["x"], BF), dev(c["w_router"], BF)
     wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
     bias = dev(c["bias"], torch.float32) if "bias" in c else None
@@ -130,7 +131,7 @@ def _shard_plan(name, backward=False):
     w = WORKLOADS[name]
     c = cached(name)
     plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda",
-                             backward=backward)
+                             backward=backward, save_act=True)
     x = dev(c["x"], BF)
     wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
     idx = dev(c["topk_idx"], torch.int32)

@@ -310,8 +310,8 @@ def test_determinism():
     args = (dev(c["x"], bf), dev(c["w_router"], bf), dev(c["w_gate_up"], bf),
             dev(c["w_down"], bf))
     case("determinism")
-    p1 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda")
-    p2 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda")
+    p1 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda", save_act=True)
+    p2 = laep.MoELayerPlan(1500, 512, 64, 8, 256, dtype=bf, device="cuda", save_act=True)
     o1 = p1.forward(*args).clone()
     o2 = p2.forward(*args)
     torch.cuda.synchronize()
