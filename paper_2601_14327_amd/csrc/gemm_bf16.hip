@@ -17,24 +17,20 @@
 // Workgroup ids are remapped so that each of the 8 XCDs walks a contiguous
 // range of tiles (same expert, same weight blocks -> its own L2).
 //
-// Two main loops share the epilogues:
-//  * ring (default): k-steps of 64, so every row segment a step loads is one
-//    whole 128-byte line.  The L2 -> CU feed is bound by cache-line requests
-//    (about half a line per clock per CU, measured with LDS-DMA), so whole
-//    lines double the bytes per request against 64-byte half lines.  One
-//    operand's k-step is a 32 KB "half"; the LDS is a ring of five halves
-//    (A0 B0 A1 B1 A2 | B2 A3 ...), so while step i computes, the B half of
-//    step i+1 and the A half of step i+2 are in flight: every half has at
-//    least one whole k-step (2048 MFMA cycles per SIMD) to land.
-//  * pipe: k-tiles of 32 (64-byte rows), five 32 KB stages.
+// Main loop: 256 x 256 tiles, 8 waves (2 x 4, each 128 x 64), k-steps of 64,
+// so every row segment a step loads is one whole 128-byte line.  The L2 -> CU
+// feed is bound by cache-line requests (about half a line per clock per CU,
+// measured with LDS-DMA), so whole lines double the bytes per request against
+// the 64-byte half lines of 32-wide k-steps.  One operand's k-step is a 32 KB
+// "half"; the LDS is a ring of five halves (A0 B0 A1 B1 A2 | B2 A3 ...), so
+// while step i computes, the B half of step i+1 and the A half of step i+2
+// are in flight: every half has at least one whole k-step (2048 MFMA cycles
+// per SIMD) to land.
 #include "common.hpp"
 #include "internal.hpp"
 #include "tiles.hpp"
 #include "gemm_common.hpp"
 
-#include <cstdlib>
-#include <cstring>
-#include <type_traits>
 
 namespace laep {
 namespace {
@@ -48,17 +44,6 @@ __device__ __forceinline__ void dma_chunks(char* dst, const bf16_t* const* src, 
   for (int i = 0; i < NC; ++i)
     __builtin_amdgcn_global_load_lds(src[i] + k0, (lds_void_t*)(dst + (i * NT + wave * 64) * 16),
                                      16, 0, 0);
-}
-
-// The same for chunk i at row row_of(i) of a row-major operand (base already
-// offset to this thread's column).
-template <int NC, int NT, class RowOf>
-__device__ __forceinline__ void dma_rows(char* dst, const bf16_t* base, long long ld, int wave,
-                                         RowOf row_of) {
-#pragma unroll
-  for (int i = 0; i < NC; ++i)
-    __builtin_amdgcn_global_load_lds(base + (long long)row_of(i) * ld,
-                                     (lds_void_t*)(dst + (i * NT + wave * 64) * 16), 16, 0, 0);
 }
 
 // s_waitcnt vmcnt(N) lgkmcnt(0)
@@ -345,461 +330,12 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
 }
 
 // ---------------------------------------------------------------------------
-// Persistent ring: one workgroup per CU walks its tiles with the ring of
-// halves running on across tile boundaries, so the first k-steps of the next
-// tile load while the current tile finishes and writes out.  The epilogue
-// stages the output in the two halves the tile's last k-step released (64 KB,
-// in passes) and refills them only after its last LDS read; its global
-// stores then drain while the next tile computes.
-// ---------------------------------------------------------------------------
-// LDS address of byte b of staged row r, rows of RB bytes spread over two
-// 32 KB halves; 16-byte chunks XOR-swizzled by the row so that the 32 rows a
-// staging instruction writes fall in different banks.
-template <int RB>
-__device__ __forceinline__ char* staged(char* s0, char* s1, int r, int b) {
-  constexpr int RPS = 32768 / RB;  // rows per half
-  char* base = r < RPS ? s0 : s1;
-  const int rr = r < RPS ? r : r - RPS;
-  return base + rr * RB + ((((b >> 4) ^ (rr & 15))) << 4) + (b & 15);
-}
-
-template <int EPI, bool SAVE>
-__device__ __forceinline__ void persist_epilogue(const GemmParams& p, const TileEntry& te, int nt,
-                                                 f32x16_t (&acc)[4][2], char* s0, char* s1) {
-  constexpr int NT = 512, WTM = 128, WTN = 64, TM = 4, TN = 2, NWN = 4, BN = 256;
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave / NWN, wn = wave % NWN;
-  const int lrow = lane & 31;
-  const int lcol = (lane >> 5) * 4;
-  // staged rows [0, nrows) of RB bytes -> dst + (row0_out + r) * ld, bytes
-  // [b0, b0 + nbytes) of each staged row; rows past the expert are skipped
-  auto flush = [&](auto rb_tag, int nrows, int row0_out, bf16_t* dst, long long ld, int b0,
-                   int nbytes) {
-    constexpr int RB = decltype(rb_tag)::value;
-    const int cpr = nbytes >> 4;
-    for (int c = tid; c < nrows * cpr; c += NT) {
-      const int r = c / cpr, cc = c % cpr;
-      if (row0_out + r < te.rows) {
-        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(staged<RB>(s0, s1, r, b0 + cc * 16));
-        *reinterpret_cast<u32x4_t*>(dst + (long long)(te.row0 + row0_out + r) * ld + cc * 8) = v;
-      }
-    }
-  };
-  auto put = [&](auto rb_tag, int r, int col, float a, float b, float c, float d) {
-    constexpr int RB = decltype(rb_tag)::value;
-    u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
-    *reinterpret_cast<u32x2_t*>(staged<RB>(s0, s1, r, col * 2)) = w;
-  };
-  using R256 = std::integral_constant<int, 256>;
-  using R512 = std::integral_constant<int, 512>;
-  auto sync = [&]() {
-    wait_lgkm0();
-    __builtin_amdgcn_s_barrier();
-  };
-  if (EPI == EPI_GU) {
-    const int f = p.f;
-    const int fbase = nt * (BN / 2);
-    const int fcols = min(BN / 2, f - fbase);
-    if (SAVE) {  // act_save: the gate block, then the up block (256 rows x 128 columns)
-      auto save = [&](auto g_tag) {
-        constexpr int g = decltype(g_tag)::value;
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int pp = 0; pp < TN / 2; ++pp) {
-            const int grp = (wn * WTN) / 64 + pp;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              put(R256{}, wm * WTM + i * 32 + lrow, grp * 32 + q * 8 + lcol,
-                  acc[i][2 * pp + g][q * 4], acc[i][2 * pp + g][q * 4 + 1],
-                  acc[i][2 * pp + g][q * 4 + 2], acc[i][2 * pp + g][q * 4 + 3]);
-          }
-        sync();
-        flush(R256{}, 256, 0, p.out2 + g * f + fbase, 2LL * f, 0, fcols * 2);
-        sync();
-      };
-      save(std::integral_constant<int, 0>{});
-      save(std::integral_constant<int, 1>{});
-    }
-    // H = silu(gate) * up: 256 rows x 128 columns
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int pp = 0; pp < TN / 2; ++pp) {
-        const int grp = (wn * WTN) / 64 + pp;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float h[4];
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-            h[c] = fast_silu(acc[i][2 * pp][q * 4 + c]) * acc[i][2 * pp + 1][q * 4 + c];
-          put(R256{}, wm * WTM + i * 32 + lrow, grp * 32 + q * 8 + lcol, h[0], h[1], h[2], h[3]);
-        }
-      }
-    sync();
-    flush(R256{}, 256, 0, p.out + fbase, f, 0, fcols * 2);
-    sync();
-  } else {  // 256 x 256 bf16, one wave row (128 rows) per pass
-    const int ncols = min(BN, p.N - nt * BN);
-    for (int pass = 0; pass < 2; ++pass) {
-      if (wm == pass) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              put(R512{}, i * 32 + lrow, wn * WTN + j * 32 + q * 8 + lcol, acc[i][j][q * 4],
-                  acc[i][j][q * 4 + 1], acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
-      }
-      sync();
-      flush(R512{}, 128, pass * 128, p.out + nt * BN, p.ldo, 0, ncols * 2);
-      sync();
-    }
-  }
-}
-
-template <int EPI, bool GU_ROWS, bool SAVE>
-__global__ __launch_bounds__(512) void gemm_nt_persist_kernel(GemmParams p) {
-  constexpr int BM = 256, BN = 256, NWM = 2, NWN = 4;
-  constexpr int NT = 64 * NWM * NWN;
-  constexpr int WTM = BM / NWM, WTN = BN / NWN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int ROWB = 128;
-  constexpr int HALF = BM * ROWB;
-  constexpr int NSLOT = 5;
-  constexpr int NH = BM * 8 / NT;
-  static_assert(TM == 4 && TN == 2, "persist_epilogue assumes 4 x 2 blocks per wave");
-  __shared__ __attribute__((aligned(1024))) char smem[NSLOT * HALF];
-
-  // XCD-contiguous schedule: XCD x = blockIdx % 8 owns tiles [x*per, (x+1)*per);
-  // its G workgroups take them with stride G.
-  const int n_valid = (*p.n_entries) * p.tiles_per_entry;
-  const int per = (n_valid + 7) >> 3;
-  const int G = gridDim.x >> 3;
-  const int xcd = blockIdx.x & 7, g0 = blockIdx.x >> 3;
-  auto tile_id = [&](int j) {
-    const int sl = g0 + j * G;
-    const int L = xcd * per + sl;
-    return (sl < per && L < n_valid) ? L : -1;
-  };
-  if (tile_id(0) < 0) return;
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave / NWN, wn = wave % NWN;
-  const int nk = p.K / 64;
-
-  // ---- producer: the stream of halves over this workgroup's tiles --------------
-  // Chunk i of a half is row r = 64 i + tid / 8 of the tile, logical chunk
-  // (tid % 8) ^ swz8(r) (swz8 does not depend on i).  Only the producer
-  // tile's (uniform) entry is kept; each issue recomputes the addresses.
-  int pj = 0, ph = 0, gslot = 0;
-  bool p_live = true;
-  TileEntry pte = p.table[tile_id(0) / p.tiles_per_entry];
-  int pnt = tile_id(0) % p.tiles_per_entry;
-  const int t8 = tid >> 3;
-  const int lc8 = ((tid & 7) ^ swz8(t8)) * 8;
-  // Every call issues NH loads (past the last tile, a valid half is loaded
-  // again into a released slot and never read), so one constant vmcnt serves
-  // every wait.
-  auto issue_half = [&]() {
-    char* dst = smem + gslot * HALF;
-    const int k0 = (p_live ? (ph >> 1) * 64 : 0) + lc8;
-    if (ph & 1) {
-      const bf16_t* Bw = p.B + (long long)pte.phys * p.strideB + k0;
-      dma_rows<NH, NT>(dst, Bw, p.ldb, wave, [&](int i) {
-        return weight_row<BN, GU_ROWS>(p, pnt, i * 64 + t8);
-      });
-    } else {
-      const bf16_t* Ab = p.A + (long long)pte.row0 * p.lda + k0;
-      dma_rows<NH, NT>(dst, Ab, p.lda, wave, [&](int i) {
-        const int r = i * 64 + t8;
-        return r < pte.rows ? r : pte.rows - 1;
-      });
-    }
-    gslot = gslot + 1 == NSLOT ? 0 : gslot + 1;
-    if (p_live && ++ph == 2 * nk) {
-      ph = 0;
-      const int L = tile_id(++pj);
-      if (L >= 0) {
-        pte = p.table[L / p.tiles_per_entry];
-        pnt = L % p.tiles_per_entry;
-      } else {
-        p_live = false;
-      }
-    }
-  };
-
-  // ---- consumer --------------------------------------------------------------
-  int a_off[TM], b_off[TN];
-  const int lc0 = lane >> 5;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = wm * WTM + i * 32 + (lane & 31);
-    a_off[i] = r * ROWB + ((lc0 ^ swz8(r)) << 4);
-  }
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int r = wn * WTN + j * 32 + (lane & 31);
-    b_off[j] = r * ROWB + ((lc0 ^ swz8(r)) << 4);
-  }
-  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-  auto read_frags = [&](const char* sa, const char* sb, int s, u32x4_t* fa, u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      fa[i] = *reinterpret_cast<const u32x4_t*>(sa + (a_off[i] ^ (s << 5)));
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      fb[j] = *reinterpret_cast<const u32x4_t*>(sb + (b_off[j] ^ (s << 5)));
-  };
-  f32x16_t acc[TM][TN];
-  auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
-            0, 0, 0);
-  };
-  auto interleave = [&]() {
-#pragma unroll
-    for (int i = 0; i < TM + TN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - TM - TN, 0);
-  };
-  auto next_slot = [](int s) { return s + 1 == NSLOT ? 0 : s + 1; };
-
-#pragma unroll 1
-  for (int h = 0; h < NSLOT; ++h) issue_half();
-  wait_vmcnt<3 * NH>();
-  __builtin_amdgcn_s_barrier();
-  int cslot = 0;  // slot of the current k-step's A half (B is the next slot)
-
-  for (int j = 0;; ++j) {
-    const int L = tile_id(j);
-    if (L < 0) break;
-    const TileEntry te = p.table[L / p.tiles_per_entry];
-    const int nt = L % p.tiles_per_entry;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int jj = 0; jj < TN; ++jj)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][jj][r] = 0.0f;
-    read_frags(smem + cslot * HALF, smem + next_slot(cslot) * HALF, 0, fa0, fb0);
-    int ea = 0, eb = 0;
-    for (int kt = 0; kt < nk; ++kt) {
-      const char* sa = smem + cslot * HALF;
-      const char* sb = smem + next_slot(cslot) * HALF;
-      read_frags(sa, sb, 1, fa1, fb1);
-      mma_step(fa0, fb0);
-      interleave();
-      read_frags(sa, sb, 2, fa0, fb0);
-      mma_step(fa1, fb1);
-      interleave();
-      read_frags(sa, sb, 3, fa1, fb1);
-      mma_step(fa0, fb0);
-      interleave();
-      // the next k-step (possibly the next tile's first) has landed for every
-      // thread, and every wave's reads of this step are done
-      wait_vmcnt_lgkm0<NH>();
-      __builtin_amdgcn_s_barrier();
-      ea = cslot;
-      eb = next_slot(cslot);
-      cslot = next_slot(eb);
-      if (kt + 1 < nk) {
-        issue_half();
-        issue_half();
-        read_frags(smem + cslot * HALF, smem + next_slot(cslot) * HALF, 0, fa0, fb0);
-      }
-      mma_step(fa1, fb1);
-      interleave();
-    }
-    // the two halves of the last k-step stage the output, then refill
-    persist_epilogue<EPI, SAVE>(p, te, nt, acc, smem + ea * HALF, smem + eb * HALF);
-    if (tile_id(j + 1) < 0) break;
-    issue_half();
-    issue_half();
-  }
-  // no LDS-DMA may still be writing when the workgroup retires
-  wait_vmcnt<0>();
-}
-
-// ---------------------------------------------------------------------------
-// Pipe main loop: 256 x 256 tiles, 8 waves, k-tiles of 32 (64-byte LDS rows,
-// chunk c of row r at c ^ ((r >> 2) & 3): zero bank-conflict cycles measured),
-// NS stages in flight, one barrier per k-tile.
-// ---------------------------------------------------------------------------
-template <int NS, int EPI, bool GU_ROWS>
-__global__ __launch_bounds__(512) void gemm_nt_pipe_kernel(GemmParams p) {
-  constexpr int BM = 256, BN = 256, NWM = 2, NWN = 4;
-  constexpr int NT = 64 * NWM * NWN;
-  static_assert(NS >= 3, "at least three stages");
-  constexpr int WTM = BM / NWM, WTN = BN / NWN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int A_BYTES = BM * PROW, B_BYTES = BN * PROW;
-  constexpr int STAGE = A_BYTES + B_BYTES;
-  constexpr int NA = BM * 4 / NT, NB = BN * 4 / NT;  // 16-byte chunks per thread
-  constexpr int NLD = NA + NB;                        // loads per thread per k-tile
-  constexpr int NFR = TM + TN;                        // fragment reads per k16 step
-  constexpr int SMEM = (NS * STAGE > BM * (BN * 2 + 16)) ? NS * STAGE : BM * (BN * 2 + 16);
-  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-
-  const int L = xcd_tile(p);
-  if (L < 0) return;
-  const TileEntry te = p.table[L / p.tiles_per_entry];
-  const int nt = L % p.tiles_per_entry;
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave / NWN, wn = wave % NWN;
-
-  const bf16_t* a_src[NA];
-#pragma unroll
-  for (int i = 0; i < NA; ++i) {
-    const int q = i * NT + tid;
-    const int r = q >> 2;
-    const int lc = (q & 3) ^ pswz(r);
-    const int rr = r < te.rows ? r : te.rows - 1;
-    a_src[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
-  }
-  const bf16_t* Bw = p.B + (long long)te.phys * p.strideB;
-  const bf16_t* b_src[NB];
-#pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int q = i * NT + tid;
-    const int r = q >> 2;
-    const int lc = (q & 3) ^ pswz(r);
-    b_src[i] = Bw + (long long)weight_row<BN, GU_ROWS>(p, nt, r) * p.ldb + lc * 8;
-  }
-  auto issue = [&](int kt) {
-    char* st = smem + (kt % NS) * STAGE;
-    dma_chunks<NA, NT>(st, a_src, kt * PBK, wave);
-    dma_chunks<NB, NT>(st + A_BYTES, b_src, kt * PBK, wave);
-  };
-  int a_off[TM], b_off[TN];
-  const int lc0 = lane >> 5;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int r = wm * WTM + i * 32 + (lane & 31);
-    a_off[i] = r * PROW + ((lc0 ^ pswz(r)) << 4);
-  }
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int r = wn * WTN + j * 32 + (lane & 31);
-    b_off[j] = A_BYTES + r * PROW + ((lc0 ^ pswz(r)) << 4);
-  }
-  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-  auto read_frags = [&](const char* st, int flip, u32x4_t* fa, u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa[i] = *reinterpret_cast<const u32x4_t*>(st + (a_off[i] ^ flip));
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb[j] = *reinterpret_cast<const u32x4_t*>(st + (b_off[j] ^ flip));
-  };
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
-            0, 0, 0);
-  };
-  auto interleave = [&]() {
-#pragma unroll
-    for (int i = 0; i < NFR; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - NFR, 0);
-  };
-
-  const int nk = p.K / PBK;
-  // every iteration issues one k-tile of loads (past the end the last k-tile
-  // again, never read), so one constant vmcnt serves every wait
-#pragma unroll
-  for (int t = 0; t < NS - 1; ++t) issue(t < nk ? t : nk - 1);
-  wait_vmcnt<(NS - 2) * NLD>();
-  __builtin_amdgcn_s_barrier();
-  read_frags(smem, 0, fa0, fb0);
-  for (int kt = 0; kt < nk; ++kt) {
-    const char* st = smem + (kt % NS) * STAGE;
-    read_frags(st, 32, fa1, fb1);
-    mma_step(fa0, fb0);
-    interleave();
-    // tile kt+1 has landed for every thread, and every wave is done with
-    // stage (kt-1) % NS, which receives tile kt+NS-1
-    wait_vmcnt<(NS - 3) * NLD>();
-    __builtin_amdgcn_s_barrier();
-    {
-      const int t = kt + NS - 1;
-      issue(t < nk ? t : nk - 1);
-    }
-    read_frags(smem + ((kt + 1) % NS) * STAGE, 0, fa0, fb0);
-    mma_step(fa1, fb1);
-    interleave();
-  }
-  wait_vmcnt<0>();
-  wait_lgkm0();
-  __builtin_amdgcn_s_barrier();
-  fwd_epilogue<BM, BN, NWM, NWN, EPI>(p, te, nt, acc, smem);
-}
-
-// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-enum FwdLoop { LOOP_RING = 0, LOOP_PIPE = 1, LOOP_PERSIST = 2, LOOP_RING4 = 3 };
-
-// LAEP_GEMM_LOOP=pipe selects the k32 pipeline (for comparisons).
-FwdLoop pick_fwd_loop() {
-  static const char* env = getenv("LAEP_GEMM_LOOP");
-  if (env && strcmp(env, "pipe") == 0) return LOOP_PIPE;
-  if (env && strcmp(env, "persist") == 0) return LOOP_PERSIST;
-  if (env && strcmp(env, "ring4") == 0) return LOOP_RING4;
-  return LOOP_RING;
-}
-
-// compute units of the current device (one persistent workgroup each)
-int cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-      n = 256;
-    cached[dev] = (n / 8) * 8 > 0 ? (n / 8) * 8 : 8;
-  }
-  return cached[dev];
-}
-
 template <int EPI, bool GU>
-hipError_t launch_fwd(FwdLoop loop, const GemmParams& p, int grid, hipStream_t s) {
+hipError_t launch_fwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  if (loop == LOOP_PIPE)
-    hipLaunchKernelGGL((gemm_nt_pipe_kernel<5, EPI, GU>), dim3(round8(grid)), dim3(512), 0, s, p);
-  else if (loop == LOOP_PERSIST && p.out2)
-    hipLaunchKernelGGL((gemm_nt_persist_kernel<EPI, GU, EPI == EPI_GU>),
-                       dim3(min(round8(grid), cu_count())), dim3(512), 0, s, p);
-  else if (loop == LOOP_PERSIST)
-    hipLaunchKernelGGL((gemm_nt_persist_kernel<EPI, GU, false>),
-                       dim3(min(round8(grid), cu_count())), dim3(512), 0, s, p);
-  else if (loop == LOOP_RING4)
-    hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 2, EPI, GU>), dim3(round8(grid)), dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU>), dim3(round8(grid)), dim3(512), 0, s, p);
+  hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU>), dim3(round8(grid)), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 
@@ -818,7 +354,6 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
                                hipStream_t s) {
-  const FwdLoop loop = pick_fwd_loop();
   bf16_t* H = static_cast<bf16_t*>(ws);
   const int max_entries = ceil_div(R, kFwdBM) + E;
   TableWs tw = carve_table(static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256), max_entries);
@@ -841,7 +376,7 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.out = H;
   g.ldo = f;
   g.out2 = static_cast<bf16_t*>(act_save);
-  hipError_t err = launch_fwd<EPI_GU, true>(loop, g, max_entries * g.n_tiles_n, s);
+  hipError_t err = launch_fwd<EPI_GU, true>(g, max_entries * g.n_tiles_n, s);
   if (err != hipSuccess) return err;
   // down projection
   g.A = H;
@@ -856,7 +391,7 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.out = static_cast<bf16_t*>(y_perm);
   g.ldo = d;
   g.out2 = nullptr;
-  return launch_fwd<EPI_STORE, false>(loop, g, max_entries * g.n_tiles_n, s);
+  return launch_fwd<EPI_STORE, false>(g, max_entries * g.n_tiles_n, s);
 }
 
 }  // namespace laep
