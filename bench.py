@@ -4,22 +4,40 @@
 Default workload ("balanced"): T=8192 tokens, d_model=2048, 64 experts,
 top-8 renormalised softmax gating, SwiGLU d_ff=1024, bf16 with fp32
 accumulation.  One step = one forward pass of the whole layer:
-route -> expert counts -> permute -> grouped SwiGLU FFN -> combine.
+route -> expert counts -> permute -> grouped SwiGLU FFN -> combine, every
+call a kernel of the C-ABI library; three input sets rotate over the steps so
+the activations are not cache-resident.
 
 Prints ONE JSON line:
-  value      = tokens/s of the layer forward (inputs resident in HBM)
-  roofline   = the grouped SwiGLU FFN (its two bf16 MFMA GEMM launches) against
-               the bf16 dense MFMA peak, timed with HIP events on its stream
-  cpu_baseline = the CPU oracle timed on a bounded token sample
-Other workloads (--workload skewed | skewed_mild | shard | shard_bwd) are for
-profiling; the shard workloads report routed rows/s.
+  value        tokens/s of the whole step (wall clock over the timed steps,
+               inputs resident in HBM)
+  roofline     the dominant call (the grouped FFN) against the bf16 dense MFMA
+               peak; its duration comes from HIP events recorded around it on
+               its stream in every timed step.  `traffic` is the HBM bytes per
+               call from the committed rocprofv3 counter summary, reported only
+               while the kernel sources still match the ones it was taken on.
+  breakdown    every call: mean / median / p10 / p90 microseconds over the timed
+               steps and its rate on algorithmic bytes or flops
+  attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
+  cpu_baseline the float64 CPU oracle timed on a bounded token sample
+
+Other workloads: skewed, skewed_mild (routed, pruned), shard (16 experts,
+given Zipf routing), shard_bwd (shard forward + backward).
+
+Profiling helpers (used by the commands recorded under profiles/):
+  --profile-target ffn|copy   run only that call a few times (for --pmc runs)
+  --summarize-pmc DIR         turn FETCH_SIZE / WRITE_SIZE counter CSVs into the
+                              traffic summary (--out FILE)
+  --summarize-trace DIR       turn a --kernel-trace --stats run into a summary
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
-import math
 import os
+import re
 import sys
 import time
 
@@ -28,11 +46,28 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+CSRC = os.path.join(ROOT, "paper_2601_14327_amd", "csrc")
+# sources of the forward FFN's kernels (traffic counts are valid for these bits only)
+FFN_FWD_SOURCES = ["gemm_bf16.hip", "gemm_common.hpp", "tiles.hpp", "common.hpp"]
+FFN_BWD_SOURCES = ["gemm_bwd.hip", "gemm_common.hpp", "tiles.hpp", "common.hpp"]
+COPY_CALIB_BYTES = 1 << 32
+PROFILE_CALLS = 5
+PROFILES = os.path.join(ROOT, "profiles")
 
 
+def sources_sha(names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(CSRC, n), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------------------
+# CPU oracle baseline
+# ---------------------------------------------------------------------------------------
 def _cpu_baseline(w, c, budget_s: float):
     """Time the plain float64 oracle on a token sample of the same workload."""
-    import numpy as np
     import oracle.moe as om
 
     try:
@@ -65,130 +100,358 @@ def _cpu_baseline(w, c, budget_s: float):
     unit = "tokens/s" if w.routed else "rows/s"
     return {"value": n / dt, "unit": unit, "cores": threads, "kind": "oracle",
             "sample": f"{n} of {w.T} {'tokens' if w.routed else 'rows'} of the same workload, "
-                      f"full layer forward in float64 NumPy ({dt:.1f} s)"}
+                      f"layer forward in float64 NumPy ({dt:.1f} s)"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="balanced")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              f"expert-parallel path is not part of this build.", file=sys.stderr)
-        sys.exit(2)
+# ---------------------------------------------------------------------------------------
+# the layer step, call by call
+# ---------------------------------------------------------------------------------------
+class Setup:
+    def __init__(self, w, dev):
+        import numpy as np
+        import torch
 
-    import numpy as np
+        import paper_2601_14327_amd as laep
+        from workloads import cached
+
+        self.w, self.dev = w, dev
+        c = cached(w.name)
+        self.c = c
+        bf = torch.bfloat16
+        to = lambda a, dt=bf: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
+        rng = np.random.default_rng(0)
+        self.n_sets = 3
+        self.xs = [to(c["x"])] + [to(c["x"][rng.permutation(w.T)]) for _ in range(self.n_sets - 1)]
+        self.wgu, self.wd = to(c["w_gate_up"]), to(c["w_down"])
+        self.plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=bf, device=dev,
+                                      backward=w.backward)
+        if w.routed:
+            self.wr = to(c["w_router"])
+            self.bias = to(c["bias"], torch.float32) if "bias" in c else None
+        else:
+            self.idx = to(c["topk_idx"], torch.int32)
+            self.gate = to(c["topk_gate"], torch.float32)
+            self.dout = to(c["dout"]) if w.backward else None
+        self.laep = laep
+
+    def calls(self, i):
+        """(name, fn) for every call of step i, in order."""
+        w, p, L = self.w, self.plan, self.laep
+        x = self.xs[i % self.n_sets]
+        R = w.T * w.k
+        out = []
+        if w.routed:
+            route = lambda alive=None: L.moe_route(x, self.wr, w.k, bias=self.bias, alive=alive,
+                                                   renorm=w.renorm, topk_idx=p.topk_idx,
+                                                   topk_gate=p.topk_gate)
+            out += [("route", route), ("counts", p.count)]
+            if w.prune_beta is not None:
+                out += [("prune", lambda: p.prune(w.prune_beta, w.prune_alpha)),
+                        ("route_masked", lambda: route(p.alive)), ("counts_masked", p.count)]
+            gate = p.topk_gate
+        else:
+            out += [("counts", lambda: L.moe_expert_counts(self.idx, w.E, ws=p.ws_counts,
+                                                           counts=p.counts, offsets=p.offsets,
+                                                           dest_row=p.dest_row))]
+            gate = self.gate
+        out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm)),
+                ("ffn_fwd", lambda: L.moe_grouped_ffn_fwd(p.x_perm, self.wgu, self.wd, p.offsets,
+                                                          ws=p.ws_ffn, y_perm=p.y_perm,
+                                                          save_act=p.act_save is not None,
+                                                          act_save=p.act_save)),
+                ("combine", lambda: L.moe_combine(p.y_perm, gate, p.dest_row, out=p.out))]
+        if w.backward:
+            if p.dw_gate_up is None:
+                import torch
+                p.dw_gate_up = torch.empty(self.wgu.shape, dtype=torch.float32, device=self.dev)
+                p.dw_down = torch.empty(self.wd.shape, dtype=torch.float32, device=self.dev)
+            out += [("combine_bwd", lambda: L.moe_combine_bwd(self.dout, p.y_perm, gate,
+                                                              p.dest_row, dy_perm=p.dy_perm,
+                                                              dgate=p.dgate)),
+                    ("ffn_bwd", lambda: L.moe_grouped_ffn_bwd(
+                        p.dy_perm, p.x_perm, p.act_save, self.wgu, self.wd, p.offsets,
+                        dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,
+                        dx_perm=p.dx_perm)),
+                    ("permute_bwd", lambda: L.moe_permute_bwd(p.dx_perm, p.dest_row, w.T, w.k,
+                                                              out=p.dx))]
+        return out
+
+    def algorithmic(self):
+        """Algorithmic bytes (HBM-bound calls) or flops (matrix-core calls) per call."""
+        w = self.w
+        T, d, E, k, f = w.T, w.d_model, w.E, w.k, w.d_ff
+        R = T * k
+        e = 2  # bf16
+        by = {
+            "route": T * d * e + E * d * e + 2 * T * k * 4,
+            "counts": T * k * 4 + 2 * (E + 1) * 4 + R * 4,
+            "permute": T * d * e + R * d * e + R * 4,
+            "combine": R * d * e + T * d * e + 2 * R * 4,
+            "combine_bwd": T * d * e + 2 * R * d * e + 3 * R * 4,
+            "permute_bwd": R * d * e + T * d * e + R * 4,
+        }
+        by["route_masked"], by["counts_masked"] = by["route"], by["counts"]
+        fl = {"ffn_fwd": 6.0 * R * d * f, "ffn_bwd": 12.0 * R * d * f}
+        return by, fl
+
+
+def _stats(v):
+    v = sorted(v)
+    n = len(v)
+    pick = lambda q: v[min(n - 1, max(0, int(round(q * (n - 1)))))]
+    return {"mean_us": round(1e3 * sum(v) / n, 2), "median_us": round(1e3 * pick(0.5), 2),
+            "p10_us": round(1e3 * pick(0.1), 2), "p90_us": round(1e3 * pick(0.9), 2)}
+
+
+def _attainable(dev):
+    """A plain copy kernel and a bf16 MFMA loop, timed with events."""
     import torch
 
     import paper_2601_14327_amd as laep
-    from workloads import WORKLOADS, cached
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty(n, dtype=torch.uint8, device=dev)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    laep.laep_calib_copy(src, dst)
+    times = []
+    for _ in range(10):
+        s.record()
+        laep.laep_calib_copy(src, dst)
+        e.record()
+        torch.cuda.synchronize()
+        times.append(s.elapsed_time(e))
+    copy_gbs = 2 * n / (sorted(times)[len(times) // 2] * 1e-3) / 1e9
+    del src, dst
+    wg, iters = 256 * 4, 4096
+    out = torch.empty(wg * 512, dtype=torch.float32, device=dev)
+    laep.laep_calib_mfma(wg, 64, out)
+    s.record()
+    laep.laep_calib_mfma(wg, iters, out)
+    e.record()
+    torch.cuda.synchronize()
+    tf = wg * 8 * iters * 8 * 32768 / (s.elapsed_time(e) * 1e-3) / 1e12
+    return {"copy_GBs": round(copy_gbs, 1), "mfma_bf16_TFLOPs": round(tf, 1),
+            "copy_frac_of_peak": round(copy_gbs / PEAK_HBM_GBS, 3),
+            "mfma_frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 3)}
+
+
+def _traffic(name, sources):
+    """HBM bytes per call from the committed counter summary, if still valid."""
+    path = os.path.join(PROFILES, f"{name}_traffic.md")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), flags=re.S)
+    if not m:
+        return None, "summary has no data block"
+    rec = json.loads(m.group(1))
+    if rec.get("kernel_sources_sha256") != sources_sha(sources):
+        return None, "kernel changed since the counters were taken"
+    return rec["traffic_bytes_per_call"], os.path.relpath(path, ROOT)
+
+
+# ---------------------------------------------------------------------------------------
+# profiling helpers
+# ---------------------------------------------------------------------------------------
+def profile_target(args):
+    import torch
+
+    from workloads import WORKLOADS
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.profile_target == "copy":
+        import paper_2601_14327_amd as laep
+        src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev)
+        for _ in range(PROFILE_CALLS):
+            laep.laep_calib_copy(src, dst)
+        torch.cuda.synchronize()
+        print(f"profile target: laep_calib_copy of {COPY_CALIB_BYTES} bytes x {PROFILE_CALLS}",
+              flush=True)
+        return
+    import paper_2601_14327_amd as laep
+    su = Setup(WORKLOADS[args.workload], dev)
+    calls = dict(su.calls(0))
+    for name, fn in su.calls(0):       # one full step prepares every input
+        fn()
+    # marker dispatch: the counters of every dispatch after it belong to the target
+    marker = torch.empty(512, dtype=torch.float32, device=dev)
+    laep.laep_calib_mfma(1, 1, marker)
+    for _ in range(PROFILE_CALLS):
+        calls[args.profile_target]()
+    torch.cuda.synchronize()
+    print(f"profile target: {args.profile_target} x {PROFILE_CALLS} on {args.workload}",
+          flush=True)
+
+
+def _read_counters(d):
+    """[(dispatch id, kernel, counter, value)] from rocprofv3 counter CSVs."""
+    import csv
+    out = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            out.append((int(r["Dispatch_Id"]), r["Kernel_Name"], r["Counter_Name"],
+                        float(r["Counter_Value"])))
+    return out
+
+
+def _per_call(d, counter):
+    """Counter total per target call (dispatches after the marker) and per kernel."""
+    rows = [r for r in _read_counters(d) if r[2] == counter]
+    mark = max(r[0] for r in rows if "mfma_loop_kernel" in r[1])
+    tot, per_k = 0.0, {}
+    for did, k, _, v in rows:
+        if did > mark:
+            tot += v
+            name = re.sub(r"\(.*", "", k.replace("(anonymous namespace)::", ""))
+            per_k[name] = per_k.get(name, 0.0) + v / PROFILE_CALLS
+    return tot / PROFILE_CALLS, per_k
+
+
+def _per_copy(d, counter):
+    vals = [r[3] for r in _read_counters(d) if r[2] == counter and "copy_kernel" in r[1]]
+    return sum(vals) / len(vals)
+
+
+def summarize_pmc(args):
+    """Traffic summary of one call from four counter runs: DIR/call_fetch,
+    DIR/call_write (the call, PROFILE_CALLS times after a marker dispatch),
+    DIR/copy_fetch, DIR/copy_write (the calibration copy of COPY_CALIB_BYTES)."""
+    d = args.summarize_pmc
+    call = args.profile_call
+    srcs = FFN_FWD_SOURCES if call == "ffn_fwd" else FFN_BWD_SOURCES
+    copy_f = _per_copy(os.path.join(d, "copy_fetch"), "FETCH_SIZE")
+    copy_w = _per_copy(os.path.join(d, "copy_write"), "WRITE_SIZE")
+    k_fetch = COPY_CALIB_BYTES / copy_f     # bytes per counter unit, reads
+    k_write = COPY_CALIB_BYTES / copy_w     # bytes per counter unit, writes
+    ff, ffk = _per_call(os.path.join(d, "call_fetch"), "FETCH_SIZE")
+    fw, fwk = _per_call(os.path.join(d, "call_write"), "WRITE_SIZE")
+    fetch, write = ff * k_fetch, fw * k_write
+    rec = {"call": call, "workload": args.workload,
+           "kernel_sources_sha256": sources_sha(srcs),
+           "copy_calibration": {"bytes_read_and_written": COPY_CALIB_BYTES,
+                                "FETCH_SIZE": copy_f, "WRITE_SIZE": copy_w,
+                                "bytes_per_fetch_unit": k_fetch, "bytes_per_write_unit": k_write},
+           "FETCH_SIZE_per_call_by_kernel": ffk, "WRITE_SIZE_per_call_by_kernel": fwk,
+           "fetch_bytes_per_call": fetch, "write_bytes_per_call": write,
+           "traffic_bytes_per_call": fetch + write}
+    cmd = args.command_note or ""
+    text = (f"# HBM traffic of `{call}` on workload `{args.workload}`\n\n"
+            f"rocprofv3 counters FETCH_SIZE and WRITE_SIZE (one --pmc pass each), summed over "
+            f"the call's dispatches, each scaled by what the same counter reads for the "
+            f"library's plain copy kernel moving {COPY_CALIB_BYTES} bytes.\n\n"
+            f"- fetched: {fetch / 1e6:.1f} MB per call\n- written: {write / 1e6:.1f} MB per call\n"
+            f"- calibration: {k_fetch:.1f} bytes per FETCH_SIZE unit, {k_write:.1f} bytes per "
+            f"WRITE_SIZE unit\n\nCommands:\n\n```\n{cmd}\n```\n\n```json\n"
+            f"{json.dumps(rec, indent=1)}\n```\n")
+    with open(args.out, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
+def summarize_trace(args):
+    import csv
+    f = glob.glob(os.path.join(args.summarize_trace, "**", "*kernel_stats.csv"), recursive=True)[0]
+    rows = list(csv.DictReader(open(f)))
+    lines = [f"# Kernel time: {args.workload}\n", "rocprofv3 --kernel-trace --stats.\n",
+             "Commands:\n", f"```\n{args.command_note or ''}\n```\n",
+             "| kernel | calls | average (us) | min (us) | max (us) | share |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        name = re.sub(r"\(.*", "", r["Name"].replace("(anonymous namespace)::", ""))
+        lines.append(f"| `{name[:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f}% |")
+    text = "\n".join(lines) + "\n"
+    with open(args.out, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
+# ---------------------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="balanced")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-attainable", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--profile-target", choices=["ffn_fwd", "ffn_bwd", "copy", "route", "permute",
+                                                 "combine", "counts"])
+    ap.add_argument("--summarize-pmc")
+    ap.add_argument("--summarize-trace")
+    ap.add_argument("--profile-call", default="ffn_fwd")
+    ap.add_argument("--command-note")
+    ap.add_argument("--out")
+    args = ap.parse_args()
+    if args.summarize_pmc:
+        return summarize_pmc(args)
+    if args.summarize_trace:
+        return summarize_trace(args)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): this build has no "
+              f"multi-GPU expert-parallel path; the sharding design is described in DESIGN.md.",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.profile_target:
+        return profile_target(args)
+
+    import torch
+
+    from workloads import WORKLOADS
 
     w = WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    c = cached(w.name)
-    bf = torch.bfloat16
-    to = lambda a, dt=bf: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
-
-    # three input sets rotated per step so activations are not cache-resident
-    n_sets = 3
-    rng = np.random.default_rng(0)
-    xs = [to(c["x"])] + [to(c["x"][rng.permutation(w.T)]) for _ in range(n_sets - 1)]
-    wgu, wd = to(c["w_gate_up"]), to(c["w_down"])
-    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=bf, device=dev,
-                             backward=w.backward)
-    if w.routed:
-        wr = to(c["w_router"])
-        bias = to(c["bias"], torch.float32) if "bias" in c else None
-
-        def step(i):
-            return plan.forward(xs[i % n_sets], wr, wgu, wd, bias=bias, renorm=w.renorm,
-                                prune_beta=w.prune_beta, prune_alpha=w.prune_alpha)
-    else:
-        idx = to(c["topk_idx"], torch.int32)
-        gate = to(c["topk_gate"], torch.float32)
-        dout = to(c["dout"]) if w.backward else None
-
-        def step(i):
-            plan.forward_given_routing(xs[i % n_sets], idx, gate, wgu, wd)
-            if w.backward:
-                plan.backward(dout, wgu, wd)
+    su = Setup(w, dev)
+    stream = torch.cuda.current_stream(dev)
 
     for i in range(args.warmup):
-        step(i)
+        for _, fn in su.calls(i):
+            fn()
     torch.cuda.synchronize()
+    names = [n for n, _ in su.calls(0)]
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in names] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i)
+        for j, (_, fn) in enumerate(su.calls(i)):
+            ev[i][j][0].record(stream)
+            fn()
+            ev[i][j][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = wall * 1e3 / args.steps
 
-    # ---- the dominant kernel: grouped SwiGLU FFN, HIP events on its stream ----
-    stream = torch.cuda.current_stream(dev)
-    n_ev = max(10, args.steps)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(n_ev)]
-    for i in range(n_ev):
-        s, e = evs[i]
-        s.record(stream)
-        laep.moe_grouped_ffn_fwd(plan.x_perm, wgu, wd, plan.offsets, ws=plan.ws_ffn,
-                                 y_perm=plan.y_perm, act_save=plan.act_save)
-        e.record(stream)
-    torch.cuda.synchronize()
-    ffn_ms = sorted(s.elapsed_time(e) for s, e in evs)
-    ffn_ms_avg = sum(ffn_ms) / len(ffn_ms)
-    R = w.T * w.k
-    ffn_flops = 6.0 * R * w.d_model * w.d_ff
-    achieved = ffn_flops / (ffn_ms_avg * 1e-3) / 1e12
-
-    # ---- per-step breakdown (events around each call) -------------------------
+    by, fl = su.algorithmic()
     breakdown = {}
-    if w.routed:
-        x0 = xs[0]
-        parts = [("route", lambda: plan.route(x0, wr, bias=bias, renorm=w.renorm)),
-                 ("counts", lambda: plan.count()),
-                 ("permute", lambda: laep.moe_permute(x0, plan.dest_row, w.k, R,
-                                                      out=plan.x_perm)),
-                 ("combine", lambda: laep.moe_combine(plan.y_perm, plan.topk_gate,
-                                                      plan.dest_row, out=plan.out))]
-        for name, fn in parts:
-            es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(10)]
-            for s, e in es:
-                s.record(stream)
-                fn()
-                e.record(stream)
-            torch.cuda.synchronize()
-            breakdown[name + "_us"] = round(1e3 * sum(s.elapsed_time(e) for s, e in es) / 10, 2)
-        elem = 2
-        bytes_route = w.T * w.d_model * elem + w.E * w.d_model * elem + 2 * w.T * w.k * 4
-        bytes_perm = w.T * w.d_model * elem + R * w.d_model * elem + R * 4
-        breakdown["route_GBs"] = round(bytes_route / (breakdown["route_us"] * 1e-6) / 1e9, 1)
-        breakdown["permute_GBs"] = round(bytes_perm / (breakdown["permute_us"] * 1e-6) / 1e9, 1)
-        breakdown["combine_GBs"] = round(
-            (R * w.d_model * elem + w.T * w.d_model * elem + R * 8)
-            / (breakdown["combine_us"] * 1e-6) / 1e9, 1)
-    breakdown["ffn_us"] = round(ffn_ms_avg * 1e3, 2)
-    breakdown["ffn_TFLOPs"] = round(achieved, 1)
+    for j, n in enumerate(names):
+        st = _stats([ev[i][j][0].elapsed_time(ev[i][j][1]) for i in range(args.steps)])
+        if n in by:
+            st["GBs"] = round(by[n] / (st["mean_us"] * 1e-6) / 1e9, 1)
+            st["frac_hbm_peak"] = round(st["GBs"] / PEAK_HBM_GBS, 3)
+        if n in fl:
+            st["TFLOPs"] = round(fl[n] / (st["mean_us"] * 1e-6) / 1e12, 1)
+            st["frac_mfma_peak"] = round(st["TFLOPs"] / PEAK_BF16_TFLOPS, 3)
+        breakdown[n] = st
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = _cpu_baseline(w, c, args.cpu_budget)
+    # the dominant call: the grouped FFN (backward when the step has one)
+    dom = "ffn_bwd" if w.backward else "ffn_fwd"
+    dom_us = breakdown[dom]["mean_us"]
+    achieved = fl[dom] / (dom_us * 1e-6) / 1e12
+    traffic, traffic_src = _traffic(f"{dom}_{w.name}",
+                                    FFN_BWD_SOURCES if dom == "ffn_bwd" else FFN_FWD_SOURCES)
+    attain = None if args.no_attainable else _attainable(dev)
+    cpu = None if args.no_cpu_baseline else _cpu_baseline(w, su.c, args.cpu_budget)
 
     unit = "tokens/s" if w.routed else "rows/s"
-    per_step = w.T
     metric = ("MoE-layer tokens/s at 1 GPU; grouped-GEMM TFLOP/s as % bf16 MFMA peak"
               if w.routed else "MoE expert-shard routed rows/s at 1 GPU (fwd" +
               ("+bwd" if w.backward else "") + ")")
     line = {
         "metric": metric,
-        "value": per_step / (ms * 1e-3),
+        "value": w.T / (ms * 1e-3),
         "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
@@ -203,10 +466,16 @@ def main():
                                f"d_ff={w.d_ff} bf16" + (" fwd+bwd" if w.backward else " fwd"),
                    "tokens": w.T, "experts": w.E, "top_k": w.k, "d_model": w.d_model,
                    "d_ff": w.d_ff},
-        "roofline": {"bound": "mfma", "kernel": "grouped SwiGLU FFN fwd (gate/up + down GEMMs)",
+        "roofline": {"bound": "mfma",
+                     "kernel": f"{dom}: grouped SwiGLU FFN "
+                               f"({'dgrad + wgrad GEMMs' if dom == 'ffn_bwd' else 'gate/up + down GEMMs'}"
+                               f" and tile-table build), one C-ABI call",
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None},
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "traffic_source": traffic_src,
+                     "algorithmic_flops_per_call": fl[dom], "mean_call_us": dom_us},
         "cpu_baseline": cpu,
+        "attainable": attain,
         "breakdown": breakdown,
     }
     print(json.dumps(line), flush=True)

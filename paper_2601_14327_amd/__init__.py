@@ -11,10 +11,13 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     moe_combine          gate-weighted combine
     moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
     laep_rearrange       host utility: balanced expert placement
+    laep_calib_copy, laep_calib_mfma   measurement kernels (attained peaks)
 """
 from ._lib import LAEP_BF16, LAEP_F32, LaepError, LIB_PATH, lib  # noqa: F401
 from .api import (  # noqa: F401
     ffn_bwd_ws_views,
+    laep_calib_copy,
+    laep_calib_mfma,
     laep_prune_mask,
     laep_rearrange,
     moe_combine,

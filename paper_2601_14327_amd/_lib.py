@@ -60,6 +60,9 @@ SIGNATURES = {
     "moe_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "laep_rearrange": (_i, [_p, _i, _i, _p, _p, _p]),
     "laep_last_error": (ctypes.c_char_p, []),
+    # measurement kernels (laep_calib.h)
+    "laep_calib_copy": (_i, [_p, _p, _sz, _p]),
+    "laep_calib_mfma": (_i, [_i, _i, _p, _p]),
 }
 
 _lock = threading.Lock()

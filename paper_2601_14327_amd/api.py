@@ -230,3 +230,22 @@ def laep_rearrange(loads, n_groups: int):
     check(lib().laep_rearrange(loads.ctypes.data, n, n_groups, group_of.ctypes.data,
                                order.ctypes.data, sums.ctypes.data))
     return dict(group_of=group_of, order=order, sums=sums[:n_groups])
+
+
+# ---- measurement kernels (laep_calib.h) -----------------------------------------------
+def laep_calib_copy(src: torch.Tensor, dst: torch.Tensor):
+    """dst <- src (raw bytes) with the library's streaming copy kernel."""
+    _dev(src, "src")
+    _dev(dst, "dst")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst is smaller than src")
+    check(lib().laep_calib_copy(_ptr(src), _ptr(dst), nbytes, _stream(src.device)))
+
+
+def laep_calib_mfma(n_workgroups: int, iters: int, out: torch.Tensor):
+    """bf16 MFMA loop: n_workgroups x 8 waves x iters x 8 MFMA 32x32x16."""
+    _dev(out, "out")
+    if out.dtype != torch.float32 or out.numel() < n_workgroups * 512:
+        raise ValueError("out must be float32 with n_workgroups * 512 elements")
+    check(lib().laep_calib_mfma(n_workgroups, iters, _ptr(out), _stream(out.device)))

@@ -9,6 +9,7 @@
 #include <cstring>
 
 #include "../../include/laep_moe.h"
+#include "../../include/laep_calib.h"
 #include "internal.hpp"
 
 namespace {
@@ -279,6 +280,20 @@ int moe_permute_bwd(const void* dx_perm, const int32_t* dest_row, int T, int k, 
   return hip_status(laep::launch_combine(dx_perm, nullptr, dest_row, T, k, d_model, dtype, dx,
                                          as_stream(stream)),
                     "moe_permute_bwd");
+}
+
+// ---- measurement kernels (laep_calib.h) ------------------------------------------
+int laep_calib_copy(const void* src, void* dst, size_t bytes, void* stream) {
+  REQUIRE(src && dst && aligned16(src) && aligned16(dst) && bytes % 16 == 0,
+          LAEP_ERR_INVALID_ARG, "laep_calib_copy: null or misaligned pointer, or bytes %% 16 != 0");
+  return hip_status(laep::launch_calib_copy(src, dst, bytes, as_stream(stream)), "laep_calib_copy");
+}
+
+int laep_calib_mfma(int n_workgroups, int iters, float* out, void* stream) {
+  REQUIRE(out && n_workgroups >= 1 && iters >= 1, LAEP_ERR_INVALID_ARG,
+          "laep_calib_mfma: null out, n_workgroups < 1 or iters < 1");
+  return hip_status(laep::launch_calib_mfma(n_workgroups, iters, out, as_stream(stream)),
+                    "laep_calib_mfma");
 }
 
 }  // extern "C"

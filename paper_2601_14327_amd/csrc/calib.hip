@@ -1,0 +1,54 @@
+// Measurement kernels (laep_calib.h): a streaming copy and a bf16 MFMA loop.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace laep {
+namespace {
+
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4_t* __restrict__ src,
+                                                   u32x4_t* __restrict__ dst, size_t n) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __restrict__ out) {
+  f32x16_t a0 = {}, a1 = {}, a2 = {}, a3 = {};
+  bf16x8_t x, y;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    x[i] = (__bf16)(0.001f * (lane + i));
+    y[i] = (__bf16)(0.002f * (i + 1));
+  }
+  for (int it = 0; it < iters; ++it) {
+    a0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a1, 0, 0, 0);
+    a2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a2, 0, 0, 0);
+    a3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a3, 0, 0, 0);
+    a0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a1, 0, 0, 0);
+    a2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a2, 0, 0, 0);
+    a3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a3, 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s += a0[r] + a1[r] + a2[r] + a3[r];
+  out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+}  // namespace
+
+hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_kernel, dim3(256 * 16), dim3(256), 0, s,
+                     static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), bytes / 16);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_mfma(int n_workgroups, int iters, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(mfma_loop_kernel, dim3(n_workgroups), dim3(512), 0, s, iters, out);
+  return hipGetLastError();
+}
+
+}  // namespace laep

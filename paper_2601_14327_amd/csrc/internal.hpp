@@ -53,4 +53,8 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                                void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
                                void* ws, hipStream_t s);
 
+// Measurement kernels (laep_calib.h).
+hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_calib_mfma(int n_workgroups, int iters, float* out, hipStream_t s);
+
 }  // namespace laep

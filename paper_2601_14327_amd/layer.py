@@ -82,7 +82,7 @@ class MoELayerPlan:
         api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
         api.moe_grouped_ffn_fwd(self.x_perm, w_gate_up, w_down, self.offsets,
                                 expert_map=expert_map, ws=self.ws_ffn, y_perm=self.y_perm,
-                                act_save=self.act_save)
+                                save_act=self.act_save is not None, act_save=self.act_save)
         api.moe_combine(self.y_perm, self.topk_gate, self.dest_row, out=self.out)
         return self.out
 

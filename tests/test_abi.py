@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "laep_moe.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 
 
 @pytest.fixture(scope="module")
@@ -25,9 +26,11 @@ def L():
 
 
 def _declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
 
 
 def test_header_declares_the_hot_path_calls():
@@ -40,7 +43,7 @@ def test_header_declares_the_hot_path_calls():
 
 def test_library_exports_every_declared_symbol(L):
     for n in _declared_functions():
-        assert hasattr(L, n), f"{n} declared in laep_moe.h but not exported"
+        assert hasattr(L, n), f"{n} declared in include/*.h but not exported"
 
 
 def test_binding_covers_every_declared_symbol():
@@ -106,6 +109,16 @@ def test_ffn_validation(L):
     assert L.moe_grouped_ffn_bwd(p, p, p, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0, p,
                                  1 << 30, None) == 2
     assert "LAEP_BF16" in _err(L)
+
+
+def test_calib_validation(L):
+    keep, p = _fake()
+    assert L.laep_calib_copy(p, p + 2, 64, None) == 1
+    assert L.laep_calib_copy(p, p, 60, None) == 1
+    assert L.laep_calib_copy(None, p, 64, None) == 1
+    assert L.laep_calib_mfma(0, 10, p, None) == 1
+    assert L.laep_calib_mfma(8, 0, p, None) == 1
+    assert L.laep_calib_mfma(8, 10, None, None) == 1
 
 
 def test_rowop_validation(L):
