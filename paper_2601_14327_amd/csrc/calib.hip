@@ -5,11 +5,23 @@
 namespace laep {
 namespace {
 
+// Four 16-byte loads in flight per thread before the stores.
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4_t* __restrict__ src,
                                                    u32x4_t* __restrict__ dst, size_t n) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-    dst[i] = src[i];
+  const size_t stride = (size_t)gridDim.x * blockDim.x * 4;
+  for (size_t base = (size_t)blockIdx.x * blockDim.x * 4 + threadIdx.x; base < n; base += stride) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const size_t i = base + (size_t)j * blockDim.x;
+      if (i < n) v[j] = src[i];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const size_t i = base + (size_t)j * blockDim.x;
+      if (i < n) dst[i] = v[j];
+    }
+  }
 }
 
 __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __restrict__ out) {
@@ -41,7 +53,7 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __rest
 
 hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_kernel, dim3(256 * 16), dim3(256), 0, s,
+  hipLaunchKernelGGL(copy_kernel, dim3(256 * 8), dim3(256), 0, s,
                      static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), bytes / 16);
   return hipGetLastError();
 }

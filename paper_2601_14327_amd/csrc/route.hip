@@ -2,13 +2,18 @@
 //
 // One workgroup of 512 threads handles 32 tokens.
 //  1. logits[32 x EP] = x_tile . W_r^T on the matrix cores.  The reduction
-//     dimension is split over the 8 waves (chunks of consecutive 16-wide
-//     k-steps dealt round robin); each wave holds a 32 x 32 fp32 block per 32
-//     experts.  The eight partial blocks are summed through LDS in wave
-//     order, so the result is deterministic.
-//  2. top-k: 8 lanes per token, each lane owning experts e = 8q + lane.  k
-//     passes of a (value desc, index asc) arg-max across the 8 lanes.  The
-//     slot order is descending logit, ties to the lower expert index.
+//     dimension is split over the 8 waves; each wave holds a 32 x 32 fp32
+//     block per 32 experts.  The eight partial blocks are summed through LDS
+//     in wave order, so the result is deterministic.
+//     bf16 with up to 128 experts: x and W_r go through LDS in chunks of 256
+//     (or 128) columns by LDS-DMA, 3-4 stages deep, so every global request
+//     is a whole 128-byte line (in the MFMA operand layout a direct load
+//     touches 32 bytes of each of 32 rows, four requests per line).  Other
+//     cases load the operands directly, U k-steps per chunk in flight.
+//  2. top-k: 16 lanes (one DPP row) per token, lane g owning experts
+//     e = 16q + g.  k passes of a (value desc, index asc) arg-max across the
+//     16 lanes, exchanged by DPP lane permutations.  The slot order is
+//     descending logit, ties to the lower expert index.
 //  3. gates: exp(l_j - l_max) divided by the sum over the selected k
 //     (renorm) or over all alive experts.
 #include "common.hpp"
@@ -20,7 +25,6 @@ namespace {
 constexpr int kRouteTokens = 32;
 constexpr int kRouteWaves = 8;
 constexpr int kRouteThreads = 64 * kRouteWaves;
-constexpr int kTopkThreads = 8 * kRouteTokens;  // 8 lanes per token
 
 // One k-step of the router GEMM for element type T.
 //   bf16: 16 k per step; lane loads 8 consecutive k (16 bytes) of its row.
@@ -54,7 +58,74 @@ __device__ __forceinline__ u32x4_t load16_or_zero(const T* p, bool ok) {
   return v;
 }
 
-template <typename T, int NB>
+// x and W_r chunks of KC columns staged through LDS by LDS-DMA (whole 128-byte
+// lines per request), for bf16 and d % KC == 0.  Rows of the stage: 32 tokens,
+// then EP experts; 16-byte chunk c of row r sits at c ^ (r & 15).
+template <int NB, int KC>
+struct RouterStage {
+  static constexpr int EP = 32 * NB;
+  static constexpr int ROWS = 32 + EP;
+  static constexpr int RB = KC * 2;          // bytes per staged row
+  static constexpr int CPR = RB / 16;        // chunks per row
+  static constexpr int BYTES = ROWS * RB;
+  static constexpr int NCH = ROWS * CPR / kRouteThreads;  // DMA chunks per thread
+  static_assert((ROWS * CPR) % kRouteThreads == 0, "stage chunks must divide over the threads");
+  // stages in flight: as many as fit next to the logits tile, at most 4
+  static constexpr int LOGITS = 32 * (EP + 1) * 4;
+  static constexpr int FIT = (156 * 1024 - LOGITS) / BYTES;
+  static constexpr int NS = FIT > 4 ? 4 : FIT;
+  static_assert(NS >= 2, "at least two stages");
+};
+
+template <int NB, int KC>
+struct StageBytes {
+  static constexpr int value = RouterStage<NB, KC>::NS * RouterStage<NB, KC>::BYTES;
+};
+template <int NB>
+struct StageBytes<NB, 0> {
+  static constexpr int value = 16;
+};
+
+// Lane exchange inside a 16-lane DPP row (no LDS round trip): quad_perm
+// [1,0,3,2] and [2,3,0,1] swap neighbours at distance 1 and 2, row_half_mirror
+// and row_mirror pair lane i with 7-i and 15-i.  Applied in that order, a
+// symmetric pairwise combine leaves every lane of the row with the row's result.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+// (value desc, index asc) arg-max step
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(float& bv, int& be) {
+  const float ov = dpp_f<CTRL>(bv);
+  const int oe = dpp_i<CTRL>(be);
+  if (ov > bv || (ov == bv && oe < be)) {
+    bv = ov;
+    be = oe;
+  }
+}
+
+template <int NCH>
+__device__ __forceinline__ void route_dma(char* dst, const bf16_t* const* src, int k0, int wave) {
+#pragma unroll
+  for (int i = 0; i < NCH; ++i)
+    __builtin_amdgcn_global_load_lds(src[i] + k0,
+                                     (__attribute__((address_space(3))) void*)(
+                                         dst + (i * kRouteThreads + wave * 64) * 16),
+                                     16, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ void route_wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <typename T, int NB, int KC>
 __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     const T* __restrict__ x, const T* __restrict__ w, const float* __restrict__ bias,
     const uint8_t* __restrict__ alive, int n_tok, int d, int E, int k, int renorm,
@@ -62,10 +133,10 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     float* __restrict__ gate_out) {
   constexpr int EP = 32 * NB;        // experts padded to 32
   constexpr int LD = EP + 1;         // LDS row stride (floats)
-  constexpr int EPL = EP / 8;        // experts owned per top-k lane
-  using Step = RouterStep<T>;
-
+  constexpr int EPL = EP / 16;       // experts owned per top-k lane
   __shared__ float s_log[kRouteTokens * LD];
+  // LDS-staged path: the operand stages, reused for the cross-wave partial sums
+  __shared__ __attribute__((aligned(1024))) char s_stage[StageBytes<NB, KC>::value];
   __shared__ float s_bias[EP];
   __shared__ uint8_t s_alive[EP];
 
@@ -88,48 +159,146 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
 
   const int row = lane & 31;
   const int kh = lane >> 5;
-  const int tok = t0 + row;
-  const bool tok_ok = tok < n_tok;
-  const T* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
-  const int n_steps = (d + Step::kK - 1) / Step::kK;
-  // The reduction is cut into chunks of U consecutive k-steps dealt round
-  // robin to the waves.  A chunk's loads are all issued before its MFMAs,
-  // so each wave keeps U row loads of x in flight (the router GEMM is
-  // bound by reading x once from HBM).
-  constexpr int U = NB >= 8 ? 2 : (NB >= 4 ? 4 : 8);
-  for (int c = wave; c * U < n_steps; c += kRouteWaves) {
-    u32x4_t a[U];
-    u32x4_t b[U][NB];
+  if constexpr (KC > 0) {
+    // LDS-staged: every thread fills NCH chunks of each stage; the waves
+    // share the KC/16 k-steps of a stage round robin.
+    using St = RouterStage<NB, KC>;
+    const bf16_t* src[St::NCH];
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      const int kk = (c * U + i) * Step::kK + kh * Step::kLaneK;
-      const bool k_ok = kk < d;  // d % 8 == 0: a lane's k-group is all in or all out
-      a[i] = load16_or_zero(xrow + kk, tok_ok && k_ok);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int e = nb * 32 + row;
-        b[i][nb] = load16_or_zero(w + (size_t)(e < E ? e : 0) * d + kk, k_ok && e < E);
+    for (int i = 0; i < St::NCH; ++i) {
+      const int q = i * kRouteThreads + tid;
+      const int r = q / St::CPR;
+      const int lc = (q % St::CPR) ^ (r & 15);
+      const bf16_t* base;
+      if (r < 32) {
+        const int t = t0 + r < n_tok ? t0 + r : n_tok - 1;
+        base = reinterpret_cast<const bf16_t*>(x) + (size_t)t * d;
+      } else {
+        const int e = r - 32 < E ? r - 32 : E - 1;
+        base = reinterpret_cast<const bf16_t*>(w) + (size_t)e * d;
       }
+      src[i] = base + lc * 8;
     }
+    const int n_chunks = d / KC;
+    // NS stages: chunks c .. c+NS-2 in flight while chunk c computes.  Past the
+    // end the last chunk is loaded again into the free stage (never read), so
+    // one constant vmcnt serves every wait.
+    constexpr int NS = St::NS;
+    auto issue = [&](int c) {
+      const int cc = c < n_chunks ? c : n_chunks - 1;
+      route_dma<St::NCH>(s_stage + (c % NS) * St::BYTES, src, cc * KC, wave);
+    };
 #pragma unroll
-    for (int i = 0; i < U; ++i)
+    for (int c = 0; c < NS - 1; ++c) issue(c);
+    for (int c = 0; c < n_chunks; ++c) {
+      const char* st = s_stage + (c % NS) * St::BYTES;
+      issue(c + NS - 1);                       // into the stage chunk c-1 used
+      route_wait_vmcnt<(NS - 1) * St::NCH>();  // chunk c has landed
+      __syncthreads();
+      for (int s = wave; s < KC / 16; s += kRouteWaves) {
+        const int lc = 2 * s + kh;
+        const u32x4_t a =
+            *reinterpret_cast<const u32x4_t*>(st + row * St::RB + ((lc ^ (row & 15)) << 4));
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) Step::mma(acc[nb], a[i], b[i][nb]);
+        for (int nb = 0; nb < NB; ++nb) {
+          const int r = 32 + nb * 32 + row;
+          const u32x4_t bv =
+              *reinterpret_cast<const u32x4_t*>(st + r * St::RB + ((lc ^ (r & 15)) << 4));
+          RouterStep<bf16_t>::mma(acc[nb], a, bv);
+        }
+      }
+      __syncthreads();  // stage c % NS is refilled at the next iteration
+    }
+    route_wait_vmcnt<0>();  // no LDS-DMA may still be writing when the LDS is reused
+  } else {
+    using Step = RouterStep<T>;
+    const int tok = t0 + row;
+    const bool tok_ok = tok < n_tok;
+    const T* xrow = x + (size_t)(tok_ok ? tok : 0) * d;
+    const int n_steps = (d + Step::kK - 1) / Step::kK;
+    // The reduction is cut into chunks of U consecutive k-steps dealt round
+    // robin to the waves.  A chunk's loads are all issued before its MFMAs.
+    constexpr int U = NB >= 5 ? 2 : (NB >= 3 ? 4 : 8);
+    for (int c = wave; c * U < n_steps; c += kRouteWaves) {
+      u32x4_t a[U];
+      u32x4_t b[U][NB];
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        const int kk = (c * U + i) * Step::kK + kh * Step::kLaneK;
+        const bool k_ok = kk < d;  // d % 8 == 0: a lane's k-group is all in or all out
+        a[i] = load16_or_zero(xrow + kk, tok_ok && k_ok);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int e = nb * 32 + row;
+          b[i][nb] = load16_or_zero(w + (size_t)(e < E ? e : 0) * d + kk, k_ok && e < E);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < U; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) Step::mma(acc[nb], a[i], b[i][nb]);
+    }
   }
 
+  // ---- cross-wave sum, deterministic ----------------------------------------------
   // acc[nb][r]: token (r/4)*8 + kh*4 + r%4, expert nb*32 + row.
-  for (int wv = 0; wv < kRouteWaves; ++wv) {
-    __syncthreads();
-    if (wave == wv) {
+  auto tile_at = [&](int nb, int r, int& t, int& e) {
+    t = (r >> 2) * 8 + kh * 4 + (r & 3);
+    e = nb * 32 + row;
+  };
+  if constexpr (KC > 0) {
+    // a tree over the waves (8 -> 4 -> 2 -> 1) through the idle stage buffers
+    static_assert(4 * 32 * EP * 4 <= StageBytes<NB, KC>::value, "partials must fit the stages");
+    float* part = reinterpret_cast<float*>(s_stage);
+    constexpr int SL = 32 * EP;
+    for (int half = kRouteWaves / 2; half >= 1; half >>= 1) {
+      if (wave >= half && wave < 2 * half) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            int t, e;
+            tile_at(nb, r, t, e);
+            part[(wave - half) * SL + t * EP + e] = acc[nb][r];
+          }
+      }
+      __syncthreads();
+      if (wave < half) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            int t, e;
+            tile_at(nb, r, t, e);
+            acc[nb][r] += part[wave * SL + t * EP + e];
+          }
+      }
+      __syncthreads();
+    }
+    if (wave == 0) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int t = (r >> 2) * 8 + kh * 4 + (r & 3);
-          const int e = nb * 32 + row;
-          float* dst = &s_log[t * LD + e];
-          *dst = (wv == 0) ? acc[nb][r] : (*dst + acc[nb][r]);
+          int t, e;
+          tile_at(nb, r, t, e);
+          s_log[t * LD + e] = acc[nb][r];
         }
+    }
+  } else {
+    for (int wv = 0; wv < kRouteWaves; ++wv) {
+      __syncthreads();
+      if (wave == wv) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            int t, e;
+            tile_at(nb, r, t, e);
+            float* dst = &s_log[t * LD + e];
+            *dst = (wv == 0) ? acc[nb][r] : (*dst + acc[nb][r]);
+          }
+      }
     }
   }
   __syncthreads();
@@ -148,15 +317,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     }
   }
 
-  // ---- 2. top-k (the first 256 threads; the others idle through it) -----------
-  const bool tk = tid < kTopkThreads;
-  const int ti = tk ? (tid >> 3) : 0;  // token within the tile
-  const int g = tid & 7;               // lane within the token's group of 8
+  // ---- 2. top-k: 16 lanes (one DPP row) per token --------------------------------
+  const int ti = tid >> 4;  // token within the tile
+  const int g = tid & 15;   // lane within the token's row; owns experts e = 16 q + g
   float v[EPL];
 #pragma unroll
   for (int q = 0; q < EPL; ++q) {
-    const int e = q * 8 + g;
-    v[q] = (tk && s_alive[e]) ? s_log[ti * LD + e] : -INFINITY;
+    const int e = q * 16 + g;
+    v[q] = s_alive[e] ? s_log[ti * LD + e] : -INFINITY;
   }
   __syncthreads();  // s_log is reused below for the gate numerators
 
@@ -164,45 +332,47 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   float vmax = -INFINITY;
 #pragma unroll
   for (int q = 0; q < EPL; ++q) vmax = fmaxf(vmax, v[q]);
-#pragma unroll
-  for (int off = 1; off < 8; off <<= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, off, 8));
+  vmax = fmaxf(vmax, dpp_f<kDppXor1>(vmax));
+  vmax = fmaxf(vmax, dpp_f<kDppXor2>(vmax));
+  vmax = fmaxf(vmax, dpp_f<kDppHalfMirror>(vmax));
+  vmax = fmaxf(vmax, dpp_f<kDppMirror>(vmax));
   const bool none_alive = (vmax == -INFINITY);
   float s_all = 0.0f;
   if (!none_alive) {
 #pragma unroll
     for (int q = 0; q < EPL; ++q)
-      if (v[q] != -INFINITY) s_all += expf(v[q] - vmax);
+      if (v[q] != -INFINITY) s_all += __expf(v[q] - vmax);
   }
-#pragma unroll
-  for (int off = 1; off < 8; off <<= 1) s_all += __shfl_xor(s_all, off, 8);
+  s_all += dpp_f<kDppXor1>(s_all);
+  s_all += dpp_f<kDppXor2>(s_all);
+  s_all += dpp_f<kDppHalfMirror>(s_all);
+  s_all += dpp_f<kDppMirror>(s_all);
 
   float* s_ex = s_log;  // [32][k] gate numerators (k <= E <= EP < LD)
   const int t_glob = t0 + ti;
-  const bool write_ok = tk && t_glob < n_tok;
+  const bool write_ok = t_glob < n_tok;
   float s_sel = 0.0f;
   for (int j = 0; j < k; ++j) {
     float bv = -INFINITY;
     int be = 0x7FFFFFFF;
 #pragma unroll
     for (int q = 0; q < EPL; ++q) {
-      const int e = q * 8 + g;
+      const int e = q * 16 + g;
       if (v[q] > bv) { bv = v[q]; be = e; }  // ascending e: strict keeps the lower index
     }
-#pragma unroll
-    for (int off = 1; off < 8; off <<= 1) {
-      const float ov = __shfl_xor(bv, off, 8);
-      const int oe = __shfl_xor(be, off, 8);
-      if (ov > bv || (ov == bv && oe < be)) { bv = ov; be = oe; }
-    }
+    argmax_step<kDppXor1>(bv, be);
+    argmax_step<kDppXor2>(bv, be);
+    argmax_step<kDppHalfMirror>(bv, be);
+    argmax_step<kDppMirror>(bv, be);
     const bool found = (bv != -INFINITY);
-    if (found && (be & 7) == g) {
+    if (found && (be & 15) == g) {
 #pragma unroll
       for (int q = 0; q < EPL; ++q)
-        if (q * 8 + g == be) v[q] = -INFINITY;
+        if (q * 16 + g == be) v[q] = -INFINITY;
     }
-    const float ex = found ? expf(bv - vmax) : 0.0f;
+    const float ex = found ? __expf(bv - vmax) : 0.0f;
     s_sel += ex;
-    if (tk && g == 0) {
+    if (g == 0) {
       s_ex[ti * k + j] = ex;
       if (write_ok) idx_out[(size_t)t_glob * k + j] = found ? be : -1;
     }
@@ -211,11 +381,20 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   const float denom = renorm ? s_sel : s_all;
   const float inv_ok = (denom > 0.0f) ? 1.0f : 0.0f;
   if (write_ok) {
-    for (int j = g; j < k; j += 8) {
+    for (int j = g; j < k; j += 16) {
       const float ex = s_ex[ti * k + j];
       gate_out[(size_t)t_glob * k + j] = inv_ok * (ex / (denom > 0.0f ? denom : 1.0f));
     }
   }
+}
+
+template <typename T, int NB, int KC>
+void launch_route_nb(dim3 grid, hipStream_t s, const void* x, const void* w, const float* bias,
+                     const uint8_t* alive, int T_, int d, int E, int k, int renorm, float* logits,
+                     int32_t* idx, float* gate) {
+  hipLaunchKernelGGL((route_kernel<T, NB, KC>), grid, dim3(kRouteThreads), 0, s,
+                     static_cast<const T*>(x), static_cast<const T*>(w), bias, alive, T_, d, E, k,
+                     renorm, logits, idx, gate);
 }
 
 template <typename T>
@@ -223,27 +402,42 @@ hipError_t launch_route_t(const void* x, const void* w, const float* bias, const
                           int T_, int d, int E, int k, int renorm, float* logits, int32_t* idx,
                           float* gate, hipStream_t s) {
   const int nb = (E + 31) / 32;
-  dim3 grid((T_ + kRouteTokens - 1) / kRouteTokens), block(kRouteThreads);
-  const T* xp = static_cast<const T*>(x);
-  const T* wp = static_cast<const T*>(w);
-#define LAEP_ROUTE_CASE(N)                                                                    \
-  case N:                                                                                     \
-    hipLaunchKernelGGL((route_kernel<T, N>), grid, block, 0, s, xp, wp, bias, alive, T_, d, E, \
-                       k, renorm, logits, idx, gate);                                         \
-    break;
-  switch (nb) {
-    LAEP_ROUTE_CASE(1)
-    LAEP_ROUTE_CASE(2)
-    LAEP_ROUTE_CASE(3)
-    LAEP_ROUTE_CASE(4)
-    LAEP_ROUTE_CASE(5)
-    LAEP_ROUTE_CASE(6)
-    LAEP_ROUTE_CASE(7)
-    LAEP_ROUTE_CASE(8)
-    default:
-      return hipErrorInvalidValue;
+  const dim3 grid((T_ + kRouteTokens - 1) / kRouteTokens);
+  // bf16 with up to 128 experts: LDS-staged chunks of 256 (NB <= 2) or 128 columns
+  int kc = 0;
+  if (sizeof(T) == 2 && nb <= 4) {
+    if (nb <= 2 && d % 256 == 0) kc = 256;
+    else if (d % 128 == 0) kc = 128;
   }
-#undef LAEP_ROUTE_CASE
+#define LAEP_ROUTE_ARGS grid, s, x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate
+  if constexpr (sizeof(T) == 2) {
+    if (kc == 256) {
+      if (nb == 1) launch_route_nb<T, 1, 256>(LAEP_ROUTE_ARGS);
+      else launch_route_nb<T, 2, 256>(LAEP_ROUTE_ARGS);
+      return hipGetLastError();
+    }
+    if (kc == 128) {
+      switch (nb) {
+        case 1: launch_route_nb<T, 1, 128>(LAEP_ROUTE_ARGS); break;
+        case 2: launch_route_nb<T, 2, 128>(LAEP_ROUTE_ARGS); break;
+        case 3: launch_route_nb<T, 3, 128>(LAEP_ROUTE_ARGS); break;
+        default: launch_route_nb<T, 4, 128>(LAEP_ROUTE_ARGS); break;
+      }
+      return hipGetLastError();
+    }
+  }
+  switch (nb) {
+    case 1: launch_route_nb<T, 1, 0>(LAEP_ROUTE_ARGS); break;
+    case 2: launch_route_nb<T, 2, 0>(LAEP_ROUTE_ARGS); break;
+    case 3: launch_route_nb<T, 3, 0>(LAEP_ROUTE_ARGS); break;
+    case 4: launch_route_nb<T, 4, 0>(LAEP_ROUTE_ARGS); break;
+    case 5: launch_route_nb<T, 5, 0>(LAEP_ROUTE_ARGS); break;
+    case 6: launch_route_nb<T, 6, 0>(LAEP_ROUTE_ARGS); break;
+    case 7: launch_route_nb<T, 7, 0>(LAEP_ROUTE_ARGS); break;
+    case 8: launch_route_nb<T, 8, 0>(LAEP_ROUTE_ARGS); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef LAEP_ROUTE_ARGS
   return hipGetLastError();
 }
 

@@ -36,50 +36,102 @@ __global__ __launch_bounds__(kRowThreads) void permute_kernel(
   }
 }
 
+// One 8-element row vector in its storage format: load (zero when !ok) and
+// acc[e] += g * value[e].
+template <typename T> struct RawRow;
+template <> struct RawRow<bf16_t> {
+  typedef u32x4_t type;
+  __device__ static __forceinline__ type load(const bf16_t* p, bool ok) {
+    type v = {0u, 0u, 0u, 0u};
+    if (ok) v = *reinterpret_cast<const u32x4_t*>(p);
+    return v;
+  }
+  __device__ static __forceinline__ void fma8(float acc[8], float g, const type& v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += g * lo_bf16(v[i]);
+      acc[2 * i + 1] += g * hi_bf16(v[i]);
+    }
+  }
+};
+template <> struct RawRow<float> {
+  struct type { f32x4_t a, b; };
+  __device__ static __forceinline__ type load(const float* p, bool ok) {
+    type v;
+    v.a = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    v.b = v.a;
+    if (ok) {
+      v.a = *reinterpret_cast<const f32x4_t*>(p);
+      v.b = *reinterpret_cast<const f32x4_t*>(p + 4);
+    }
+    return v;
+  }
+  __device__ static __forceinline__ void fma8(float acc[8], float g, const type& v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[i] += g * v.a[i];
+      acc[4 + i] += g * v.b[i];
+    }
+  }
+};
+
+// Each thread owns UNR (token, vector) items per pass and issues every row
+// load of the pass (up to 8 slots per item) before the first sum, so the two
+// dependent rounds (dest_row / gate, then the rows) are paid once per pass.
 template <typename T, bool GATED>
 __global__ __launch_bounds__(kRowThreads) void combine_kernel(
     const T* __restrict__ y, const float* __restrict__ gate, const int32_t* __restrict__ dest_row,
     int n_tok, int k, int d, int tpb, T* __restrict__ out) {
+  constexpr int UNR = sizeof(T) == 2 ? 2 : 1;
   const int vec_per_row = d / 8;
   const int t_lo = blockIdx.x * tpb;
   const int n_vec = tpb * vec_per_row;
-  for (int i = threadIdx.x; i < n_vec; i += kRowThreads) {
-    const int t = t_lo + i / vec_per_row;
-    const int v = i % vec_per_row;
-    if (t >= n_tok) break;
-    float acc[8];
+  for (int i0 = threadIdx.x; i0 < n_vec; i0 += UNR * kRowThreads) {
+    int t[UNR], v[UNR];
+    bool ok[UNR];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
-    // slots in groups of 8: every row load of a group is issued before the
-    // sums, which still run in slot order
-    for (int j0 = 0; j0 < k; j0 += 8) {
-      int r[8];
-      float g[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int j = j0 + q;
-        const size_t s = (size_t)t * k + j;
-        r[q] = j < k ? dest_row[s] : -1;
-        g[q] = (GATED && j < k) ? gate[s] : 1.0f;
-      }
-      float val[8][8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (r[q] >= 0) {
-          Elem<T>::load8(y + (size_t)r[q] * d + (size_t)v * 8, val[q]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) val[q][e] = 0.0f;
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (r[q] >= 0) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[e] += g[q] * val[q][e];
-        }
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u * kRowThreads;
+      t[u] = t_lo + i / vec_per_row;
+      v[u] = i % vec_per_row;
+      ok[u] = i < n_vec && t[u] < n_tok;
     }
-    Elem<T>::store8(out + (size_t)t * d + (size_t)v * 8, acc);
+    float acc[UNR][8];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[u][q] = 0.0f;
+    // slots in groups of 8; the sums run in slot order
+    for (int j0 = 0; j0 < k; j0 += 8) {
+      int r[UNR][8];
+      float g[UNR][8];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int j = j0 + q;
+          const size_t s = (size_t)t[u] * k + j;
+          const bool in = ok[u] && j < k;
+          r[u][q] = in ? dest_row[s] : -1;
+          g[u][q] = (GATED && in) ? gate[s] : 1.0f;
+        }
+      // rows stay in their storage format until summed (bf16: 4 registers per row)
+      typename RawRow<T>::type raw[UNR][8];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          raw[u][q] = RawRow<T>::load(y + (size_t)(r[u][q] >= 0 ? r[u][q] : 0) * d +
+                                      (size_t)v[u] * 8, r[u][q] >= 0);
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (r[u][q] >= 0) RawRow<T>::fma8(acc[u], g[u][q], raw[u][q]);
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+      if (ok[u]) Elem<T>::store8(out + (size_t)t[u] * d + (size_t)v[u] * 8, acc[u]);
   }
 }
 

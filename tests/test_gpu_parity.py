@@ -41,6 +41,8 @@ def _route_case(c, k, dtype, renorm=True, alive=None):
     (1000, 256, 64, 8, "bf16", True, 0.0),    # ragged token tail
     (777, 512, 64, 8, "bf16", True, 2.0),     # biased router
     (333, 192, 40, 5, "bf16", False, 0.0),    # E not a multiple of 32
+    (300, 384, 100, 6, "bf16", True, 1.0),    # LDS-staged router, 128-column chunks, 4 expert blocks
+    (96, 128, 8, 2, "bf16", False, 0.0),      # LDS-staged router, one 128-column chunk
     (130, 64, 256, 16, "bf16", True, 0.5),    # largest expert count
     (65, 136, 3, 3, "bf16", True, 0.0),       # k = E, d not a multiple of 16
     (1, 64, 1, 1, "f32", True, 0.0),          # one token, one expert
