@@ -4,9 +4,11 @@
 Default workload ("balanced"): T=8192 tokens, d_model=2048, 64 experts,
 top-8 renormalised softmax gating, SwiGLU d_ff=1024, bf16 with fp32
 accumulation.  One step = one forward pass of the whole layer:
-route -> expert counts -> permute -> grouped SwiGLU FFN -> combine, every
-call a kernel of the C-ABI library; three input sets rotate over the steps so
-the activations are not cache-resident.
+route -> expert counts -> dispatch + grouped SwiGLU FFN (one call, the
+dispatch folded into the FFN's operand loads) -> combine, every call a kernel
+of the C-ABI library; three input sets rotate over the steps so the
+activations are not cache-resident.  Training steps (shard_bwd) keep the
+separate permute, because the weight gradient reads x_perm.
 
 Prints ONE JSON line:
   value        tokens/s of the whole step (wall clock over the timed steps,
@@ -152,14 +154,19 @@ class Setup:
         else:
             out += [("counts", lambda: L.moe_expert_counts(self.idx, w.E, ws=p.ws_counts,
                                                            counts=p.counts, offsets=p.offsets,
-                                                           dest_row=p.dest_row))]
+                                                           dest_row=p.dest_row,
+                                                           row_src=p.row_src))]
             gate = self.gate
-        out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm)),
-                ("ffn_fwd", lambda: L.moe_grouped_ffn_fwd(p.x_perm, self.wgu, self.wd, p.offsets,
-                                                          ws=p.ws_ffn, y_perm=p.y_perm,
-                                                          save_act=p.act_save is not None,
-                                                          act_save=p.act_save)),
-                ("combine", lambda: L.moe_combine(p.y_perm, gate, p.dest_row, out=p.out))]
+        if p.fused:   # dispatch folded into the FFN's operand loads
+            out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather(
+                x, p.row_src, w.k, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
+                y_perm=p.y_perm, save_act=p.act_save is not None, act_save=p.act_save))]
+        else:
+            out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm)),
+                    ("ffn_fwd", lambda: L.moe_grouped_ffn_fwd(
+                        p.x_perm, self.wgu, self.wd, p.offsets, ws=p.ws_ffn, y_perm=p.y_perm,
+                        save_act=p.act_save is not None, act_save=p.act_save))]
+        out += [("combine", lambda: L.moe_combine(p.y_perm, gate, p.dest_row, out=p.out))]
         if w.backward:
             if p.dw_gate_up is None:
                 import torch

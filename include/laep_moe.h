@@ -108,7 +108,9 @@ int moe_route(const void* x, const void* w_router, const float* bias,
  *   row_src[dest_row[s]] = s   (inverse map; optional)
  *   etn_accum[e] += counts[e]  (optional int64 running ETN row)
  *
- *   topk_idx device [T, k] int32, values in [0, E) or -1
+ *   topk_idx device [T, k] int32, values in [0, E) or -1; the ids of one
+ *   token are distinct (as moe_route writes them; a repeated id within a token
+ *   is counted once and its slots share one row)
  *   counts device [E] int32, offsets device [E + 1] int32,
  *   dest_row device [T * k] int32, row_src device [T * k] int32 or NULL,
  *   etn_accum device [E] int64 or NULL.
@@ -176,6 +178,26 @@ int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
                         int d_model, int d_ff, int64_t R, void* y_perm,
                         void* act_save, void* ws, size_t ws_bytes,
                         void* stream);
+
+/*
+ * moe_grouped_ffn_fwd_gather -- moe_permute followed by moe_grouped_ffn_fwd
+ * in one pass: the gate/up product reads each routed row straight from the
+ * token rows (x_perm is never written).  Routed row r is token
+ * row_src[r] / k, as moe_expert_counts writes row_src (the inverse of
+ * dest_row).  Results are bit-identical to the two calls.
+ *
+ *   x device [T, d_model] bf16; row_src device [R] int32 (every entry in
+ *   [0, T*k)); the other arguments and the workspace are those of
+ *   moe_grouped_ffn_fwd.  dtype must be LAEP_BF16 (LAEP_ERR_UNSUPPORTED
+ *   otherwise).
+ */
+int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
+                               int k, const void* w_gate_up,
+                               const void* w_down, const int32_t* offsets,
+                               const int32_t* expert_map, int dtype, int E,
+                               int d_model, int d_ff, int64_t R,
+                               void* y_perm, void* act_save, void* ws,
+                               size_t ws_bytes, void* stream);
 
 /*
  * moe_grouped_ffn_bwd -- backward of moe_grouped_ffn_fwd (data and weight

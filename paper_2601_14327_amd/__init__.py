@@ -8,6 +8,7 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     laep_prune_mask      LAEP prune decision (alpha / beta thresholds)
     moe_permute          dispatch of token rows to expert order
     moe_grouped_ffn_fwd  grouped SwiGLU expert FFN (bf16 MFMA)
+    moe_grouped_ffn_fwd_gather   the same with the dispatch folded into the operand loads
     moe_combine          gate-weighted combine
     moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
     laep_rearrange       host utility: balanced expert placement
@@ -25,6 +26,7 @@ from .api import (  # noqa: F401
     moe_expert_counts,
     moe_grouped_ffn_bwd,
     moe_grouped_ffn_fwd,
+    moe_grouped_ffn_fwd_gather,
     moe_permute,
     moe_permute_bwd,
     moe_route,

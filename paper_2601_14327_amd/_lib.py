@@ -51,6 +51,8 @@ SIGNATURES = {
     "laep_prune_mask": (_i, [_p, _i, _i64, _d, _d, _p, _p, _p]),
     "moe_permute": (_i, [_p, _i, _p, _i, _i, _i, _p, _p]),
     "moe_grouped_ffn_fwd": (_i, [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p, _sz, _p]),
+    "moe_grouped_ffn_fwd_gather": (_i, [_p, _p, _i, _i, _p, _p, _p, _p, _i, _i, _i, _i, _i64,
+                                        _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_bwd": (_i, [_p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p,
                                  _i, _p, _sz, _p]),
     "laep_ws_hb_offset": (_sz, [_i64, _i, _i]),

@@ -76,7 +76,8 @@ def moe_route(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=None, ali
 
 
 def moe_expert_counts(topk_idx: torch.Tensor, E: int, *, want_row_src: bool = False,
-                      etn_accum=None, ws=None, counts=None, offsets=None, dest_row=None):
+                      etn_accum=None, ws=None, counts=None, offsets=None, dest_row=None,
+                      row_src=None):
     """Returns (counts [E] i32, offsets [E+1] i32, dest_row [T*k] i32[, row_src])."""
     _dev(topk_idx, "topk_idx")
     T, k = topk_idx.shape
@@ -84,7 +85,9 @@ def moe_expert_counts(topk_idx: torch.Tensor, E: int, *, want_row_src: bool = Fa
     counts = torch.empty(E, dtype=torch.int32, device=dev) if counts is None else counts
     offsets = torch.empty(E + 1, dtype=torch.int32, device=dev) if offsets is None else offsets
     dest_row = torch.empty(T * k, dtype=torch.int32, device=dev) if dest_row is None else dest_row
-    row_src = torch.empty(T * k, dtype=torch.int32, device=dev) if want_row_src else None
+    want_row_src = want_row_src or row_src is not None
+    if want_row_src and row_src is None:
+        row_src = torch.empty(T * k, dtype=torch.int32, device=dev)
     nbytes = workspace_bytes(LAEP_CALL_COUNTS, T, k, E)
     ws = _workspace(ws, nbytes, dev)
     check(lib().moe_expert_counts(_ptr(topk_idx), T, k, E, _ptr(counts), _ptr(offsets),
@@ -140,6 +143,35 @@ def moe_grouped_ffn_fwd(x_perm: torch.Tensor, w_gate_up: torch.Tensor, w_down: t
                                     _ptr(expert_map), _dtype_code(x_perm), E, d, f, R,
                                     _ptr(y_perm), _ptr(act_save), _ptr(ws), ws.numel(),
                                     _stream(dev)))
+    return y_perm, act_save
+
+
+def moe_grouped_ffn_fwd_gather(x: torch.Tensor, row_src: torch.Tensor, k: int,
+                               w_gate_up: torch.Tensor, w_down: torch.Tensor,
+                               offsets: torch.Tensor, *, rows: Optional[int] = None,
+                               expert_map=None, save_act: bool = False, ws=None, y_perm=None,
+                               act_save=None):
+    """moe_permute + moe_grouped_ffn_fwd in one pass (bf16): routed row r reads
+    token row row_src[r] // k.  Returns (y_perm, act_save or None)."""
+    for t, n in ((x, "x"), (row_src, "row_src"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
+                 (offsets, "offsets")):
+        _dev(t, n)
+    T, d = x.shape
+    R = T * k if rows is None else rows
+    f = w_down.shape[2]
+    E = offsets.shape[0] - 1
+    dev = x.device
+    y_perm = torch.empty((R, d), dtype=x.dtype, device=dev) if y_perm is None else y_perm
+    if save_act and act_save is None:
+        act_save = torch.empty((R, 2 * f), dtype=x.dtype, device=dev)
+    if not save_act:
+        act_save = None
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d, f), dev)
+    check(lib().moe_grouped_ffn_fwd_gather(_ptr(x), _ptr(row_src), T, k, _ptr(w_gate_up),
+                                           _ptr(w_down), _ptr(offsets), _ptr(expert_map),
+                                           _dtype_code(x), E, d, f, R, _ptr(y_perm),
+                                           _ptr(act_save), _ptr(ws), ws.numel(),
+                                           _stream(dev)))
     return y_perm, act_save
 
 

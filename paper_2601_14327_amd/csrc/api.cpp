@@ -206,6 +206,35 @@ int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up, const void* w
   return hip_status(e, "moe_grouped_ffn_fwd");
 }
 
+int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T, int k,
+                               const void* w_gate_up, const void* w_down, const int32_t* offsets,
+                               const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
+                               int64_t R, void* y_perm, void* act_save, void* ws, size_t ws_bytes,
+                               void* stream) {
+  int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
+  if (rc) return rc;
+  REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_fwd_gather: only LAEP_BF16 is supported");
+  REQUIRE(T >= 0 && k >= 1, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: T=%d, k=%d", T, k);
+  REQUIRE(R <= (int64_t)T * k, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather: R=%lld exceeds T*k", (long long)R);
+  REQUIRE(offsets, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: offsets must be non-null");
+  if (R == 0) return ok();
+  REQUIRE(x && row_src && w_gate_up && w_down && y_perm && ws, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather: x, row_src, w_gate_up, w_down, y_perm and ws must be "
+          "non-null");
+  REQUIRE(aligned16(x) && aligned16(w_gate_up) && aligned16(w_down) && aligned16(y_perm) &&
+              aligned16(act_save) && aligned16(ws),
+          LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: buffers must be 16-byte aligned");
+  const size_t need = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, dtype);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE,
+          "moe_grouped_ffn_fwd_gather: workspace %zu < %zu bytes", ws_bytes, need);
+  return hip_status(laep::launch_ffn_fwd_bf16(x, w_gate_up, w_down, offsets, expert_map, E,
+                                              d_model, d_ff, R, y_perm, act_save, ws,
+                                              as_stream(stream), row_src, k),
+                    "moe_grouped_ffn_fwd_gather");
+}
+
 int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act_save,
                         const void* w_gate_up, const void* w_down, const int32_t* offsets,
                         const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,

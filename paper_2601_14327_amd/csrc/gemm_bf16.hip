@@ -190,7 +190,7 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
 // Ring main loop: 256 x 256 tiles, 8 waves (2 x 4, each 128 x 64), k-steps
 // of 64 through a ring of five 32 KB halves.
 // ---------------------------------------------------------------------------
-template <int NWM, int NWN, int EPI, bool GU_ROWS>
+template <int NWM, int NWN, int EPI, bool GU_ROWS, bool GATHER>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams p) {
   constexpr int BM = 256, BN = 256;
   constexpr int NT = 64 * NWM * NWN;
@@ -225,7 +225,10 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
     const int r = q >> 3;
     const int lc = (q & 7) ^ swz8(r);
     const int rr = r < te.rows ? r : te.rows - 1;  // rows past the expert: any valid row
-    a_src[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
+    // gathered rows: the token row of routed row te.row0 + rr (dispatch folded in)
+    const long long arow = GATHER ? (long long)(p.row_src[te.row0 + rr] / p.slots_k)
+                                  : (long long)(te.row0 + rr);
+    a_src[i] = p.A + arow * p.lda + lc * 8;
     b_src[i] = Bw + (long long)weight_row<BN, GU_ROWS>(p, nt, r) * p.ldb + lc * 8;
   }
   const int nk = p.K / 64;
@@ -332,10 +335,11 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
 // ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
-template <int EPI, bool GU>
+template <int EPI, bool GU, bool GATHER = false>
 hipError_t launch_fwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU>), dim3(round8(grid)), dim3(512), 0, s, p);
+  hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU, GATHER>), dim3(round8(grid)), dim3(512), 0,
+                     s, p);
   return hipGetLastError();
 }
 
@@ -353,7 +357,7 @@ size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
 hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
-                               hipStream_t s) {
+                               hipStream_t s, const int32_t* row_src, int slots_k) {
   bf16_t* H = static_cast<bf16_t*>(ws);
   const int max_entries = ceil_div(R, kFwdBM) + E;
   TableWs tw = carve_table(static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256), max_entries);
@@ -376,7 +380,10 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.out = H;
   g.ldo = f;
   g.out2 = static_cast<bf16_t*>(act_save);
-  hipError_t err = launch_fwd<EPI_GU, true>(g, max_entries * g.n_tiles_n, s);
+  g.row_src = row_src;
+  g.slots_k = slots_k;
+  hipError_t err = row_src ? launch_fwd<EPI_GU, true, true>(g, max_entries * g.n_tiles_n, s)
+                           : launch_fwd<EPI_GU, true>(g, max_entries * g.n_tiles_n, s);
   if (err != hipSuccess) return err;
   // down projection
   g.A = H;
@@ -391,6 +398,7 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.out = static_cast<bf16_t*>(y_perm);
   g.ldo = d;
   g.out2 = nullptr;
+  g.row_src = nullptr;
   return launch_fwd<EPI_STORE, false>(g, max_entries * g.n_tiles_n, s);
 }
 

@@ -32,6 +32,8 @@ struct GemmParams {
   long long strideW;
   int accumulate;
   const bf16_t* zero;  // >= 1 KB of zeros (ragged-K tail loads of the weight gradient)
+  const int32_t* row_src;  // gathered A rows: row r of the product is A row row_src[r] / slots_k
+  int slots_k;
 };
 
 __device__ __forceinline__ void store_bf16x4(bf16_t* p, float a, float b, float c, float d) {

@@ -6,6 +6,9 @@ Forward (router path):
     -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
 Forward (given routing, one device's expert shard with k = 1):
     moe_expert_counts -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
+With fused dispatch (bf16 forward-only plans, the default there),
+moe_permute + moe_grouped_ffn_fwd become one moe_grouped_ffn_fwd_gather
+call that reads the token rows through row_src; x_perm is never written.
 Backward:
     moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
 
@@ -27,7 +30,7 @@ from ._lib import LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD
 class MoELayerPlan:
     def __init__(self, T: int, d_model: int, E: int, k: int, d_ff: int,
                  dtype: torch.dtype = torch.bfloat16, device="cuda", backward: bool = False,
-                 save_act: Optional[bool] = None):
+                 save_act: Optional[bool] = None, fused_dispatch: Optional[bool] = None):
         self.T, self.d, self.E, self.k, self.f = T, d_model, E, k, d_ff
         self.R = T * k
         self.dtype = dtype
@@ -42,10 +45,17 @@ class MoELayerPlan:
         self.dest_row = torch.empty(R, dtype=i32, device=dev)
         self.alive = torch.empty(E, dtype=torch.uint8, device=dev)
         self.n_pruned = torch.empty(1, dtype=i32, device=dev)
-        self.x_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
-        self.y_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
         # pre-activations are kept when a backward pass will read them (or on request)
         save_act = backward if save_act is None else save_act
+        # the dispatch folds into the FFN's operand loads unless x_perm is needed
+        # (the weight gradient reads it) or the dtype has no fused kernel
+        if fused_dispatch is None:
+            fused_dispatch = dtype == torch.bfloat16 and not backward and not save_act
+        self.fused = bool(fused_dispatch)
+        self.x_perm = (None if self.fused else
+                       torch.empty((R, d_model), dtype=dtype, device=dev))
+        self.row_src = torch.empty(R, dtype=i32, device=dev) if self.fused else None
+        self.y_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
         self.act_save = (torch.empty((R, 2 * d_ff), dtype=dtype, device=dev) if save_act
                          else None)
         self.out = torch.empty((T, d_model), dtype=dtype, device=dev)
@@ -72,17 +82,24 @@ class MoELayerPlan:
     def count(self, etn_accum=None):
         api.moe_expert_counts(self.topk_idx, self.E, ws=self.ws_counts, counts=self.counts,
                               offsets=self.offsets, dest_row=self.dest_row,
-                              etn_accum=etn_accum)
+                              row_src=self.row_src, etn_accum=etn_accum)
 
     def prune(self, beta: float, alpha: float = math.inf):
         api.laep_prune_mask(self.counts, self.T * self.k, alpha, beta, alive=self.alive,
                             n_pruned=self.n_pruned)
 
     def experts_and_combine(self, x, w_gate_up, w_down, expert_map=None):
-        api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
-        api.moe_grouped_ffn_fwd(self.x_perm, w_gate_up, w_down, self.offsets,
-                                expert_map=expert_map, ws=self.ws_ffn, y_perm=self.y_perm,
-                                save_act=self.act_save is not None, act_save=self.act_save)
+        if self.fused:
+            api.moe_grouped_ffn_fwd_gather(x, self.row_src, self.k, w_gate_up, w_down,
+                                           self.offsets, rows=self.R, expert_map=expert_map,
+                                           ws=self.ws_ffn, y_perm=self.y_perm,
+                                           save_act=self.act_save is not None,
+                                           act_save=self.act_save)
+        else:
+            api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
+            api.moe_grouped_ffn_fwd(self.x_perm, w_gate_up, w_down, self.offsets,
+                                    expert_map=expert_map, ws=self.ws_ffn, y_perm=self.y_perm,
+                                    save_act=self.act_save is not None, act_save=self.act_save)
         api.moe_combine(self.y_perm, self.topk_gate, self.dest_row, out=self.out)
         return self.out
 

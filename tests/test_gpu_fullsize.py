@@ -213,3 +213,30 @@ def test_shard_backward_full_size():
     # permute backward (k = 1: a gather back to token order)
     dx_tok = h32(plan.dx[torch.from_numpy(toks).cuda()])
     assert np.array_equal(dx_tok, h32(plan.dx_perm[torch.from_numpy(rows).cuda()]))
+
+
+@pytest.mark.parametrize("name", ["balanced", "shard"])
+def test_fused_dispatch_matches_unfused_full_size(name):
+    """The forward-only plan folds the dispatch into the FFN's operand loads;
+    its outputs must equal the permute + FFN chain's bit for bit."""
+    w = WORKLOADS[name]
+    c = cached(name)
+    x = dev(c["x"], BF)
+    wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
+    pf = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda")
+    pu = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda",
+                           fused_dispatch=False)
+    assert pf.fused and not pu.fused
+    case(f"full-size fused vs unfused dispatch ({name})")
+    if w.routed:
+        wr = dev(c["w_router"], BF)
+        of = pf.forward(x, wr, wgu, wd, renorm=w.renorm)
+        ou = pu.forward(x, wr, wgu, wd, renorm=w.renorm)
+    else:
+        idx = dev(c["topk_idx"], torch.int32)
+        gate = dev(c["topk_gate"], torch.float32)
+        of = pf.forward_given_routing(x, idx, gate, wgu, wd)
+        ou = pu.forward_given_routing(x, idx, gate, wgu, wd)
+    torch.cuda.synchronize()
+    assert torch.equal(pf.y_perm, pu.y_perm)
+    assert torch.equal(of, ou)

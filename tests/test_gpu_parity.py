@@ -243,6 +243,41 @@ def test_ffn_fwd_expert_map_with_pruned_slots():
     assert rownorm_err(host(y), ry) <= TOL_BF16
 
 
+@pytest.mark.parametrize("T,k,E,d,f,mapped", [
+    (300, 4, 8, 256, 128, False),    # ragged tiles, top-4
+    (257, 1, 3, 128, 256, False),    # one slot per token
+    (700, 8, 12, 192, 192, True),    # expert_map with unused slots, f % 128 = 64
+])
+def test_ffn_fwd_gather_matches_permute_then_ffn(T, k, E, d, f, mapped):
+    rng = np.random.default_rng(T + 13 * E)
+    c = random_case(T + E, T=T, d_model=d, E=E + 2 if mapped else E, k=1, d_ff=f, dtype="bf16")
+    # k distinct experts per token (as routing gives), expert E-1 never chosen
+    # (an empty expert) and expert 0 preferred (a heavy one)
+    w = np.r_[3.0, np.ones(E - 2), 0.0]
+    ids = np.stack([rng.choice(E, size=k, replace=False, p=w / w.sum()) for _ in range(T)])
+    bf = torch.bfloat16
+    x, wgu, wd = dev(c["x"], bf), dev(c["w_gate_up"], bf), dev(c["w_down"], bf)
+    emap = dev(np.array([(e + 2) if mapped else e for e in range(E)], np.int32), torch.int32) \
+        if mapped else None
+    idx = dev(ids.astype(np.int32), torch.int32)
+    case(f"ffn fwd gather T={T} k={k} E={E} d={d} f={f} mapped={mapped}")
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+    x_perm = laep.moe_permute(x, dest_row, k)
+    y1, a1 = laep.moe_grouped_ffn_fwd(x_perm, wgu, wd, offsets, expert_map=emap)
+    y2, a2 = laep.moe_grouped_ffn_fwd_gather(x, row_src, k, wgu, wd, offsets, expert_map=emap,
+                                            save_act=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+    assert torch.equal(a1, a2)
+    # and against the oracle's permute + grouped FFN
+    rc, ro, rd = om.expert_counts(ids, E)
+    xp = om.permute(c["x"], rd, k)
+    ry, ract = om.grouped_ffn_fwd(xp, c["w_gate_up"], c["w_down"], ro,
+                                  expert_map=host(emap) if mapped else None, dtype="bf16")
+    assert rownorm_err(host(y2), ry) <= TOL_BF16
+    assert rownorm_err(host(a2), ract) <= TOL_BF16
+
+
 @pytest.mark.parametrize("counts,d,f", [
     ([60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
     ([300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),
