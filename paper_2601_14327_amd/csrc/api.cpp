@@ -96,8 +96,10 @@ size_t moe_workspace_bytes(int which_call, int T, int k, int E, int d_model, int
     case LAEP_CALL_COUNTS:
       return laep::counts_ws_bytes(T, k, E);
     case LAEP_CALL_FFN_FWD: {
-      // large enough for either dtype: H in fp32 plus the tile table
-      return laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeF32);
+      // large enough for either dtype
+      const size_t a = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeF32);
+      const size_t b = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeBf16);
+      return a > b ? a : b;
     }
     case LAEP_CALL_FFN_BWD:
       return laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeBf16);

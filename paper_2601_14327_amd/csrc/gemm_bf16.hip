@@ -208,8 +208,8 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
 
   const int L = xcd_tile(p);
   if (L < 0) return;
-  const TileEntry te = p.table[L / p.tiles_per_entry];
-  const int nt = L % p.tiles_per_entry;
+  const TileEntry te = p.table[L];  // per-tile list (tiles_per_entry == 1)
+  const int nt = te.nt;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -347,11 +347,18 @@ constexpr int kFwdBM = 256, kFwdBN = 256;
 
 }  // namespace
 
+// bf16 workspace: H [R, f], then the per-tile lists of the two products
+namespace {
+inline int fwd_list_max(int64_t R, int E, int n_tiles) { return (ceil_div(R, kFwdBM) + E) * n_tiles; }
+}  // namespace
+
 size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
-  (void)d;
-  const size_t elem = dtype == kDtypeBf16 ? 2 : 4;
-  // the table is sized for the smallest row tile of either dtype (64 rows)
-  return align_up((size_t)R * f * elem, 256) + table_bytes(ceil_div(R, 64) + E);
+  if (dtype == kDtypeBf16)
+    return align_up((size_t)R * f * 2, 256) +
+           table_bytes(fwd_list_max(R, E, ceil_div(f, kFwdBN / 2))) +
+           table_bytes(fwd_list_max(R, E, ceil_div(d, kFwdBN)));
+  // fp32: H, then one entry per 64-row tile
+  return align_up((size_t)R * f * 4, 256) + table_bytes(ceil_div(R, 64) + E);
 }
 
 hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
@@ -359,13 +366,18 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
                                hipStream_t s, const int32_t* row_src, int slots_k) {
   bf16_t* H = static_cast<bf16_t*>(ws);
-  const int max_entries = ceil_div(R, kFwdBM) + E;
-  TableWs tw = carve_table(static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256), max_entries);
-  hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
-                     E, kFwdBM, 0, max_entries, tw.n_entries, tw.table);
+  const int nt_gu = ceil_div(f, kFwdBN / 2), nt_d = ceil_div(d, kFwdBN);
+  const int max_gu = fwd_list_max(R, E, nt_gu), max_d = fwd_list_max(R, E, nt_d);
+  char* tables = static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256);
+  TableWs tgu = carve_table(tables, max_gu);
+  TableWs td = carve_table(tables + table_bytes(max_gu), max_d);
+  TileList lgu = {nt_gu, 2 * f, max_gu, tgu.n_entries, tgu.table};
+  TileList ld = {nt_d, d, max_d, td.n_entries, td.table};
+  hipLaunchKernelGGL(build_tile_lists_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets,
+                     expert_map, E, kFwdBM, lgu, ld);
   GemmParams g = {};
-  g.table = tw.table;
-  g.n_entries = tw.n_entries;
+  g.table = tgu.table;
+  g.n_entries = tgu.n_entries;
   g.f = f;
   // gate/up + SwiGLU: B rows interleaved gate/up per 32, BN/2 f-columns per tile
   g.A = static_cast<const bf16_t*>(x_perm);
@@ -375,17 +387,19 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.strideB = (long long)2 * f * d;
   g.N = 2 * f;
   g.K = d;
-  g.n_tiles_n = ceil_div(f, kFwdBN / 2);
-  g.tiles_per_entry = g.n_tiles_n;
+  g.n_tiles_n = nt_gu;
+  g.tiles_per_entry = 1;
   g.out = H;
   g.ldo = f;
   g.out2 = static_cast<bf16_t*>(act_save);
   g.row_src = row_src;
   g.slots_k = slots_k;
-  hipError_t err = row_src ? launch_fwd<EPI_GU, true, true>(g, max_entries * g.n_tiles_n, s)
-                           : launch_fwd<EPI_GU, true>(g, max_entries * g.n_tiles_n, s);
+  hipError_t err = row_src ? launch_fwd<EPI_GU, true, true>(g, max_gu, s)
+                           : launch_fwd<EPI_GU, true>(g, max_gu, s);
   if (err != hipSuccess) return err;
   // down projection
+  g.table = td.table;
+  g.n_entries = td.n_entries;
   g.A = H;
   g.lda = f;
   g.B = static_cast<const bf16_t*>(w_d);
@@ -393,13 +407,13 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.strideB = (long long)d * f;
   g.N = d;
   g.K = f;
-  g.n_tiles_n = ceil_div(d, kFwdBN);
-  g.tiles_per_entry = g.n_tiles_n;
+  g.n_tiles_n = nt_d;
+  g.tiles_per_entry = 1;
   g.out = static_cast<bf16_t*>(y_perm);
   g.ldo = d;
   g.out2 = nullptr;
   g.row_src = nullptr;
-  return launch_fwd<EPI_STORE, false>(g, max_entries * g.n_tiles_n, s);
+  return launch_fwd<EPI_STORE, false>(g, max_d, s);
 }
 
 }  // namespace laep

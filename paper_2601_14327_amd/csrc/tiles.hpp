@@ -13,6 +13,7 @@ struct TileEntry {
   int rows;    // rows in this tile (ragged) / rows of the expert (wgrad)
   int expert;  // logical expert
   int phys;    // weight slot
+  int nt;      // output column block (per-tile lists only)
 };
 
 // ---------------------------------------------------------------------------
@@ -76,6 +77,7 @@ __global__ __launch_bounds__(kTableThreads) void build_table_kernel(
         te.rows = min(BM, rows - i * BM);
         te.expert = e;
         te.phys = phys;
+        te.nt = 0;
         table[pos] = te;
       }
     }
@@ -88,10 +90,59 @@ __global__ __launch_bounds__(kTableThreads) void build_table_kernel(
       te.rows = rows;
       te.expert = e;
       te.phys = phys;
+      te.nt = 0;
       table[start] = te;
     }
     int tot = block_excl_scan_256(cnt, s_tmp) + cnt;
     if (e == kTableThreads - 1) *n_entries = min(tot, max_entries);
+  }
+}
+
+// Per-tile lists of two row-tile products (one launch): every (row tile,
+// column block) of every expert with rows, experts in order.  Within an expert
+// the tiles run column-block-major when the expert has fewer rows than the
+// product has output columns, so the tiles that run together share one weight
+// panel and the smaller activation panels are the ones fetched again when an
+// expert's tiles span two rounds of workgroups; row-tile-major otherwise.
+struct TileList {
+  int n_tiles;     // column blocks of the product
+  int order_rows;  // experts with rows < order_rows go column-block-major
+  int max_entries;
+  int* n_entries;
+  TileEntry* table;
+};
+
+__global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
+    const int32_t* __restrict__ offsets, const int32_t* __restrict__ expert_map, int E, int BM,
+    TileList la, TileList lb) {
+  __shared__ int s_tmp[4];
+  const int e = threadIdx.x;
+  int rows = 0, phys = -1;
+  if (e < E) {
+    rows = offsets[e + 1] - offsets[e];
+    phys = expert_map ? expert_map[e] : e;
+  }
+  const int mt = (e < E && phys >= 0 && rows > 0) ? (rows + BM - 1) / BM : 0;
+  for (int which = 0; which < 2; ++which) {
+    const TileList& L = which == 0 ? la : lb;
+    const int cnt = mt * L.n_tiles;
+    const int start = block_excl_scan_256(cnt, s_tmp);
+    const bool col_major = rows < L.order_rows;
+    for (int i = 0; i < cnt; ++i) {
+      const int pos = start + i;
+      if (pos >= L.max_entries) break;
+      const int m = col_major ? i % mt : i / L.n_tiles;
+      const int n = col_major ? i / mt : i % L.n_tiles;
+      TileEntry te;
+      te.row0 = offsets[e] + m * BM;
+      te.rows = min(BM, rows - m * BM);
+      te.expert = e;
+      te.phys = phys;
+      te.nt = n;
+      L.table[pos] = te;
+    }
+    const int total = block_excl_scan_256(cnt, s_tmp) + cnt;
+    if (e == kTableThreads - 1) *L.n_entries = min(total, L.max_entries);
   }
 }
 
