@@ -371,8 +371,10 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   char* tables = static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256);
   TableWs tgu = carve_table(tables, max_gu);
   TableWs td = carve_table(tables + table_bytes(max_gu), max_d);
-  TileList lgu = {nt_gu, 2 * f, max_gu, tgu.n_entries, tgu.table};
-  TileList ld = {nt_d, d, max_d, td.n_entries, td.table};
+  // default: all row tiles of an expert in one group (column-block-major)
+  const int group = tile_group("LAEP_TILE_GROUP_FWD", 1 << 20);
+  TileList lgu = {nt_gu, group, max_gu, tgu.n_entries, tgu.table};
+  TileList ld = {nt_d, group, max_d, td.n_entries, td.table};
   hipLaunchKernelGGL(build_tile_lists_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets,
                      expert_map, E, kFwdBM, lgu, ld);
   GemmParams g = {};

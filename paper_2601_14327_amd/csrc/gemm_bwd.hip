@@ -117,10 +117,26 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     L = (blockIdx.x & 7) * per + slot;
   }
   if (L >= n_valid) return;
-  const TileEntry te = p.table[L / p.tiles_per_entry];
-  const int rem = L % p.tiles_per_entry;
-  const int mt = (EPI == EPI_WGRAD) ? rem / p.n_tiles_n : 0;
-  const int nt = (EPI == EPI_WGRAD) ? rem % p.n_tiles_n : rem;
+  // Tiles are rasterised in groups of p.group row tiles (column blocks in
+  // the middle, the group's row tiles innermost), so the workgroups running
+  // together touch few operand panels: row-tile products over the table's
+  // row-tile entries, weight gradients over each expert's output tiles.
+  int entry, mt, nt;
+  if (EPI == EPI_WGRAD) {
+    entry = L / p.tiles_per_entry;
+    int m, n;
+    grouped_tile(L % p.tiles_per_entry, p.tiles_per_entry / p.n_tiles_n, p.n_tiles_n, p.group,
+                 m, n);
+    mt = m;
+    nt = n;
+  } else {
+    int m, n;
+    grouped_tile(L, *p.n_entries, p.n_tiles_n, p.group, m, n);
+    entry = m;
+    mt = 0;
+    nt = n;
+  }
+  const TileEntry te = p.table[entry];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -463,7 +479,9 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                      kZeroBytes / 4);
 
   // dgrad 1: dH = dY W_d, SwiGLU backward epilogue -> dA, H_b
+  const int group = tile_group("LAEP_TILE_GROUP_BWD", 8);
   GemmParams g = {};
+  g.group = group;
   g.table = tr.table;
   g.n_entries = tr.n_entries;
   g.f = f;
@@ -502,6 +520,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
 
   // wgrad W_d: dW_d[p] [d, f] = dY^T H_b over the expert's rows
   GemmParams w = {};
+  w.group = group;
   w.table = te.table;
   w.n_entries = te.n_entries;
   w.f = f;

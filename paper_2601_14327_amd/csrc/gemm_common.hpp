@@ -5,6 +5,8 @@
 #include "internal.hpp"
 #include "tiles.hpp"
 
+#include <cstdlib>
+
 namespace laep {
 namespace {
 
@@ -34,7 +36,16 @@ struct GemmParams {
   const bf16_t* zero;  // >= 1 KB of zeros (ragged-K tail loads of the weight gradient)
   const int32_t* row_src;  // gathered A rows: row r of the product is A row row_src[r] / slots_k
   int slots_k;
+  int group;               // row tiles per rasterisation group (backward products)
 };
+
+// Row tiles per rasterisation group of the tile orders: `fallback` unless the
+// environment variable `name` holds a positive integer (a tuning override).
+inline int tile_group(const char* name, int fallback) {
+  const char* v = getenv(name);
+  const int g = v ? atoi(v) : 0;
+  return g > 0 ? g : fallback;
+}
 
 __device__ __forceinline__ void store_bf16x4(bf16_t* p, float a, float b, float c, float d) {
   u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};

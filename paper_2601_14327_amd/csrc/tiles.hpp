@@ -100,17 +100,26 @@ __global__ __launch_bounds__(kTableThreads) void build_table_kernel(
 
 // Per-tile lists of two row-tile products (one launch): every (row tile,
 // column block) of every expert with rows, experts in order.  Within an expert
-// the tiles run column-block-major when the expert has fewer rows than the
-// product has output columns, so the tiles that run together share one weight
-// panel and the smaller activation panels are the ones fetched again when an
-// expert's tiles span two rounds of workgroups; row-tile-major otherwise.
+// the tiles are rasterised in groups of `group` row tiles: column blocks in
+// the middle loop, the group's row tiles innermost.  The workgroups that run
+// together (a contiguous run of the list on one XCD) then touch about
+// group + 32/group operand panels instead of 2 + 16 or 16 + 2, which is what
+// each k-step has to bring into that XCD's L2.
 struct TileList {
   int n_tiles;     // column blocks of the product
-  int order_rows;  // experts with rows < order_rows go column-block-major
+  int group;       // row tiles per rasterisation group
   int max_entries;
   int* n_entries;
   TileEntry* table;
 };
+
+__device__ __forceinline__ void grouped_tile(int i, int mt, int n_tiles, int group, int& m, int& n) {
+  const int per_group = group * n_tiles;
+  const int g = i / per_group, r = i % per_group;
+  const int gsize = min(group, mt - g * group);  // the last group may be short
+  n = r / gsize;
+  m = g * group + r % gsize;
+}
 
 __global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ expert_map, int E, int BM,
@@ -127,12 +136,11 @@ __global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
     const TileList& L = which == 0 ? la : lb;
     const int cnt = mt * L.n_tiles;
     const int start = block_excl_scan_256(cnt, s_tmp);
-    const bool col_major = rows < L.order_rows;
     for (int i = 0; i < cnt; ++i) {
       const int pos = start + i;
       if (pos >= L.max_entries) break;
-      const int m = col_major ? i % mt : i / L.n_tiles;
-      const int n = col_major ? i / mt : i % L.n_tiles;
+      int m, n;
+      grouped_tile(i, mt, L.n_tiles, L.group, m, n);
       TileEntry te;
       te.row0 = offsets[e] + m * BM;
       te.rows = min(BM, rows - m * BM);
