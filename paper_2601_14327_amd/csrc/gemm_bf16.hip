@@ -375,8 +375,9 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   const int group = tile_group("LAEP_TILE_GROUP_FWD", 1 << 20);
   TileList lgu = {nt_gu, group, max_gu, tgu.n_entries, tgu.table};
   TileList ld = {nt_d, group, max_d, td.n_entries, td.table};
-  hipLaunchKernelGGL(build_tile_lists_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets,
-                     expert_map, E, kFwdBM, lgu, ld);
+  const int list_blocks = ceil_div(max_gu > max_d ? max_gu : max_d, kTableThreads);
+  hipLaunchKernelGGL(build_tile_lists_kernel, dim3(list_blocks), dim3(kTableThreads), 0, s,
+                     offsets, expert_map, E, kFwdBM, lgu, ld);
   GemmParams g = {};
   g.table = tgu.table;
   g.n_entries = tgu.n_entries;

@@ -121,10 +121,19 @@ __device__ __forceinline__ void grouped_tile(int i, int mt, int n_tiles, int gro
   m = g * group + r % gsize;
 }
 
+// One thread per tile: every workgroup recomputes the per-expert tile starts
+// (E <= 256, one LDS scan) and writes the tiles of its own range of the list,
+// finding each tile's expert by binary search over the starts.  Launch with
+// enough workgroups to cover the larger list's max_entries.
 __global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
     const int32_t* __restrict__ offsets, const int32_t* __restrict__ expert_map, int E, int BM,
     TileList la, TileList lb) {
   __shared__ int s_tmp[4];
+  __shared__ int s_start[kTableThreads + 1];
+  __shared__ int s_mt[kTableThreads];
+  __shared__ int s_phys[kTableThreads];
+  __shared__ int s_row0[kTableThreads];
+  __shared__ int s_rows[kTableThreads];
   const int e = threadIdx.x;
   int rows = 0, phys = -1;
   if (e < E) {
@@ -132,25 +141,39 @@ __global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
     phys = expert_map ? expert_map[e] : e;
   }
   const int mt = (e < E && phys >= 0 && rows > 0) ? (rows + BM - 1) / BM : 0;
+  s_mt[e] = mt;
+  s_phys[e] = phys;
+  s_row0[e] = e < E ? offsets[e] : 0;
+  s_rows[e] = rows;
   for (int which = 0; which < 2; ++which) {
     const TileList& L = which == 0 ? la : lb;
     const int cnt = mt * L.n_tiles;
-    const int start = block_excl_scan_256(cnt, s_tmp);
-    for (int i = 0; i < cnt; ++i) {
-      const int pos = start + i;
-      if (pos >= L.max_entries) break;
+    const int start = block_excl_scan_256(cnt, s_tmp);  // (synchronises the block)
+    s_start[e] = start;
+    if (e == kTableThreads - 1) s_start[kTableThreads] = start + cnt;
+    __syncthreads();
+    const int total = s_start[kTableThreads];
+    if (blockIdx.x == 0 && e == 0) *L.n_entries = min(total, L.max_entries);
+    const int i = blockIdx.x * kTableThreads + e;
+    if (i < total && i < L.max_entries) {
+      int lo = 0, hi = kTableThreads - 1;  // last expert with start <= i
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_start[mid] <= i) lo = mid;
+        else hi = mid - 1;
+      }
+      const int x = lo;  // experts with no tiles share a start; the last of them has tiles
       int m, n;
-      grouped_tile(i, mt, L.n_tiles, L.group, m, n);
+      grouped_tile(i - s_start[x], s_mt[x], L.n_tiles, L.group, m, n);
       TileEntry te;
-      te.row0 = offsets[e] + m * BM;
-      te.rows = min(BM, rows - m * BM);
-      te.expert = e;
-      te.phys = phys;
+      te.row0 = s_row0[x] + m * BM;
+      te.rows = min(BM, s_rows[x] - m * BM);
+      te.expert = x;
+      te.phys = s_phys[x];
       te.nt = n;
-      L.table[pos] = te;
+      L.table[i] = te;
     }
-    const int total = block_excl_scan_256(cnt, s_tmp) + cnt;
-    if (e == kTableThreads - 1) *L.n_entries = min(total, L.max_entries);
+    __syncthreads();  // s_start is rewritten for the second list
   }
 }
 
