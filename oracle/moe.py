@@ -95,6 +95,57 @@ def route(x, w_router, k, bias=None, alive=None, renorm=True):
     return idx, gate, margin, logits
 
 
+def route_bwd(dgate, idx, gate, x, w_router, logits=None, alive=None, renorm: bool = True,
+              dtype: str = "bf16", dx_in=None):
+    """Backward of router scoring and gating with the selection held fixed
+    (the top-k choice is piecewise constant in the logits, so no gradient
+    flows through it).
+
+    dl[t, e] = dLoss/dlogits[t, e] for dLoss/dgate[t, j] = dgate[t, j]:
+      renorm:      the gates are a softmax over the k selected logits, so for
+                   e = idx[t, j]:  dl = g_j (dg_j - sum_i g_i dg_i); 0 elsewhere.
+      full softmax: the gates are p_e at the selected experts, p = softmax over
+                   the alive logits; with q_e = dg_j at e = idx[t, j] (0 for
+                   the other experts):  dl_e = p_e (q_e - sum_j g_j dg_j) for
+                   alive e; 0 for dead ones.  Needs the logits.
+    dW_r = dl^T x and db = sum_t dl (float32);
+    dx = round_dtype(dx_in + dl W_r)  (dx_in = 0 when not given).
+    Slots with idx = -1 carry no gradient.
+    Returns (dl rounded to float32 [T, E], dW_r [E, d], db [E], dx [T, d]).
+    """
+    dgate = np.asarray(dgate, F64)
+    idx = np.asarray(idx)
+    gate = np.asarray(gate, F64)
+    x = np.asarray(x, F64)
+    w = np.asarray(w_router, F64)
+    T, k = idx.shape
+    E = w.shape[0]
+    ok = idx >= 0
+    s = np.sum(np.where(ok, gate * dgate, 0.0), axis=1)          # sum_j g_j dg_j
+    dl = np.zeros((T, E), F64)
+    if renorm:
+        tt, jj = np.nonzero(ok)
+        dl[tt, idx[tt, jj]] = gate[tt, jj] * (dgate[tt, jj] - s[tt])
+    else:
+        l = round_f32(np.asarray(logits, F64))
+        alive_m = np.ones(E, bool) if alive is None else np.asarray(alive).astype(bool)
+        masked = np.where(alive_m[None, :], l, -np.inf)
+        top = masked.max(axis=1, keepdims=True)
+        ex = np.where(alive_m[None, :], np.exp(masked - top), 0.0)
+        p = ex / ex.sum(axis=1, keepdims=True)
+        q = np.zeros((T, E), F64)
+        tt, jj = np.nonzero(ok)
+        q[tt, idx[tt, jj]] = dgate[tt, jj]
+        dl = np.where(alive_m[None, :], p * (q - s[:, None]), 0.0)
+    dl = round_f32(dl)
+    dw = round_f32(dl.T @ x)
+    db = round_f32(dl.sum(axis=0))
+    dx = dl @ w
+    if dx_in is not None:
+        dx = dx + np.asarray(dx_in, F64)
+    return dl, dw, db, rounder(dtype)(dx)
+
+
 # --------------------------------------------------------------------------
 # Per-expert token histogram, offsets and the dispatch permutation
 # --------------------------------------------------------------------------
