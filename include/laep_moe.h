@@ -65,6 +65,7 @@ extern "C" {
 #define LAEP_CALL_COUNTS 1
 #define LAEP_CALL_FFN_FWD 2
 #define LAEP_CALL_FFN_BWD 3
+#define LAEP_CALL_ROUTE_BWD 4
 
 /* Limits of this build. */
 #define LAEP_MAX_EXPERTS 256
@@ -140,6 +141,43 @@ int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E,
 int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha,
                     double beta, uint8_t* alive, int32_t* n_pruned,
                     void* stream);
+
+/*
+ * moe_route_bwd -- backward of moe_route's scoring and gating, with the
+ * top-k selection held fixed (it is piecewise constant in the logits; the
+ * paper trains through the router, Section 3.1, and does not define this
+ * step further).  From dgate = dLoss/dgate:
+ *
+ *   renorm = 1 (softmax over the k selected logits), for e = topk_idx[t, j]:
+ *     dl[t, e] = g_j * (dg_j - sum_i g_i dg_i),    0 for the other experts
+ *   renorm = 0 (softmax over the alive experts, p = that softmax):
+ *     dl[t, e] = p_e * (q_e - sum_j g_j dg_j) for alive e, 0 for dead ones,
+ *     with q_e = dg_j where e = topk_idx[t, j], 0 elsewhere
+ *   dlogits[t, e] = dl[t, e]                         (optional, float32)
+ *   dw_router[e] = sum_t dl[t, e] x[t]                (float32, overwritten)
+ *   dbias[e]     = sum_t dl[t, e]                     (optional, float32)
+ *   dx[t]        = round(dx[t] + sum_e dl[t, e] W_r[e])  (accumulate_dx = 1)
+ *                  round(sum_e dl[t, e] W_r[e])            (accumulate_dx = 0)
+ *   Slots with topk_idx == -1 carry no gradient.  Sums are fp32 in a fixed
+ *   order (deterministic, no atomics).
+ *
+ *   dgate, topk_gate device [T, k] float32; topk_idx device [T, k] int32
+ *   (as moe_route wrote them); x device [T, d_model] dtype; w_router device
+ *   [E, d_model] dtype; dx device [T, d_model] dtype.
+ *   renorm = 1 needs offsets [E + 1] and row_src [T * k] from
+ *   moe_expert_counts on the same topk_idx (dw_router is summed over each
+ *   expert's routed rows in that order); logits and alive may be NULL.
+ *   renorm = 0 needs logits [T, E] (moe_route's float32 logits output) and
+ *   the alive mask moe_route used (NULL = all alive).
+ *   Workspace: moe_workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, 0, 0).
+ */
+int moe_route_bwd(const float* dgate, const int32_t* topk_idx,
+                  const float* topk_gate, const float* logits,
+                  const uint8_t* alive, const void* x, const void* w_router,
+                  const int32_t* offsets, const int32_t* row_src, int dtype,
+                  int T, int d_model, int E, int k, int renorm, float* dlogits,
+                  float* dw_router, float* dbias, void* dx, int accumulate_dx,
+                  void* ws, size_t ws_bytes, void* stream);
 
 /*
  * moe_permute -- dispatch: x_perm[dest_row[t*k + j]] = x[t] (a copy; slots

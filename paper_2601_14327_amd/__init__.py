@@ -11,6 +11,7 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     moe_grouped_ffn_fwd_gather   the same with the dispatch folded into the operand loads
     moe_combine          gate-weighted combine
     moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
+    moe_route_bwd        router / gate backward (softmax Jacobian, dW_r, dx)
     laep_rearrange       host utility: balanced expert placement
     laep_calib_copy, laep_calib_mfma   measurement kernels (attained peaks)
 """
@@ -30,6 +31,7 @@ from .api import (  # noqa: F401
     moe_permute,
     moe_permute_bwd,
     moe_route,
+    moe_route_bwd,
     workspace_bytes,
 )
 from .layer import MoELayerPlan, layer_forward  # noqa: F401

@@ -19,6 +19,7 @@ LAEP_CALL_ROUTE = 0
 LAEP_CALL_COUNTS = 1
 LAEP_CALL_FFN_FWD = 2
 LAEP_CALL_FFN_BWD = 3
+LAEP_CALL_ROUTE_BWD = 4
 
 ERROR_NAMES = {
     1: "LAEP_ERR_INVALID_ARG",
@@ -47,6 +48,8 @@ _d = ctypes.c_double
 # name -> (restype, argtypes)
 SIGNATURES = {
     "moe_route": (_i, [_p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _sz, _p]),
+    "moe_route_bwd": (_i, [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p,
+                           _p, _p, _i, _p, _sz, _p]),
     "moe_expert_counts": (_i, [_p, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "laep_prune_mask": (_i, [_p, _i, _i64, _d, _d, _p, _p, _p]),
     "moe_permute": (_i, [_p, _i, _p, _i, _i, _i, _p, _p]),

@@ -13,7 +13,7 @@ from typing import Optional, Tuple
 import torch
 
 from ._lib import (LAEP_BF16, LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD,
-                   LAEP_F32, LaepError, check, lib)
+                   LAEP_CALL_ROUTE_BWD, LAEP_F32, LaepError, check, lib)
 
 _DT = {torch.float32: LAEP_F32, torch.bfloat16: LAEP_BF16}
 
@@ -73,6 +73,35 @@ def moe_route(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=None, ali
                           E, k, int(renorm), _ptr(logits), _ptr(topk_idx), _ptr(topk_gate), None,
                           0, _stream(dev)))
     return (topk_idx, topk_gate, logits) if want_logits else (topk_idx, topk_gate)
+
+
+def moe_route_bwd(dgate: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor,
+                  x: torch.Tensor, w_router: torch.Tensor, *, renorm: bool = True,
+                  logits=None, alive=None, offsets=None, row_src=None, dx=None,
+                  accumulate_dx: bool = False, want_dlogits: bool = False,
+                  want_dbias: bool = False, dw_router=None, dlogits=None, dbias=None, ws=None):
+    """Router/gate backward with the selection fixed.
+    Returns (dx, dw_router, dbias or None, dlogits or None)."""
+    for t, n in ((dgate, "dgate"), (topk_idx, "topk_idx"), (topk_gate, "topk_gate"), (x, "x"),
+                 (w_router, "w_router")):
+        _dev(t, n)
+    T, k = topk_idx.shape
+    E, d = w_router.shape
+    dev = x.device
+    dx = torch.zeros_like(x) if dx is None else dx
+    dw_router = (torch.empty((E, d), dtype=torch.float32, device=dev) if dw_router is None
+                 else dw_router)
+    if want_dlogits and dlogits is None:
+        dlogits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    if want_dbias and dbias is None:
+        dbias = torch.empty(E, dtype=torch.float32, device=dev)
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E), dev)
+    check(lib().moe_route_bwd(_ptr(dgate), _ptr(topk_idx), _ptr(topk_gate), _ptr(logits),
+                              _ptr(alive), _ptr(x), _ptr(w_router), _ptr(offsets), _ptr(row_src),
+                              _dtype_code(x), T, d, E, k, int(renorm), _ptr(dlogits),
+                              _ptr(dw_router), _ptr(dbias), _ptr(dx), int(accumulate_dx),
+                              _ptr(ws), ws.numel(), _stream(dev)))
+    return dx, dw_router, dbias, dlogits
 
 
 def moe_expert_counts(topk_idx: torch.Tensor, E: int, *, want_row_src: bool = False,

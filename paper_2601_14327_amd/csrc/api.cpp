@@ -103,6 +103,8 @@ size_t moe_workspace_bytes(int which_call, int T, int k, int E, int d_model, int
     }
     case LAEP_CALL_FFN_BWD:
       return laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeBf16);
+    case LAEP_CALL_ROUTE_BWD:
+      return laep::route_bwd_ws_bytes(T, k, E);
     default:
       return 0;
   }
@@ -165,6 +167,40 @@ int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha, d
   return hip_status(
       laep::launch_prune(counts, E, total, alpha, beta, alive, n_pruned, as_stream(stream)),
       "laep_prune_mask");
+}
+
+int moe_route_bwd(const float* dgate, const int32_t* topk_idx, const float* topk_gate,
+                  const float* logits, const uint8_t* alive, const void* x, const void* w_router,
+                  const int32_t* offsets, const int32_t* row_src, int dtype, int T, int d_model,
+                  int E, int k, int renorm, float* dlogits, float* dw_router, float* dbias,
+                  void* dx, int accumulate_dx, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  if ((rc = check_experts(E, k))) return rc;
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  REQUIRE(w_router && dw_router, LAEP_ERR_INVALID_ARG,
+          "moe_route_bwd: w_router and dw_router must be non-null");
+  REQUIRE(aligned16(w_router) && aligned16(dw_router), LAEP_ERR_INVALID_ARG,
+          "moe_route_bwd: w_router and dw_router must be 16-byte aligned");
+  if (T > 0) {
+    REQUIRE(dgate && topk_idx && topk_gate && x && dx && ws, LAEP_ERR_INVALID_ARG,
+            "moe_route_bwd: dgate, topk_idx, topk_gate, x, dx and ws must be non-null");
+    REQUIRE(aligned16(x) && aligned16(dx), LAEP_ERR_INVALID_ARG,
+            "moe_route_bwd: x and dx must be 16-byte aligned");
+    if (renorm)
+      REQUIRE(offsets && row_src, LAEP_ERR_INVALID_ARG,
+              "moe_route_bwd: renorm = 1 needs offsets and row_src from moe_expert_counts");
+    else
+      REQUIRE(logits, LAEP_ERR_INVALID_ARG, "moe_route_bwd: renorm = 0 needs the logits");
+    const size_t need = laep::route_bwd_ws_bytes(T, k, E);
+    REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_route_bwd: workspace %zu < %zu bytes",
+            ws_bytes, need);
+  }
+  return hip_status(laep::launch_route_bwd(dgate, topk_idx, topk_gate, logits, alive, x, w_router,
+                                           offsets, row_src, dtype, T, d_model, E, k, renorm,
+                                           dlogits, dw_router, dbias, dx, accumulate_dx, ws,
+                                           as_stream(stream)),
+                    "moe_route_bwd");
 }
 
 int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T, int k, int d_model,

@@ -54,6 +54,15 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                                void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
                                void* ws, hipStream_t s);
 
+// Router backward.
+size_t route_bwd_ws_bytes(int T, int k, int E);
+hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float* gate,
+                            const float* logits, const uint8_t* alive, const void* x,
+                            const void* w_router, const int32_t* offsets, const int32_t* row_src,
+                            int dtype, int T, int d, int E, int k, int renorm, float* dlogits,
+                            float* dw_router, float* dbias, void* dx, int accumulate_dx, void* ws,
+                            hipStream_t s);
+
 // Measurement kernels (laep_calib.h).
 hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_calib_mfma(int n_workgroups, int iters, float* out, hipStream_t s);

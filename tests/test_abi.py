@@ -118,6 +118,26 @@ def test_ffn_validation(L):
                                         p, 1 << 30, None) == 1
 
 
+def test_route_bwd_validation(L):
+    keep, p = _fake()
+    args = lambda **kw: dict(dict(dgate=p, idx=p, gate=p, logits=None, alive=None, x=p, w=p,
+                                  offsets=p, row_src=p, dtype=1, T=16, d=64, E=8, k=2, renorm=1,
+                                  dl=None, dw=p, db=None, dx=p, acc=0, ws=p, wsb=1 << 20), **kw)
+    call = lambda a: L.moe_route_bwd(a["dgate"], a["idx"], a["gate"], a["logits"], a["alive"],
+                                     a["x"], a["w"], a["offsets"], a["row_src"], a["dtype"],
+                                     a["T"], a["d"], a["E"], a["k"], a["renorm"], a["dl"],
+                                     a["dw"], a["db"], a["dx"], a["acc"], a["ws"], a["wsb"], None)
+    assert call(args(row_src=None)) == 1          # renorm needs the dispatch order
+    assert "row_src" in _err(L)
+    assert call(args(renorm=0)) == 1              # full softmax needs the logits
+    assert "logits" in _err(L)
+    assert call(args(dtype=5)) == 2
+    assert call(args(k=9)) == 1
+    assert call(args(wsb=16)) == 3
+    need = L.moe_workspace_bytes(4, 16, 2, 8, 0, 0)
+    assert need >= 16 * 8 * 4
+
+
 def test_calib_validation(L):
     keep, p = _fake()
     assert L.laep_calib_copy(p, p + 2, 64, None) == 1

@@ -354,3 +354,42 @@ def test_determinism():
     torch.cuda.synchronize()
     assert torch.equal(o1, o2)
     assert torch.equal(p1.act_save, p2.act_save)
+
+
+# ---------------------------------------------------------------------------
+# router / gate backward (teacher-forced on the GPU's routing)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("T,d,E,k,dtype,renorm,bias,dead", [
+    (500, 256, 16, 4, "bf16", True, 0.0, 0),       # renormalised gates
+    (256, 128, 8, 2, "f32", False, 0.0, 0),        # tiny layer: full-softmax gates
+    (333, 192, 12, 5, "bf16", True, 1.0, 8),       # 4 alive of 12, k = 5: unroutable slots
+    (300, 128, 10, 3, "bf16", False, 0.5, 3),      # full softmax with dead experts
+])
+def test_route_bwd_parity(T, d, E, k, dtype, renorm, bias, dead):
+    c = random_case(T + 17 * E, T=T, d_model=d, E=E, k=k, d_ff=64, dtype=dtype, bias_std=bias)
+    td = TD[dtype]
+    rng = np.random.default_rng(T)
+    alive_np = np.ones(E, bool)
+    alive_np[rng.choice(E, dead, replace=False)] = False
+    alive = dev(alive_np.astype(np.uint8), torch.uint8) if dead else None
+    x, wr = dev(c["x"], td), dev(c["w_router"], td)
+    b = dev(c["bias"], torch.float32) if "bias" in c else None
+    case(f"route bwd T={T} d={d} E={E} k={k} {dtype} renorm={renorm} dead={dead}")
+    idx, gate, logits = laep.moe_route(x, wr, k, bias=b, alive=alive, renorm=renorm,
+                                       want_logits=True)
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+    dg = dev(rng.standard_normal((T, k)).astype(np.float32), torch.float32)
+    dx_in = rng.standard_normal((T, d)).astype(np.float32)
+    dx = dev(dx_in, td)
+    dx_in = host(dx)   # the rounded values the GPU accumulates onto
+    dx, dw, db, dl = laep.moe_route_bwd(dg, idx, gate, x, wr, renorm=renorm, logits=logits,
+                                        alive=alive, offsets=offsets, row_src=row_src, dx=dx,
+                                        accumulate_dx=True, want_dlogits=True, want_dbias=True)
+    torch.cuda.synchronize()
+    rl, rw, rb, rx = om.route_bwd(host(dg), host(idx), host(gate), c["x"], c["w_router"],
+                                  logits=host(logits), alive=alive_np if dead else None,
+                                  renorm=renorm, dtype=dtype, dx_in=dx_in)
+    assert rownorm_err(host(dl), rl) <= TOL_F32
+    assert rownorm_err(host(dw), rw) <= TOL_F32
+    assert rownorm_err(host(db), rb) <= TOL_F32
+    assert rownorm_err(host(dx), rx) <= (TOL_BF16 if dtype == "bf16" else TOL_F32)
