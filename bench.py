@@ -24,7 +24,8 @@ Prints ONE JSON line:
   cpu_baseline the float64 CPU oracle timed on a bounded token sample
 
 Other workloads: skewed, skewed_mild (routed, pruned), shard (16 experts,
-given Zipf routing), shard_bwd (shard forward + backward).
+given Zipf routing), shard_bwd (shard forward + backward), balanced_bwd
+(balanced forward + backward through the combine, FFN, dispatch and router).
 
 Profiling helpers (used by the commands recorded under profiles/):
   --profile-target ffn|copy   run only that call a few times (for --pmc runs)
@@ -133,7 +134,7 @@ class Setup:
         else:
             self.idx = to(c["topk_idx"], torch.int32)
             self.gate = to(c["topk_gate"], torch.float32)
-            self.dout = to(c["dout"]) if w.backward else None
+        self.dout = to(c["dout"]) if w.backward else None
         self.laep = laep
 
     def calls(self, i):
@@ -181,6 +182,8 @@ class Setup:
                         dx_perm=p.dx_perm)),
                     ("permute_bwd", lambda: L.moe_permute_bwd(p.dx_perm, p.dest_row, w.T, w.k,
                                                               out=p.dx))]
+            if w.routed:   # router / gate backward, accumulated onto dx
+                out += [("route_bwd", lambda: p.route_backward(x, self.wr, renorm=w.renorm))]
         return out
 
     def algorithmic(self):
@@ -196,6 +199,8 @@ class Setup:
             "combine": R * d * e + T * d * e + 2 * R * 4,
             "combine_bwd": T * d * e + 2 * R * d * e + 3 * R * 4,
             "permute_bwd": R * d * e + T * d * e + R * 4,
+            # dx read + written, W_r once, x once (summed into dW_r), dgate/gates/ids, dW_r
+            "route_bwd": 2 * T * d * e + E * d * e + T * d * e + 3 * T * k * 4 + E * d * 4,
         }
         by["route_masked"], by["counts_masked"] = by["route"], by["counts"]
         fl = {"ffn_fwd": 6.0 * R * d * f, "ffn_bwd": 12.0 * R * d * f}

@@ -11,6 +11,7 @@ moe_permute + moe_grouped_ffn_fwd become one moe_grouped_ffn_fwd_gather
 call that reads the token rows through row_src; x_perm is never written.
 Backward:
     moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
+      [-> moe_route_bwd, accumulating the router's dx]   (router path)
 
 All buffers are allocated once, so a pass makes no allocation and no host
 synchronisation; every step runs in the library's kernels on the current
@@ -24,7 +25,7 @@ from typing import Optional
 import torch
 
 from . import api
-from ._lib import LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD
+from ._lib import LAEP_CALL_COUNTS, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD, LAEP_CALL_ROUTE_BWD
 
 
 class MoELayerPlan:
@@ -54,7 +55,10 @@ class MoELayerPlan:
         self.fused = bool(fused_dispatch)
         self.x_perm = (None if self.fused else
                        torch.empty((R, d_model), dtype=dtype, device=dev))
-        self.row_src = torch.empty(R, dtype=i32, device=dev) if self.fused else None
+        # the dispatch order is kept when the FFN gathers through it or the
+        # router backward sums dW_r over it
+        self.row_src = (torch.empty(R, dtype=i32, device=dev) if self.fused or backward
+                        else None)
         self.y_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
         self.act_save = (torch.empty((R, 2 * d_ff), dtype=dtype, device=dev) if save_act
                          else None)
@@ -73,6 +77,11 @@ class MoELayerPlan:
                 dtype=torch.uint8, device=dev)
             self.dw_gate_up = None
             self.dw_down = None
+            self.dw_router = None
+            self.dbias = None
+            self.ws_route_bwd = torch.empty(
+                max(1, api.workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E)), dtype=torch.uint8,
+                device=dev)
 
     # -- pieces --------------------------------------------------------------
     def route(self, x, w_router, bias=None, alive=None, renorm=True):
@@ -119,6 +128,21 @@ class MoELayerPlan:
         self.topk_gate.copy_(topk_gate)
         self.count()
         return self.experts_and_combine(x, w_gate_up, w_down)
+
+    def route_backward(self, x, w_router, renorm=True, want_dbias=False):
+        """Router / gate backward from self.dgate (the combine's gate gradient),
+        accumulated onto self.dx.  Renormalised gates only (the full-softmax
+        form needs the logits, which the plan does not keep)."""
+        if not renorm:
+            raise NotImplementedError("the plan keeps no logits; call moe_route_bwd directly")
+        if self.dw_router is None:
+            self.dw_router = torch.empty(w_router.shape, dtype=torch.float32, device=self.device)
+            self.dbias = torch.empty(self.E, dtype=torch.float32, device=self.device)
+        api.moe_route_bwd(self.dgate, self.topk_idx, self.topk_gate, x, w_router, renorm=True,
+                          offsets=self.offsets, row_src=self.row_src, dx=self.dx,
+                          accumulate_dx=True, dw_router=self.dw_router,
+                          dbias=self.dbias if want_dbias else None, ws=self.ws_route_bwd)
+        return self.dx, self.dw_router
 
     def backward(self, dout, w_gate_up, w_down, expert_map=None, accumulate=False):
         api.moe_combine_bwd(dout, self.y_perm, self.topk_gate, self.dest_row,

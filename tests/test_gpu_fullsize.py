@@ -240,3 +240,29 @@ def test_fused_dispatch_matches_unfused_full_size(name):
     torch.cuda.synchronize()
     assert torch.equal(pf.y_perm, pu.y_perm)
     assert torch.equal(of, ou)
+
+
+def test_routed_training_step_full_size():
+    """balanced_bwd: forward, the expert backward, then the router backward
+    accumulated onto dx; the router part is checked against the oracle,
+    teacher-forced on the GPU's routing, gate gradient and expert-path dx."""
+    w = WORKLOADS["balanced_bwd"]
+    c = cached("balanced_bwd")
+    x, wr = dev(c["x"], BF), dev(c["w_router"], BF)
+    wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
+    dout = dev(c["dout"], BF)
+    plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=BF, device="cuda",
+                             backward=True)
+    case("full-size routed training step (balanced_bwd)")
+    plan.forward(x, wr, wgu, wd, renorm=w.renorm)
+    plan.backward(dout, wgu, wd)
+    torch.cuda.synchronize()
+    dx_expert = h32(plan.dx)
+    plan.route_backward(x, wr, renorm=w.renorm, want_dbias=True)
+    torch.cuda.synchronize()
+    rl, rw, rb, rx = om.route_bwd(hint(plan.dgate).astype(np.float64), hint(plan.topk_idx),
+                                  hint(plan.topk_gate).astype(np.float64), c["x"], c["w_router"],
+                                  renorm=True, dtype="bf16", dx_in=dx_expert)
+    assert rownorm_err(hint(plan.dw_router), rw) <= TOL_F32
+    assert rownorm_err(hint(plan.dbias), rb) <= TOL_F32
+    assert rownorm_err(h32(plan.dx), rx) <= TOL_BF16

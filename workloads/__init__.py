@@ -76,6 +76,10 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("shard_bwd", 1005, T=32768, d_model=4096, E=16, k=1,
                  d_ff=2048, dtype="bf16", renorm=False, routed=False,
                  zipf_s=1.1, backward=True),
+        # routed pre-training step: balanced forward, then backward through the
+        # combine, the expert FFN, the dispatch and the router
+        Workload("balanced_bwd", 1006, T=8192, d_model=2048, E=64, k=8, d_ff=1024,
+                 dtype="bf16", renorm=True, backward=True),
     ]
 }
 
