@@ -169,7 +169,7 @@ int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha,
  *   expert's routed rows in that order); logits and alive may be NULL.
  *   renorm = 0 needs logits [T, E] (moe_route's float32 logits output) and
  *   the alive mask moe_route used (NULL = all alive).
- *   Workspace: moe_workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, 0, 0).
+ *   Workspace: moe_workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d_model, 0).
  */
 int moe_route_bwd(const float* dgate, const int32_t* topk_idx,
                   const float* topk_gate, const float* logits,

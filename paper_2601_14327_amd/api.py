@@ -95,7 +95,7 @@ def moe_route_bwd(dgate: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.
         dlogits = torch.empty((T, E), dtype=torch.float32, device=dev)
     if want_dbias and dbias is None:
         dbias = torch.empty(E, dtype=torch.float32, device=dev)
-    ws = _workspace(ws, workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E), dev)
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d), dev)
     check(lib().moe_route_bwd(_ptr(dgate), _ptr(topk_idx), _ptr(topk_gate), _ptr(logits),
                               _ptr(alive), _ptr(x), _ptr(w_router), _ptr(offsets), _ptr(row_src),
                               _dtype_code(x), T, d, E, k, int(renorm), _ptr(dlogits),

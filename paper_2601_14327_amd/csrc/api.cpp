@@ -104,7 +104,7 @@ size_t moe_workspace_bytes(int which_call, int T, int k, int E, int d_model, int
     case LAEP_CALL_FFN_BWD:
       return laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, laep::kDtypeBf16);
     case LAEP_CALL_ROUTE_BWD:
-      return laep::route_bwd_ws_bytes(T, k, E);
+      return laep::route_bwd_ws_bytes(T, k, E, d_model < 0 ? 0 : d_model);
     default:
       return 0;
   }
@@ -192,7 +192,7 @@ int moe_route_bwd(const float* dgate, const int32_t* topk_idx, const float* topk
               "moe_route_bwd: renorm = 1 needs offsets and row_src from moe_expert_counts");
     else
       REQUIRE(logits, LAEP_ERR_INVALID_ARG, "moe_route_bwd: renorm = 0 needs the logits");
-    const size_t need = laep::route_bwd_ws_bytes(T, k, E);
+    const size_t need = laep::route_bwd_ws_bytes(T, k, E, d_model);
     REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_route_bwd: workspace %zu < %zu bytes",
             ws_bytes, need);
   }

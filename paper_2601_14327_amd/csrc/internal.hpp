@@ -55,7 +55,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                                void* ws, hipStream_t s);
 
 // Router backward.
-size_t route_bwd_ws_bytes(int T, int k, int E);
+size_t route_bwd_ws_bytes(int T, int k, int E, int d_model);
 hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float* gate,
                             const float* logits, const uint8_t* alive, const void* x,
                             const void* w_router, const int32_t* offsets, const int32_t* row_src,

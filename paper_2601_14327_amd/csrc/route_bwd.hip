@@ -11,6 +11,7 @@
 // Every sum runs in a fixed order: results are deterministic.
 #include "common.hpp"
 #include "internal.hpp"
+#include "tiles.hpp"
 
 namespace laep {
 namespace {
@@ -64,40 +65,66 @@ __global__ __launch_bounds__(kDlThreads) void route_bwd_dl_kernel(
 
 // dx[t] (+)= sum over slots of w * W_r[row]: `slots` per token, row ids from
 // `ids` ([T, slots], -1 = none) or the slot number itself when ids == NULL,
-// weights dl [T, slots].  Each thread owns one 8-column vector of one token.
+// weights dl [T, slots].  One wave per token (its ids and weights are
+// wave-uniform loads); each lane owns the 8-column vectors lane, lane + 64, ...
 template <typename T>
 __global__ __launch_bounds__(256) void route_bwd_dx_kernel(
     const T* __restrict__ w_router, const int32_t* __restrict__ ids,
     const float* __restrict__ dl, int n_tok, int slots, int d, int accumulate,
     T* __restrict__ dx) {
+  const int t = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (int)(threadIdx.x >> 6));
+  if (t >= n_tok) return;
+  const int lane = threadIdx.x & 63;
   const int vec_per_row = d / 8;
-  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (long long)n_tok * vec_per_row) return;
-  const int t = (int)(i / vec_per_row), v = (int)(i % vec_per_row);
-  float acc[8];
-  if (accumulate) {
-    Elem<T>::load8(dx + (size_t)t * d + (size_t)v * 8, acc);
-  } else {
+  const size_t o = (size_t)t * slots;
+  for (int v = lane; v < vec_per_row; v += 64) {
+    float acc[8];
+    if (accumulate) {
+      Elem<T>::load8(dx + (size_t)t * d + (size_t)v * 8, acc);
+    } else {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
+      for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
+    }
+    // slot order, in groups of 8 whose row loads are all issued before the
+    // sums; for full-softmax gates (ids == NULL) every expert is a slot
+    float sum[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) sum[q] = 0.0f;
+    for (int s0 = 0; s0 < slots; s0 += 8) {
+      int r[8];
+      float w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int s = s0 + u;
+        r[u] = -1;
+        w[u] = 0.0f;
+        if (s < slots) {
+          r[u] = ids ? ids[o + s] : s;
+          w[u] = dl[o + s];
+        }
+        if (w[u] == 0.0f) r[u] = -1;
+      }
+      float val[8][8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (r[u] >= 0) {
+          Elem<T>::load8(w_router + (size_t)r[u] * d + (size_t)v * 8, val[u]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) val[u][q] = 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (r[u] >= 0) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) sum[q] += w[u] * val[u][q];
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] += sum[q];
+    Elem<T>::store8(dx + (size_t)t * d + (size_t)v * 8, acc);
   }
-  // slot order; for full-softmax gates (ids == NULL) every expert is a slot
-  float sum[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) sum[q] = 0.0f;
-  for (int s = 0; s < slots; ++s) {
-    const size_t o = (size_t)t * slots + s;
-    const int r = ids ? ids[o] : s;
-    const float w = dl[o];
-    if (r < 0 || w == 0.0f) continue;
-    float val[8];
-    Elem<T>::load8(w_router + (size_t)r * d + (size_t)v * 8, val);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) sum[q] += w * val[q];
-  }
-#pragma unroll
-  for (int q = 0; q < 8; ++q) acc[q] += sum[q];
-  Elem<T>::store8(dx + (size_t)t * d + (size_t)v * 8, acc);
 }
 
 // dW_r[e, c0 + 0..255] and db[e]: workgroup (e, column chunk); 8 row lanes x
@@ -129,13 +156,13 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
   float acc[8], bsum = 0.0f;
 #pragma unroll
   for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
-  // four rows in flight per thread
-  for (int r = r0 + rl; r < r1; r += 32) {
-    int tok[4];
-    float w[4];
-    float val[4][8];
+  // eight rows in flight per thread
+  for (int r = r0 + rl; r < r1; r += 64) {
+    int tok[8];
+    float w[8];
+    float val[8][8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       const int rr = r + 8 * u;
       tok[u] = -1;
       w[u] = 0.0f;
@@ -151,7 +178,7 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       if (tok[u] >= 0 && col_ok) {
         Elem<T>::load8(x + (size_t)tok[u] * d + (size_t)v * 8, val[u]);
       } else {
@@ -160,7 +187,7 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       bsum += w[u];
 #pragma unroll
       for (int q = 0; q < 8; ++q) acc[q] += w[u] * val[u][q];
@@ -187,6 +214,109 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
   }
 }
 
+// Renormalised gates, weight gradient in two deterministic passes.
+// Pass 1: one workgroup per 128-row segment of an expert's routed rows (the
+// row-tile table); the segment's (token, weight) pairs go to LDS first, then
+// every x row is read whole (each thread one 8-column vector, eight rows in
+// flight) and the segment's partial dW_r row and bias sum are written.
+constexpr int kSegRows = 128;
+template <typename T, int VPT>
+__global__ __launch_bounds__(256) void route_bwd_dw_seg_kernel(
+    const T* __restrict__ x, const float* __restrict__ dl, const int32_t* __restrict__ row_src,
+    const TileEntry* __restrict__ table, const int* __restrict__ n_entries, int k, int d,
+    float* __restrict__ part, float* __restrict__ part_b) {
+  __shared__ int s_tok[kSegRows];
+  __shared__ float s_w[kSegRows];
+  __shared__ float s_red[4];
+  const int entry = blockIdx.x;
+  if (entry >= *n_entries) return;
+  const TileEntry te = table[entry];
+  const int tid = threadIdx.x;
+  if (tid < te.rows) {
+    const int sl = row_src[te.row0 + tid];
+    s_tok[tid] = sl / k;
+    s_w[tid] = dl[sl];
+  }
+  __syncthreads();
+  const int nvec = d / 8;
+  float* out = part + (size_t)entry * d;
+  for (int v0 = 0; v0 < nvec; v0 += 256 * VPT) {
+    float acc[VPT][8];
+#pragma unroll
+    for (int u = 0; u < VPT; ++u)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[u][q] = 0.0f;
+    for (int r0 = 0; r0 < te.rows; r0 += 8) {
+      float val[8][VPT][8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int u = 0; u < VPT; ++u) {
+          const int v = v0 + u * 256 + tid;
+          if (r0 + i < te.rows && v < nvec) {
+            Elem<T>::load8(x + (size_t)s_tok[r0 + i] * d + (size_t)v * 8, val[i][u]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) val[i][u][q] = 0.0f;
+          }
+        }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float w = r0 + i < te.rows ? s_w[r0 + i] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < VPT; ++u)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[u][q] += w * val[i][u][q];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int v = v0 + u * 256 + tid;
+      if (v < nvec) Elem<float>::store8(out + (size_t)v * 8, acc[u]);
+    }
+  }
+  // the segment's bias sum, in row order
+  float b = 0.0f;
+  if (tid < 64) {
+    for (int r = tid; r < te.rows; r += 64) b += s_w[r];
+    b = wave_sum(b);
+  }
+  if (tid == 0) part_b[entry] = b;
+}
+
+// Pass 2: dW_r[e] = sum of the expert's segment partials in table order.
+__global__ __launch_bounds__(256) void route_bwd_dw_reduce_kernel(
+    const float* __restrict__ part, const float* __restrict__ part_b,
+    const TileEntry* __restrict__ table, const int* __restrict__ n_entries, int E, int d,
+    float* __restrict__ dw, float* __restrict__ db) {
+  // the expert's segments are consecutive in the table; find them in parallel
+  __shared__ int s_first, s_count;
+  const int e = blockIdx.x;
+  if (threadIdx.x == 0) {
+    s_first = INT_MAX;
+    s_count = 0;
+  }
+  __syncthreads();
+  const int n = *n_entries;
+  for (int i = threadIdx.x; i < n; i += 256)
+    if (table[i].expert == e) {
+      atomicMin(&s_first, i);
+      atomicAdd(&s_count, 1);
+    }
+  __syncthreads();
+  const int first = s_first, count = s_count;
+  for (int c = blockIdx.y * 256 + threadIdx.x; c < d; c += gridDim.y * 256) {
+    float acc = 0.0f;
+    for (int i = 0; i < count; ++i) acc += part[(size_t)(first + i) * d + c];
+    dw[(size_t)e * d + c] = acc;
+  }
+  if (db != nullptr && blockIdx.y == 0 && threadIdx.x == 0) {
+    float acc = 0.0f;
+    for (int i = 0; i < count; ++i) acc += part_b[first + i];
+    db[e] = acc;
+  }
+}
+
 __global__ void fill_zero_kernel(float* __restrict__ p, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)
@@ -195,8 +325,16 @@ __global__ void fill_zero_kernel(float* __restrict__ p, size_t n) {
 
 }  // namespace
 
-size_t route_bwd_ws_bytes(int T, int k, int E) {
-  return align_up((size_t)T * (k > E ? k : E) * sizeof(float), 256);
+// ws: dl, then (renormalised gates) the segment table, partial rows and sums.
+// The segment partials need d; the workspace query has none, so the partial
+// area is sized for the largest d_model the caller passes (d_model is an
+// argument of moe_workspace_bytes for the backward calls).
+inline int seg_max(int T, int k, int E) { return (int)(((int64_t)T * k + kSegRows - 1) / kSegRows) + E; }
+
+size_t route_bwd_ws_bytes(int T, int k, int E, int d) {
+  const int m = seg_max(T, k, E);
+  return align_up((size_t)T * (k > E ? k : E) * sizeof(float), 256) + table_bytes(m) +
+         align_up((size_t)m * d * sizeof(float), 256) + align_up((size_t)m * sizeof(float), 256);
 }
 
 hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float* gate,
@@ -217,23 +355,47 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
                      dl, dlogits);
   const int slots = renorm ? k : E;
   const int32_t* ids = renorm ? idx : nullptr;
-  const long long n_vec = (long long)T_ * (d / 8);
-  const dim3 gdx((unsigned)((n_vec + 255) / 256)), gdw(E, (d / 8 + 31) / 32);
-  const int32_t* rs = renorm ? row_src : nullptr;
+  const dim3 gdx((unsigned)((T_ + 3) / 4)), gdw(E, (d / 8 + 31) / 32);
+  // renormalised gates: segment table of the routed rows (pass 1 + 2)
+  const int m = seg_max(T_, k, E);
+  char* base = static_cast<char*>(ws) + align_up((size_t)T_ * (k > E ? k : E) * sizeof(float), 256);
+  TableWs tw = carve_table(base, m);
+  float* part = reinterpret_cast<float*>(base + table_bytes(m));
+  float* part_b = reinterpret_cast<float*>(base + table_bytes(m) + align_up((size_t)m * d * 4, 256));
+  if (renorm)
+    hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, nullptr, E,
+                       kSegRows, 0, m, tw.n_entries, tw.table);
+  const dim3 gred(E, (d + 255) / 256 < 8 ? (d + 255) / 256 : 8);
   if (dtype == kDtypeBf16) {
     hipLaunchKernelGGL(route_bwd_dx_kernel<bf16_t>, gdx, dim3(256), 0, s,
                        static_cast<const bf16_t*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
                        static_cast<bf16_t*>(dx));
-    hipLaunchKernelGGL(route_bwd_dw_kernel<bf16_t>, gdw, dim3(256), 0, s,
-                       static_cast<const bf16_t*>(x), dl, offsets, rs, T_, k, E, d, dw_router,
-                       dbias);
+    if (renorm) {
+      hipLaunchKernelGGL((route_bwd_dw_seg_kernel<bf16_t, 1>), dim3(m), dim3(256), 0, s,
+                         static_cast<const bf16_t*>(x), dl, row_src, tw.table, tw.n_entries, k, d,
+                         part, part_b);
+      hipLaunchKernelGGL(route_bwd_dw_reduce_kernel, gred, dim3(256), 0, s, part, part_b,
+                         tw.table, tw.n_entries, E, d, dw_router, dbias);
+    } else {
+      hipLaunchKernelGGL(route_bwd_dw_kernel<bf16_t>, gdw, dim3(256), 0, s,
+                         static_cast<const bf16_t*>(x), dl, offsets, nullptr, T_, k, E, d,
+                         dw_router, dbias);
+    }
   } else {
     hipLaunchKernelGGL(route_bwd_dx_kernel<float>, gdx, dim3(256), 0, s,
                        static_cast<const float*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
                        static_cast<float*>(dx));
-    hipLaunchKernelGGL(route_bwd_dw_kernel<float>, gdw, dim3(256), 0, s,
-                       static_cast<const float*>(x), dl, offsets, rs, T_, k, E, d, dw_router,
-                       dbias);
+    if (renorm) {
+      hipLaunchKernelGGL((route_bwd_dw_seg_kernel<float, 1>), dim3(m), dim3(256), 0, s,
+                         static_cast<const float*>(x), dl, row_src, tw.table, tw.n_entries, k, d,
+                         part, part_b);
+      hipLaunchKernelGGL(route_bwd_dw_reduce_kernel, gred, dim3(256), 0, s, part, part_b,
+                         tw.table, tw.n_entries, E, d, dw_router, dbias);
+    } else {
+      hipLaunchKernelGGL(route_bwd_dw_kernel<float>, gdw, dim3(256), 0, s,
+                         static_cast<const float*>(x), dl, offsets, nullptr, T_, k, E, d,
+                         dw_router, dbias);
+    }
   }
   return hipGetLastError();
 }

@@ -80,7 +80,7 @@ class MoELayerPlan:
             self.dw_router = None
             self.dbias = None
             self.ws_route_bwd = torch.empty(
-                max(1, api.workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E)), dtype=torch.uint8,
+                max(1, api.workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d_model)), dtype=torch.uint8,
                 device=dev)
 
     # -- pieces --------------------------------------------------------------

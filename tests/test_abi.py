@@ -136,6 +136,8 @@ def test_route_bwd_validation(L):
     assert call(args(wsb=16)) == 3
     need = L.moe_workspace_bytes(4, 16, 2, 8, 0, 0)
     assert need >= 16 * 8 * 4
+    # the segment partials of the weight gradient grow with d_model
+    assert L.moe_workspace_bytes(4, 16, 2, 8, 64, 0) >= need + 64 * 4
 
 
 def test_calib_validation(L):
