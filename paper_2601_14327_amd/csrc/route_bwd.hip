@@ -7,7 +7,7 @@
 // k-term weighted sum of W_r rows (like the combine) and dW_r[e] a weighted
 // sum over the expert's routed rows, which moe_expert_counts already lists
 // in expert order (row_src).  Full-softmax gates make dl dense over the alive
-// experts; the same kernels then run over all E experts and all T tokens.
+// experts; dx then sums over all E experts and dW_r over all T tokens.
 // Every sum runs in a fixed order: results are deterministic.
 #include "common.hpp"
 #include "internal.hpp"
@@ -127,16 +127,13 @@ __global__ __launch_bounds__(256) void route_bwd_dx_kernel(
   }
 }
 
-// dW_r[e, c0 + 0..255] and db[e]: workgroup (e, column chunk); 8 row lanes x
-// 32 vector lanes.  Row lane rl takes rows rl, rl + 8, ... of the expert; the
-// 8 partial sums are then added in lane order through LDS.
-//   renorm (row_src != NULL): rows = the expert's routed rows
-//     [offsets[e], offsets[e+1]); slot s = row_src[r], token s / k, weight dl[s]
-//   full softmax: rows = every token t, weight dl[t * E + e]
+// Full-softmax gates: dW_r[e, c0 + 0..255] and db[e] over every token t with
+// weight dl[t * E + e].  Workgroup (e, column chunk); 8 row lanes x 32 vector
+// lanes.  Row lane rl takes tokens rl, rl + 8, ...; the 8 partial sums are
+// then added in lane order through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
-    const T* __restrict__ x, const float* __restrict__ dl, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ row_src, int n_tok, int k, int E, int d,
+    const T* __restrict__ x, const float* __restrict__ dl, int n_tok, int E, int d,
     float* __restrict__ dw, float* __restrict__ db) {
   __shared__ float s_part[8][32 * 8 + 4];
   __shared__ float s_bias[8];
@@ -145,14 +142,7 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
   const int rl = threadIdx.x >> 5, vl = threadIdx.x & 31;
   const int v = chunk * 32 + vl;              // 8-column vector index
   const bool col_ok = v * 8 < d;
-  int r0, r1;
-  if (row_src) {
-    r0 = offsets[e];
-    r1 = offsets[e + 1];
-  } else {
-    r0 = 0;
-    r1 = n_tok;
-  }
+  const int r0 = 0, r1 = n_tok;
   float acc[8], bsum = 0.0f;
 #pragma unroll
   for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
@@ -167,14 +157,8 @@ __global__ __launch_bounds__(256) void route_bwd_dw_kernel(
       tok[u] = -1;
       w[u] = 0.0f;
       if (rr < r1) {
-        if (row_src) {
-          const int s = row_src[rr];
-          tok[u] = s / k;
-          w[u] = dl[s];
-        } else {
-          tok[u] = rr;
-          w[u] = dl[(size_t)rr * E + e];
-        }
+        tok[u] = rr;
+        w[u] = dl[(size_t)rr * E + e];
       }
     }
 #pragma unroll
@@ -378,7 +362,7 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
                          tw.table, tw.n_entries, E, d, dw_router, dbias);
     } else {
       hipLaunchKernelGGL(route_bwd_dw_kernel<bf16_t>, gdw, dim3(256), 0, s,
-                         static_cast<const bf16_t*>(x), dl, offsets, nullptr, T_, k, E, d,
+                         static_cast<const bf16_t*>(x), dl, T_, E, d,
                          dw_router, dbias);
     }
   } else {
@@ -393,7 +377,7 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
                          tw.table, tw.n_entries, E, d, dw_router, dbias);
     } else {
       hipLaunchKernelGGL(route_bwd_dw_kernel<float>, gdw, dim3(256), 0, s,
-                         static_cast<const float*>(x), dl, offsets, nullptr, T_, k, E, d,
+                         static_cast<const float*>(x), dl, T_, E, d,
                          dw_router, dbias);
     }
   }
