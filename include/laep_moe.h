@@ -69,6 +69,7 @@ extern "C" {
 
 /* Limits of this build. */
 #define LAEP_MAX_EXPERTS 256
+#define LAEP_MAX_LAYERS 256
 
 /*
  * moe_route -- router scoring and top-k gating (produces E[i, j, l] of
@@ -141,6 +142,70 @@ int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E,
 int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha,
                     double beta, uint8_t* alive, int32_t* n_pruned,
                     void* stream);
+
+/*
+ * laep_expert_pruning -- Algorithm 1 (Appendix) over a recorded window of
+ * ITER training iterations and L layers: which experts each layer prunes.
+ *
+ *   Step 1 (recording) is the caller's: etn[it, l, :] holds the tokens each
+ *   expert of layer l received in iteration it (moe_expert_counts adds them
+ *   into an int64 row through etn_accum).
+ *   Step 2: for every (it, l), the rule of laep_prune_mask on etn[it, l, :]
+ *   with total and the layer's alpha[l] marks experts; Marker[l, e] counts
+ *   the iterations that marked e, Exp_dis[l] all marks of the layer.
+ *   Step 3: layer l prunes N_l = floor(Exp_dis[l] / ITER + 0.5) experts, the
+ *   most marked, ties to the lower window load sum (equivalently the lower
+ *   mean load), then to the lower index.
+ *
+ *   etn device [ITER, L, E] int64 (>= 0); total = S * topK per iteration;
+ *   alpha host [L] double (>= 0, INFINITY disables Eq. (1)); a per-layer
+ *   schedule such as 0.2 on the first and last sixth of the layers and 0.4
+ *   in between (the ablation of Section 3.4, and the setting of the
+ *   Section 4 pre-training run) is passed here;
+ *   alive device [L, E] uint8 (out: 1 = kept); n_pruned device [L] int32
+ *   (out: N_l); marker device [L, E] int32 (out, optional: Marker).
+ *   1 <= L <= LAEP_MAX_LAYERS, 1 <= ITER.
+ */
+int laep_expert_pruning(const int64_t* etn, int ITER, int L, int E,
+                        int64_t total, const double* alpha, double beta,
+                        uint8_t* alive, int32_t* n_pruned, int32_t* marker,
+                        void* stream);
+
+/*
+ * laep_compact_experts -- slot assignment for physical expert compaction
+ * (Section 3.2: pruned experts leave the model).  Per layer, the surviving
+ * experts keep their order and take consecutive slots:
+ *   expert_map[l, e] = #{j < e : alive[l, j]} if alive[l, e], else -1
+ *   n_alive[l]       = #{e : alive[l, e]}
+ *
+ *   alive device [L, E] uint8; expert_map device [L, E] int32 (out);
+ *   n_alive device [L] int32 (out).  The map is also the expert_map of
+ *   moe_grouped_ffn_fwd/bwd over the repacked weights.
+ */
+int laep_compact_experts(const uint8_t* alive, int L, int E, int32_t* expert_map,
+                         int32_t* n_alive, void* stream);
+
+/*
+ * laep_repack_experts -- copy the surviving experts' parameters of one layer
+ * into compact buffers of n_out slots.  For every e with
+ * 0 <= p = expert_map[e] < n_out:
+ *   w_router_out[p]  = w_router[e]       ([d_model] row)
+ *   bias_out[p]      = bias[e]           (float32)
+ *   w_gate_up_out[p] = w_gate_up[e]      ([2*d_ff, d_model])
+ *   w_down_out[p]    = w_down[e]         ([d_model, d_ff])
+ * Each (source, destination) pair may be NULL together to skip that tensor;
+ * optimizer states of the same shapes are repacked by further calls with
+ * dtype LAEP_F32.  Slots an expert map does not reach are left untouched.
+ *
+ *   expert_map device [E] int32 (from laep_compact_experts); the sources are
+ *   device [E, ...] dtype, the destinations device [n_out, ...] dtype.
+ *   d_model % 8 == 0.  Sources and destinations must not overlap.
+ */
+int laep_repack_experts(const int32_t* expert_map, int E, int n_out, int dtype,
+                        int d_model, int d_ff, const void* w_router,
+                        const float* bias, const void* w_gate_up,
+                        const void* w_down, void* w_router_out, float* bias_out,
+                        void* w_gate_up_out, void* w_down_out, void* stream);
 
 /*
  * moe_route_bwd -- backward of moe_route's scoring and gating, with the

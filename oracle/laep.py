@@ -64,7 +64,7 @@ def prune_mask(counts, total: int, alpha: float = math.inf, beta: float = 0.0):
     return alive, n_pruned, order
 
 
-def expert_pruning(etn, S: int, topK: int, alpha, beta: float):
+def expert_pruning(etn, S: int, topK: int, alpha, beta: float, return_marker: bool = False):
     """Algorithm 1 over a window of ITER iterations and L layers.
 
     etn: [ITER, L, E] token counts (Step 1).  alpha: scalar or per-layer
@@ -79,7 +79,8 @@ def expert_pruning(etn, S: int, topK: int, alpha, beta: float):
       (Exp_dis accumulates over ITER but is used as a per-layer count);
     * Marker ties go to the lower mean load, then to the lower index;
     * the running sum restarts at 0 for every (iteration, layer).
-    Returns a list of L int arrays, the pruned expert ids per layer.
+    Returns a list of L int arrays, the pruned expert ids per layer (and the
+    Marker array [L, E] when return_marker).
     """
     etn = np.asarray(etn, dtype=np.int64)
     ITER, L, E = etn.shape
@@ -99,7 +100,35 @@ def expert_pruning(etn, S: int, topK: int, alpha, beta: float):
         # most-marked first; ties: lower mean load, then lower index
         order = np.lexsort((np.arange(E), mean_load[layer], -marker[layer]))
         pruned.append(np.sort(order[:n_dis]).astype(np.int64))
-    return pruned
+    return (pruned, marker) if return_marker else pruned
+
+
+# --------------------------------------------------------------------------
+# Layer-adaptive alpha and the removal of pruned experts
+# --------------------------------------------------------------------------
+def hybrid_alpha(n_layers: int, edge: float = 0.2, middle: float = 0.4):
+    """The per-layer alpha of the Section 3.4 ablation and the Section 4
+    run: ``edge`` for the first and the last sixth of the layers, ``middle``
+    for the two thirds between.  Reading: a sixth of L layers is L / 6
+    rounded to the nearest integer, halves up (the paper's models have L a
+    multiple of 6 or say nothing)."""
+    n_edge = int(math.floor(n_layers / 6 + 0.5))
+    return [edge if (l < n_edge or l >= n_layers - n_edge) else middle
+            for l in range(n_layers)]
+
+
+def compact(alive):
+    """Slots of the surviving experts (Section 3.2: pruned experts leave the
+    model).  Survivors keep their order: slot = number of alive experts with
+    a lower index; pruned experts map to -1.  Returns (expert_map, n_alive)."""
+    alive = np.asarray(alive).astype(bool)
+    expert_map = np.full(alive.shape[0], -1, dtype=np.int64)
+    slot = 0
+    for e in range(alive.shape[0]):
+        if alive[e]:
+            expert_map[e] = slot
+            slot += 1
+    return expert_map, slot
 
 
 # --------------------------------------------------------------------------

@@ -6,6 +6,8 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     moe_route            router scoring + top-k gating
     moe_expert_counts    per-expert token loads (ETN), offsets, dispatch rows
     laep_prune_mask      LAEP prune decision (alpha / beta thresholds)
+    laep_expert_pruning  Algorithm 1 over a recorded ETN window (per-layer alpha)
+    laep_compact_experts, laep_repack_experts   physical removal of pruned experts
     moe_permute          dispatch of token rows to expert order
     moe_grouped_ffn_fwd  grouped SwiGLU expert FFN (bf16 MFMA)
     moe_grouped_ffn_fwd_gather   the same with the dispatch folded into the operand loads
@@ -20,8 +22,11 @@ from .api import (  # noqa: F401
     ffn_bwd_ws_views,
     laep_calib_copy,
     laep_calib_mfma,
+    laep_compact_experts,
+    laep_expert_pruning,
     laep_prune_mask,
     laep_rearrange,
+    laep_repack_experts,
     moe_combine,
     moe_combine_bwd,
     moe_expert_counts,
@@ -35,3 +40,4 @@ from .api import (  # noqa: F401
     workspace_bytes,
 )
 from .layer import MoELayerPlan, layer_forward  # noqa: F401
+from .pruning import ExpertPruner, compact_layer, hybrid_alpha  # noqa: F401

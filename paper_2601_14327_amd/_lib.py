@@ -52,6 +52,9 @@ SIGNATURES = {
                            _p, _p, _i, _p, _sz, _p]),
     "moe_expert_counts": (_i, [_p, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "laep_prune_mask": (_i, [_p, _i, _i64, _d, _d, _p, _p, _p]),
+    "laep_expert_pruning": (_i, [_p, _i, _i, _i, _i64, _p, _d, _p, _p, _p, _p]),
+    "laep_compact_experts": (_i, [_p, _i, _i, _p, _p, _p]),
+    "laep_repack_experts": (_i, [_p, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p, _p]),
     "moe_permute": (_i, [_p, _i, _p, _i, _i, _i, _p, _p]),
     "moe_grouped_ffn_fwd": (_i, [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_fwd_gather": (_i, [_p, _p, _i, _i, _p, _p, _p, _p, _i, _i, _i, _i, _i64,

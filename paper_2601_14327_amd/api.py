@@ -7,6 +7,7 @@ Every step of the layer runs in the library's HIP kernels.
 """
 from __future__ import annotations
 
+import ctypes
 import math
 from typing import Optional, Tuple
 
@@ -137,6 +138,77 @@ def laep_prune_mask(counts: torch.Tensor, total: int, alpha: float = math.inf,
     check(lib().laep_prune_mask(_ptr(counts), E, int(total), float(alpha), float(beta),
                                 _ptr(alive), _ptr(n_pruned), _stream(dev)))
     return alive, n_pruned
+
+
+def laep_expert_pruning(etn: torch.Tensor, total: int, alpha, beta: float, *,
+                        alive=None, n_pruned=None, want_marker: bool = False):
+    """Algorithm 1 over a recorded window etn [ITER, L, E] int64.  ``alpha`` is a
+    float or a per-layer sequence.  Returns (alive [L, E] uint8, n_pruned [L]
+    int32, marker [L, E] int32 or None)."""
+    _dev(etn, "etn")
+    if etn.dtype != torch.int64 or etn.dim() != 3:
+        raise ValueError("etn must be an int64 tensor [ITER, L, E]")
+    iters, L, E = etn.shape
+    alphas = [float(alpha)] * L if isinstance(alpha, (int, float)) else [float(a) for a in alpha]
+    if len(alphas) != L:
+        raise ValueError(f"alpha has {len(alphas)} entries for {L} layers")
+    dev = etn.device
+    alive = torch.empty((L, E), dtype=torch.uint8, device=dev) if alive is None else alive
+    n_pruned = torch.empty(L, dtype=torch.int32, device=dev) if n_pruned is None else n_pruned
+    marker = torch.empty((L, E), dtype=torch.int32, device=dev) if want_marker else None
+    a_host = (ctypes.c_double * L)(*alphas)
+    check(lib().laep_expert_pruning(_ptr(etn), iters, L, E, int(total), a_host, float(beta),
+                                    _ptr(alive), _ptr(n_pruned), _ptr(marker), _stream(dev)))
+    return alive, n_pruned, marker
+
+
+def laep_compact_experts(alive: torch.Tensor, *, expert_map=None, n_alive=None):
+    """Slots of the surviving experts.  alive [E] or [L, E] uint8.
+    Returns (expert_map of alive's shape int32, n_alive [L] int32)."""
+    _dev(alive, "alive")
+    a2 = alive.reshape(-1, alive.shape[-1])
+    L, E = a2.shape
+    dev = alive.device
+    expert_map = (torch.empty(alive.shape, dtype=torch.int32, device=dev) if expert_map is None
+                  else expert_map)
+    n_alive = torch.empty(L, dtype=torch.int32, device=dev) if n_alive is None else n_alive
+    check(lib().laep_compact_experts(_ptr(alive), L, E, _ptr(expert_map), _ptr(n_alive),
+                                     _stream(dev)))
+    return expert_map, n_alive
+
+
+def laep_repack_experts(expert_map: torch.Tensor, n_out: int, *, w_router=None, bias=None,
+                        w_gate_up=None, w_down=None, out=None):
+    """Copy the surviving experts' parameters (one layer) into n_out slots.
+    Returns a dict with the repacked tensors that were given."""
+    _dev(expert_map, "expert_map")
+    E = expert_map.shape[0]
+    given = {n: t for n, t in (("w_router", w_router), ("bias", bias), ("w_gate_up", w_gate_up),
+                               ("w_down", w_down)) if t is not None}
+    mats = [t for n, t in given.items() if n != "bias"]
+    dtype = mats[0].dtype if mats else torch.float32
+    if any(t.dtype != dtype for t in mats):
+        raise ValueError("the repacked matrices must share one dtype")
+    d_model = (w_router.shape[1] if w_router is not None else
+               w_gate_up.shape[2] if w_gate_up is not None else
+               w_down.shape[1] if w_down is not None else 8)
+    d_ff = (w_gate_up.shape[1] // 2 if w_gate_up is not None else
+            w_down.shape[2] if w_down is not None else 0)
+    for n, t in given.items():
+        _dev(t, n)
+        if t.shape[0] != E:
+            raise ValueError(f"{n} has {t.shape[0]} experts, expert_map {E}")
+    out = {} if out is None else dict(out)
+    for n, t in given.items():
+        if n not in out:
+            out[n] = torch.empty((n_out, *t.shape[1:]), dtype=t.dtype, device=t.device)
+    code = _dtype_code(mats[0]) if mats else LAEP_F32
+    check(lib().laep_repack_experts(_ptr(expert_map), E, int(n_out), code, d_model, d_ff,
+                                    _ptr(w_router), _ptr(bias), _ptr(w_gate_up), _ptr(w_down),
+                                    _ptr(out.get("w_router")), _ptr(out.get("bias")),
+                                    _ptr(out.get("w_gate_up")), _ptr(out.get("w_down")),
+                                    _stream(expert_map.device)))
+    return out
 
 
 def moe_permute(x: torch.Tensor, dest_row: torch.Tensor, k: int, rows: Optional[int] = None,

@@ -169,6 +169,78 @@ int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha, d
       "laep_prune_mask");
 }
 
+int laep_expert_pruning(const int64_t* etn, int ITER, int L, int E, int64_t total,
+                        const double* alpha, double beta, uint8_t* alive, int32_t* n_pruned,
+                        int32_t* marker, void* stream) {
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(L >= 1 && L <= LAEP_MAX_LAYERS, LAEP_ERR_INVALID_ARG, "L=%d outside [1, %d]", L,
+          LAEP_MAX_LAYERS);
+  REQUIRE(ITER >= 1, LAEP_ERR_INVALID_ARG, "laep_expert_pruning: ITER=%d < 1", ITER);
+  REQUIRE(etn && alpha && alive && n_pruned, LAEP_ERR_INVALID_ARG,
+          "laep_expert_pruning: etn, alpha, alive and n_pruned must be non-null");
+  REQUIRE(total >= 0, LAEP_ERR_INVALID_ARG, "laep_expert_pruning: total=%lld < 0",
+          (long long)total);
+  REQUIRE(!std::isnan(beta) && beta >= 0, LAEP_ERR_INVALID_ARG,
+          "laep_expert_pruning: beta must be >= 0 (got %g)", beta);
+  for (int l = 0; l < L; ++l)
+    REQUIRE(!std::isnan(alpha[l]) && alpha[l] >= 0, LAEP_ERR_INVALID_ARG,
+            "laep_expert_pruning: alpha[%d] must be >= 0 (got %g)", l, alpha[l]);
+  return hip_status(laep::launch_expert_pruning(etn, ITER, L, E, total, alpha, beta, alive,
+                                                n_pruned, marker, as_stream(stream)),
+                    "laep_expert_pruning");
+}
+
+int laep_compact_experts(const uint8_t* alive, int L, int E, int32_t* expert_map,
+                         int32_t* n_alive, void* stream) {
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(L >= 1, LAEP_ERR_INVALID_ARG, "laep_compact_experts: L=%d < 1", L);
+  REQUIRE(alive && expert_map && n_alive, LAEP_ERR_INVALID_ARG,
+          "laep_compact_experts: alive, expert_map and n_alive must be non-null");
+  return hip_status(laep::launch_expert_map(alive, L, E, expert_map, n_alive, as_stream(stream)),
+                    "laep_compact_experts");
+}
+
+int laep_repack_experts(const int32_t* expert_map, int E, int n_out, int dtype, int d_model,
+                        int d_ff, const void* w_router, const float* bias, const void* w_gate_up,
+                        const void* w_down, void* w_router_out, float* bias_out,
+                        void* w_gate_up_out, void* w_down_out, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  REQUIRE(E >= 1 && E <= LAEP_MAX_EXPERTS, LAEP_ERR_INVALID_ARG, "E=%d outside [1, %d]", E,
+          LAEP_MAX_EXPERTS);
+  REQUIRE(n_out >= 0, LAEP_ERR_INVALID_ARG, "laep_repack_experts: n_out=%d < 0", n_out);
+  REQUIRE(expert_map, LAEP_ERR_INVALID_ARG, "laep_repack_experts: expert_map must be non-null");
+  REQUIRE(d_model > 0 && d_model % 8 == 0, LAEP_ERR_INVALID_ARG,
+          "laep_repack_experts: d_model=%d must be a positive multiple of 8", d_model);
+  REQUIRE(!!w_router == !!w_router_out && !!bias == !!bias_out &&
+              !!w_gate_up == !!w_gate_up_out && !!w_down == !!w_down_out,
+          LAEP_ERR_INVALID_ARG,
+          "laep_repack_experts: each source and its destination must be both set or both NULL");
+  REQUIRE(!(w_gate_up || w_down) || d_ff > 0, LAEP_ERR_INVALID_ARG,
+          "laep_repack_experts: d_ff=%d must be positive", d_ff);
+  const void* ptrs[] = {w_router, w_router_out, w_gate_up, w_gate_up_out, w_down, w_down_out};
+  for (const void* q : ptrs)
+    REQUIRE(aligned16(q), LAEP_ERR_INVALID_ARG,
+            "laep_repack_experts: weight pointers must be 16-byte aligned");
+  if (n_out == 0) return ok();
+  const size_t es = elem_bytes(dtype);
+  const hipStream_t s = as_stream(stream);
+  hipError_t e = hipSuccess;
+  if (w_router)
+    e = laep::launch_repack(expert_map, E, n_out, w_router, w_router_out, d_model * es, s);
+  if (e == hipSuccess && bias)
+    e = laep::launch_repack_scalar(expert_map, E, n_out, bias, bias_out, s);
+  if (e == hipSuccess && w_gate_up)
+    e = laep::launch_repack(expert_map, E, n_out, w_gate_up, w_gate_up_out,
+                            (size_t)2 * d_ff * d_model * es, s);
+  if (e == hipSuccess && w_down)
+    e = laep::launch_repack(expert_map, E, n_out, w_down, w_down_out,
+                            (size_t)d_model * d_ff * es, s);
+  return hip_status(e, "laep_repack_experts");
+}
+
 int moe_route_bwd(const float* dgate, const int32_t* topk_idx, const float* topk_gate,
                   const float* logits, const uint8_t* alive, const void* x, const void* w_router,
                   const int32_t* offsets, const int32_t* row_src, int dtype, int T, int d_model,

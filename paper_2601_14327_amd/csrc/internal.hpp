@@ -25,6 +25,17 @@ hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* count
 
 hipError_t launch_prune(const int32_t* counts, int E, int64_t total, double alpha, double beta,
                         uint8_t* alive, int32_t* n_pruned, hipStream_t s);
+constexpr int kMaxLayers = 256;
+// alpha: host [L] (L <= kMaxLayers)
+hipError_t launch_expert_pruning(const int64_t* etn, int iters, int L, int E, int64_t total,
+                                 const double* alpha, double beta, uint8_t* alive,
+                                 int32_t* n_pruned, int32_t* marker, hipStream_t s);
+hipError_t launch_expert_map(const uint8_t* alive, int L, int E, int32_t* expert_map,
+                             int32_t* n_alive, hipStream_t s);
+hipError_t launch_repack(const int32_t* expert_map, int E, int n_out, const void* src, void* dst,
+                         size_t bytes_per_expert, hipStream_t s);
+hipError_t launch_repack_scalar(const int32_t* expert_map, int E, int n_out, const float* src,
+                                float* dst, hipStream_t s);
 
 hipError_t launch_permute(const void* x, int elem_bytes, const int32_t* dest_row, int T, int k,
                           int d, void* x_perm, hipStream_t s);

@@ -37,7 +37,9 @@ def test_header_declares_the_hot_path_calls():
     names = _declared_functions()
     for n in ["moe_route", "moe_expert_counts", "laep_prune_mask", "moe_permute",
               "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_combine", "moe_combine_bwd",
-              "moe_permute_bwd", "moe_workspace_bytes", "laep_rearrange", "laep_last_error"]:
+              "moe_permute_bwd", "moe_workspace_bytes", "laep_rearrange", "laep_last_error",
+              "moe_route_bwd", "laep_expert_pruning", "laep_compact_experts",
+              "laep_repack_experts"]:
         assert n in names, n
 
 
@@ -188,3 +190,46 @@ def test_rearrange_errors(L):
 
     with pytest.raises(LaepError):
         laep_rearrange([1.0, 2.0], 0)
+
+
+def test_expert_pruning_validation(L):
+    keep, p = _fake()
+    a3 = (ctypes.c_double * 3)(0.2, 0.4, 0.2)
+    ok_args = dict(etn=p, it=2, L=3, E=8, total=100, alpha=a3, beta=0.1, alive=p, n=p, mk=None)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return L.laep_expert_pruning(a["etn"], a["it"], a["L"], a["E"], a["total"], a["alpha"],
+                                     a["beta"], a["alive"], a["n"], a["mk"], None)
+
+    assert call(it=0) == 1 and "ITER" in _err(L)
+    assert call(L=0) == 1
+    assert call(L=257, alpha=(ctypes.c_double * 257)()) == 1
+    assert call(E=300) == 1
+    assert call(etn=None) == 1
+    assert call(alpha=None) == 1
+    assert call(total=-1) == 1
+    assert call(beta=-0.5) == 1
+    assert call(alpha=(ctypes.c_double * 3)(0.2, float("nan"), 0.2)) == 1
+    assert "alpha[1]" in _err(L)
+    assert call(alpha=(ctypes.c_double * 3)(0.2, -1.0, 0.2)) == 1
+
+
+def test_compact_and_repack_validation(L):
+    keep, p = _fake()
+    assert L.laep_compact_experts(p, 1, 300, p, p, None) == 1
+    assert L.laep_compact_experts(p, 0, 8, p, p, None) == 1
+    assert L.laep_compact_experts(None, 1, 8, p, p, None) == 1
+    # (expert_map, E, n_out, dtype, d, f, w_r, bias, w_gu, w_d, w_r', bias', w_gu', w_d')
+    rp = L.laep_repack_experts
+    assert rp(p, 8, 4, 5, 64, 64, p, None, p, p, p, None, p, p, None) == 2
+    assert rp(None, 8, 4, 1, 64, 64, p, None, p, p, p, None, p, p, None) == 1
+    assert rp(p, 8, -1, 1, 64, 64, p, None, p, p, p, None, p, p, None) == 1
+    assert rp(p, 8, 4, 1, 60, 64, p, None, p, p, p, None, p, p, None) == 1
+    assert rp(p, 8, 4, 1, 64, 64, p, None, p, p, None, None, p, p, None) == 1
+    assert "both" in _err(L)
+    assert rp(p, 8, 4, 1, 64, 0, p, None, p, p, p, None, p, p, None) == 1
+    assert rp(p, 8, 4, 1, 64, 64, p + 4, None, p, p, p, None, p, p, None) == 1
+    assert "aligned" in _err(L)
+    # nothing to copy: valid, and enqueues nothing
+    assert rp(p, 8, 0, 1, 64, 64, p, None, p, p, p, None, p, p, None) == 0
