@@ -23,9 +23,12 @@ Prints ONE JSON line:
   attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
   cpu_baseline the float64 CPU oracle timed on a bounded token sample
 
-Other workloads: skewed, skewed_mild (routed, pruned), shard (16 experts,
-given Zipf routing), shard_bwd (shard forward + backward), balanced_bwd
-(balanced forward + backward through the combine, FFN, dispatch and router).
+Other workloads: skewed, skewed_mild (routed, pruned every step), shard (16
+experts, given Zipf routing), shard_bwd (shard forward + backward),
+balanced_bwd (balanced forward + backward through the combine, FFN, dispatch
+and router), mild_pruned (Algorithm 1 over a window of batches before the
+timed steps, pruned experts removed; the steps run the compact layer, and
+`pruning` reports the parameter reduction and the one-time repack).
 
 Profiling helpers (used by the commands recorded under profiles/):
   --profile-target ffn|copy   run only that call a few times (for --pmc runs)
@@ -69,8 +72,9 @@ def sources_sha(names) -> str:
 # ---------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ---------------------------------------------------------------------------------------
-def _cpu_baseline(w, c, budget_s: float):
-    """Time the plain float64 oracle on a token sample of the same workload."""
+def _cpu_baseline(w, c, budget_s: float, keep=None):
+    """Time the plain float64 oracle on a token sample of the same workload
+    (``keep``: the surviving experts of a pruned layer)."""
     import oracle.moe as om
 
     try:
@@ -82,8 +86,11 @@ def _cpu_baseline(w, c, budget_s: float):
     def run(n):
         t0 = time.perf_counter()
         if w.routed:
-            om.layer_forward(c["x"][:n], c["w_router"], c["w_gate_up"], c["w_down"], w.k,
-                             bias=c.get("bias"), renorm=w.renorm, dtype="bf16")
+            sel = slice(None) if keep is None else keep
+            bias = c.get("bias")
+            om.layer_forward(c["x"][:n], c["w_router"][sel], c["w_gate_up"][sel],
+                             c["w_down"][sel], w.k, bias=None if bias is None else bias[sel],
+                             renorm=w.renorm, dtype="bf16")
         else:
             idx = c["topk_idx"][:n]
             counts, offsets, dest = om.expert_counts(idx, w.E)
@@ -136,6 +143,53 @@ class Setup:
             self.gate = to(c["topk_gate"], torch.float32)
         self.dout = to(c["dout"]) if w.backward else None
         self.laep = laep
+        self.E = w.E
+        self.keep = None
+        self.pruning = None
+        if w.prune_window:
+            self._prune_and_compact()
+
+    def _prune_and_compact(self):
+        """Algorithm 1 over a window of routed batches, then the pruned experts
+        leave the layer: router rows, bias and FFN weights are repacked and the
+        timed steps run the compact layer."""
+        import torch
+
+        w, L = self.w, self.laep
+        pruner = L.ExpertPruner(w.prune_window, 1, w.E, w.T, w.k, alpha=w.prune_alpha,
+                                beta=w.prune_beta, device=self.dev)
+        for it in range(w.prune_window):
+            idx, _ = L.moe_route(self.xs[it % self.n_sets], self.wr, w.k, bias=self.bias,
+                                 renorm=w.renorm)
+            L.moe_expert_counts(idx, w.E, etn_accum=pruner.slot(it, 0))
+        alive, n_pruned, _ = pruner.decide()
+        alive = alive[0].contiguous()
+        big = sum(t.numel() * t.element_size() for t in (self.wr, self.wgu, self.wd))
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        small = L.compact_layer(alive, w_router=self.wr, w_gate_up=self.wgu, w_down=self.wd,
+                                bias=self.bias)
+        # time the repack alone (the slot map is already known)
+        s.record()
+        L.laep_repack_experts(small["expert_map"], small["n_alive"], w_router=self.wr,
+                              bias=self.bias, w_gate_up=self.wgu, w_down=self.wd,
+                              out={k: small[k] for k in ("w_router", "bias", "w_gate_up",
+                                                         "w_down") if small.get(k) is not None})
+        e.record()
+        torch.cuda.synchronize()
+        self.wr, self.wgu, self.wd = small["w_router"], small["w_gate_up"], small["w_down"]
+        self.bias = small.get("bias")
+        self.E = small["n_alive"]
+        self.keep = alive.cpu().numpy().astype(bool).nonzero()[0]
+        kept = sum(t.numel() * t.element_size() for t in (self.wr, self.wgu, self.wd))
+        us = s.elapsed_time(e) * 1e3
+        self.pruning = {"window_iters": w.prune_window, "alpha": w.prune_alpha,
+                        "beta": w.prune_beta, "experts_before": w.E, "experts_after": self.E,
+                        "weight_bytes_before": big, "weight_bytes_after": kept,
+                        "param_reduction": round(1 - kept / big, 4),
+                        "repack_us": round(us, 1),
+                        "repack_GBs": round(2 * kept / (us * 1e-6) / 1e9, 1)}
+        self.plan = L.MoELayerPlan(w.T, w.d_model, self.E, w.k, w.d_ff, dtype=torch.bfloat16,
+                                   device=self.dev, backward=w.backward)
 
     def calls(self, i):
         """(name, fn) for every call of step i, in order."""
@@ -148,7 +202,7 @@ class Setup:
                                                    renorm=w.renorm, topk_idx=p.topk_idx,
                                                    topk_gate=p.topk_gate)
             out += [("route", route), ("counts", p.count)]
-            if w.prune_beta is not None:
+            if w.prune_beta is not None and not w.prune_window:
                 out += [("prune", lambda: p.prune(w.prune_beta, w.prune_alpha)),
                         ("route_masked", lambda: route(p.alive)), ("counts_masked", p.count)]
             gate = p.topk_gate
@@ -189,7 +243,7 @@ class Setup:
     def algorithmic(self):
         """Algorithmic bytes (HBM-bound calls) or flops (matrix-core calls) per call."""
         w = self.w
-        T, d, E, k, f = w.T, w.d_model, w.E, w.k, w.d_ff
+        T, d, E, k, f = w.T, w.d_model, self.E, w.k, w.d_ff
         R = T * k
         e = 2  # bf16
         by = {
@@ -455,7 +509,7 @@ def main():
     traffic, traffic_src = _traffic(f"{dom}_{w.name}",
                                     FFN_BWD_SOURCES if dom == "ffn_bwd" else FFN_FWD_SOURCES)
     attain = None if args.no_attainable else _attainable(dev)
-    cpu = None if args.no_cpu_baseline else _cpu_baseline(w, su.c, args.cpu_budget)
+    cpu = None if args.no_cpu_baseline else _cpu_baseline(w, su.c, args.cpu_budget, su.keep)
 
     unit = "tokens/s" if w.routed else "rows/s"
     metric = ("MoE-layer tokens/s at 1 GPU; grouped-GEMM TFLOP/s as % bf16 MFMA peak"
@@ -474,7 +528,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; random-init weights)",
-        "config": {"workload": f"{w.name}: T={w.T} d_model={w.d_model} E={w.E} k={w.k} "
+        "config": {"workload": f"{w.name}: T={w.T} d_model={w.d_model} E={w.E}"
+                               + (f" (pruned to {su.E})" if su.E != w.E else "") + f" k={w.k} "
                                f"d_ff={w.d_ff} bf16" + (" fwd+bwd" if w.backward else " fwd"),
                    "tokens": w.T, "experts": w.E, "top_k": w.k, "d_model": w.d_model,
                    "d_ff": w.d_ff},
@@ -488,6 +543,7 @@ def main():
                      "algorithmic_flops_per_call": fl[dom], "mean_call_us": dom_us},
         "cpu_baseline": cpu,
         "attainable": attain,
+        "pruning": su.pruning,
         "breakdown": breakdown,
     }
     print(json.dumps(line), flush=True)

@@ -266,3 +266,55 @@ def test_routed_training_step_full_size():
     assert rownorm_err(hint(plan.dw_router), rw) <= TOL_F32
     assert rownorm_err(hint(plan.dbias), rb) <= TOL_F32
     assert rownorm_err(h32(plan.dx), rx) <= TOL_BF16
+
+
+def test_pruned_compact_layer_full_size():
+    """mild_pruned: Algorithm 1 over a window of routed batches, the pruned
+    experts removed, and the compact layer run at full size against the
+    oracle of the survivors."""
+    w = WORKLOADS["mild_pruned"]
+    c = cached("mild_pruned")
+    x, wr = dev(c["x"], BF), dev(c["w_router"], BF)
+    wgu, wd = dev(c["w_gate_up"], BF), dev(c["w_down"], BF)
+    bias = dev(c["bias"], torch.float32)
+    rng = np.random.default_rng(0)
+    perms = [np.arange(w.T)] + [rng.permutation(w.T) for _ in range(w.prune_window - 1)]
+    pruner = laep.ExpertPruner(w.prune_window, 1, w.E, w.T, w.k, alpha=w.prune_alpha,
+                               beta=w.prune_beta)
+    case("full-size pruned layer: window")
+    for it, pm in enumerate(perms):
+        idx, _ = laep.moe_route(x[torch.from_numpy(pm).cuda()], wr, w.k, bias=bias)
+        laep.moe_expert_counts(idx, w.E, etn_accum=pruner.slot(it, 0))
+    alive, n_pruned, _ = pruner.decide()
+    torch.cuda.synchronize()
+    # the window's loads are the oracle's counts of the device routing of x
+    idx0, _ = laep.moe_route(x, wr, w.k, bias=bias)
+    rc, _, _ = om.expert_counts(hint(idx0), w.E)
+    np.testing.assert_array_equal(hint(pruner.etn)[:, 0], np.stack([rc] * w.prune_window))
+    pruned = ol.expert_pruning(hint(pruner.etn), w.T, w.k, w.prune_alpha, w.prune_beta)[0]
+    a = hint(alive)[0].astype(bool)
+    assert np.nonzero(~a)[0].tolist() == pruned.tolist()
+    print(f"  pruned {len(pruned)} of {w.E} experts")
+    case("full-size pruned layer: compact + forward")
+    small = laep.compact_layer(alive[0].contiguous(), w_router=wr, w_gate_up=wgu, w_down=wd,
+                               bias=bias)
+    E2 = small["n_alive"]
+    keep = np.nonzero(a)[0]
+    assert E2 == len(keep)
+    plan = laep.MoELayerPlan(w.T, w.d_model, E2, w.k, w.d_ff, dtype=BF, device="cuda",
+                             save_act=True)
+    plan.route(x, small["w_router"], bias=small["bias"], renorm=w.renorm)
+    plan.count()
+    plan.experts_and_combine(x, small["w_gate_up"], small["w_down"])
+    torch.cuda.synchronize()
+    ridx, rgate, _, rlog = om.route(c["x"], c["w_router"][keep], w.k, bias=c["bias"][keep],
+                                    renorm=w.renorm)
+    idx = hint(plan.topk_idx)
+    check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k)
+    rc2, ro2, rd2 = om.expert_counts(idx, E2)
+    np.testing.assert_array_equal(hint(plan.counts), rc2)
+    np.testing.assert_array_equal(hint(plan.dest_row), rd2)
+    rows = _sample_rows(ro2, per_expert=2)
+    _check_ffn_rows(plan, c, rows, c["w_gate_up"][keep], c["w_down"][keep])
+    toks = np.random.default_rng(2).choice(w.T, 256, replace=False)
+    _check_combine_tokens(plan, toks)

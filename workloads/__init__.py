@@ -20,6 +20,9 @@ LAEP hot path:
 * ``shard``     one device's expert shard: 16 experts, d=4096, f=2048,
                 32768 routed rows whose expert ids follow Zipf(s=1.1)
 * ``shard_bwd`` ``shard`` plus an upstream gradient ~N(0, 1)
+* ``balanced_bwd`` ``balanced`` plus an upstream gradient (routed training step)
+* ``mild_pruned`` ``skewed_mild``'s draws; the layer after Algorithm 1 has
+                removed its pruned experts
 
 The paper's own pre-training corpus and trained weights are not available;
 these seeded inputs stand in for its stable-phase expert loads (a few
@@ -53,6 +56,9 @@ class Workload:
     prune_beta: Optional[float] = None
     prune_alpha: float = math.inf
     weight_std: float = 0.02
+    # > 0: before the timed steps, Algorithm 1 runs over a window of this
+    # many routed batches and the pruned experts are removed (compact layer)
+    prune_window: int = 0
 
     @property
     def rows(self) -> int:
@@ -76,6 +82,12 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("shard_bwd", 1005, T=32768, d_model=4096, E=16, k=1,
                  d_ff=2048, dtype="bf16", renorm=False, routed=False,
                  zipf_s=1.1, backward=True),
+        # steady state after pruning: the skewed_mild generator, Algorithm 1 over
+        # a window of 3 batches with a middle layer's setting of the paper's
+        # pre-training run (alpha = 0.4, beta = 0.1), pruned experts removed
+        Workload("mild_pruned", 1013, T=8192, d_model=2048, E=64, k=8, d_ff=1024,
+                 dtype="bf16", renorm=True, bias_std=0.5, prune_beta=0.1,
+                 prune_alpha=0.4, prune_window=3),
         # routed pre-training step: balanced forward, then backward through the
         # combine, the expert FFN, the dispatch and the router
         Workload("balanced_bwd", 1006, T=8192, d_model=2048, E=64, k=8, d_ff=1024,
