@@ -21,6 +21,8 @@ Prints ONE JSON line:
   breakdown    every call: mean / median / p10 / p90 microseconds over the timed
                steps and its rate on algorithmic bytes or flops
   attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
+  supplementary  moe_expert_counts at T x {1, 8, 64} tokens, and route followed
+               by counts as one timed pair
   cpu_baseline the float64 CPU oracle timed on a bounded token sample
 
 Other workloads: skewed, skewed_mild (routed, pruned every step), shard (16
@@ -301,6 +303,51 @@ def _attainable(dev):
             "mfma_frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 3)}
 
 
+def _supplementary(w, su, dev, reps=20):
+    """Latency-bound calls at other sizes: moe_expert_counts over T x {1, 8, 64}
+    (random distinct expert ids, the workload's E and k), and route followed
+    by counts as one event pair (the two calls the routing front end makes)."""
+    import numpy as np
+    import torch
+
+    L = su.laep
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            s.record()
+            fn()
+            e.record()
+            torch.cuda.synchronize()
+            ts.append(s.elapsed_time(e) * 1e3)
+        return round(sorted(ts)[len(ts) // 2], 2)
+
+    rng = np.random.default_rng(0)
+    sweep = []
+    for mult in (1, 8, 64):
+        T = w.T * mult
+        ids = np.argsort(rng.random((T, su.E)), axis=1)[:, :w.k].astype(np.int32)
+        idx = torch.from_numpy(ids).to(dev)
+        ws = torch.empty(max(1, L.workspace_bytes(1, T, w.k, su.E)), dtype=torch.uint8,
+                         device=dev)
+        bufs = dict(counts=torch.empty(su.E, dtype=torch.int32, device=dev),
+                    offsets=torch.empty(su.E + 1, dtype=torch.int32, device=dev),
+                    dest_row=torch.empty(T * w.k, dtype=torch.int32, device=dev))
+        us = timed(lambda: L.moe_expert_counts(idx, su.E, ws=ws, **bufs))
+        nbytes = T * w.k * 4 * 2 + 2 * (su.E + 1) * 4
+        sweep.append({"tokens": T, "median_us": us, "GBs": round(nbytes / (us * 1e-6) / 1e9, 1)})
+        del idx, ws, bufs
+    out = {"counts_T_sweep": sweep}
+    if w.routed:
+        p, x = su.plan, su.xs[0]
+        out["route_then_counts_us"] = timed(lambda: (
+            L.moe_route(x, su.wr, w.k, bias=su.bias, renorm=w.renorm, topk_idx=p.topk_idx,
+                        topk_gate=p.topk_gate), p.count()))
+    return out
+
+
 def _traffic(name, sources):
     """HBM bytes per call from the committed counter summary, if still valid."""
     path = os.path.join(PROFILES, f"{name}_traffic.md")
@@ -509,6 +556,7 @@ def main():
     traffic, traffic_src = _traffic(f"{dom}_{w.name}",
                                     FFN_BWD_SOURCES if dom == "ffn_bwd" else FFN_FWD_SOURCES)
     attain = None if args.no_attainable else _attainable(dev)
+    supp = None if args.no_attainable else _supplementary(w, su, dev)
     cpu = None if args.no_cpu_baseline else _cpu_baseline(w, su.c, args.cpu_budget, su.keep)
 
     unit = "tokens/s" if w.routed else "rows/s"
@@ -544,6 +592,7 @@ def main():
         "cpu_baseline": cpu,
         "attainable": attain,
         "pruning": su.pruning,
+        "supplementary": supp,
         "breakdown": breakdown,
     }
     print(json.dumps(line), flush=True)

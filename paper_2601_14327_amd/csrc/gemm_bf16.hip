@@ -26,6 +26,8 @@
 // while step i computes, the B half of step i+1 and the A half of step i+2
 // are in flight: every half has at least one whole k-step (2048 MFMA cycles
 // per SIMD) to land.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 #include "tiles.hpp"
@@ -204,6 +206,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
   static_assert(BM == BN, "ring slots hold either operand");
   static_assert(BM * (BN * 2 + 16) <= SMEM, "staging tile must fit in LDS");
   static_assert(EPI != EPI_GU || (TN % 2 == 0), "SwiGLU epilogue pairs gate/up blocks");
+  static_assert(TM == 4, "the ragged-tile dispatch below covers 0..4 row blocks");
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   const int L = xcd_tile(p);
@@ -256,15 +259,6 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
     const int r = wn * WTN + j * 32 + (lane & 31);
     b_off[j] = r * ROWB + ((lc0 ^ swz8(r)) << 4);
   }
-  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-  // reads in the order the MFMAs consume them (B0 A0 B1 A1 ...)
-  auto read_frags = [&](const char* sa, const char* sb, int s, u32x4_t* fa, u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < (TM > TN ? TM : TN); ++i) {
-      if (i < TN) fb[i] = *reinterpret_cast<const u32x4_t*>(sb + (b_off[i] ^ (s << 5)));
-      if (i < TM) fa[i] = *reinterpret_cast<const u32x4_t*>(sa + (a_off[i] ^ (s << 5)));
-    }
-  };
   f32x16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -272,59 +266,87 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-  auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
-            0, 0, 0);
-  };
-  // the next sub-step's fragment reads alternate with this one's MFMAs
-  auto interleave = [&]() {
-#pragma unroll
-    for (int i = 0; i < TM + TN; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - TM - TN, 0);
-  };
 
-  // prologue: halves 0 .. 4 in flight, step 0 (halves 0, 1) landed
+  // The main loop, for a wave whose first TMV 32-row MFMA blocks hold rows of
+  // the expert (a ragged last tile leaves the others empty: their MFMAs and
+  // A-fragment reads are skipped, the loads and barriers are not).
+  auto main_loop = [&](auto tmv_tag) {
+    constexpr int TMV = decltype(tmv_tag)::value;
+    constexpr int NRD = TMV > 0 ? TMV + TN : 0;  // DS reads per k16 sub-step
+    constexpr int NMM = TMV * TN;                // MFMAs per k16 sub-step
+    u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+    // reads in the order the MFMAs consume them (B0 A0 B1 A1 ...)
+    auto read_frags = [&](const char* sa, const char* sb, int s, u32x4_t* fa, u32x4_t* fb) {
+      if (TMV == 0) return;
 #pragma unroll
-  for (int h = 0; h < NSLOT; ++h) issue_half(h);
-  wait_vmcnt<3 * NH>();
-  __builtin_amdgcn_s_barrier();
-  int ia = 0, ib = 1;  // slots of the current step's A and B halves
-  read_frags(smem, smem + HALF, 0, fa0, fb0);
+      for (int i = 0; i < (TMV > TN ? TMV : TN); ++i) {
+        if (i < TN) fb[i] = *reinterpret_cast<const u32x4_t*>(sb + (b_off[i] ^ (s << 5)));
+        if (i < TMV) fa[i] = *reinterpret_cast<const u32x4_t*>(sa + (a_off[i] ^ (s << 5)));
+      }
+    };
+    auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
+#pragma unroll
+      for (int i = 0; i < TMV; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
+              0, 0, 0);
+    };
+    // the next sub-step's fragment reads alternate with this one's MFMAs
+    auto interleave = [&]() {
+      constexpr int NP = NRD < NMM ? NRD : NMM;
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+      }
+      if (NMM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NMM - NP, 0);
+      if (NRD > NP) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NP, 0);
+    };
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const char* sa = smem + ia * HALF;
-    const char* sb = smem + ib * HALF;
-    read_frags(sa, sb, 1, fa1, fb1);
-    mma_step(fa0, fb0);
-    interleave();
-    read_frags(sa, sb, 2, fa0, fb0);
-    mma_step(fa1, fb1);
-    interleave();
-    read_frags(sa, sb, 3, fa1, fb1);
-    mma_step(fa0, fb0);
-    interleave();
-    // step boundary: this thread's reads of step kt are in registers and its
-    // loads of step kt+1 have landed (only the A half of step kt+2 may still
-    // be in flight); past the barrier the same holds for every thread, so the
-    // two halves of step kt are free: they receive B of kt+2 and A of kt+3.
-    wait_vmcnt_lgkm0<NH>();
+    // prologue: halves 0 .. 4 in flight, step 0 (halves 0, 1) landed
+#pragma unroll
+    for (int h = 0; h < NSLOT; ++h) issue_half(h);
+    wait_vmcnt<3 * NH>();
     __builtin_amdgcn_s_barrier();
-    issue_half(2 * kt + 5);
-    issue_half(2 * kt + 6);
-    ia = ia + 2 >= NSLOT ? ia + 2 - NSLOT : ia + 2;
-    ib = ib + 2 >= NSLOT ? ib + 2 - NSLOT : ib + 2;
-    read_frags(smem + ia * HALF, smem + ib * HALF, 0, fa0, fb0);
-    mma_step(fa1, fb1);
-    interleave();
-  }
+    int ia = 0, ib = 1;  // slots of the current step's A and B halves
+    read_frags(smem, smem + HALF, 0, fa0, fb0);
+
+    for (int kt = 0; kt < nk; ++kt) {
+      const char* sa = smem + ia * HALF;
+      const char* sb = smem + ib * HALF;
+      read_frags(sa, sb, 1, fa1, fb1);
+      mma_step(fa0, fb0);
+      interleave();
+      read_frags(sa, sb, 2, fa0, fb0);
+      mma_step(fa1, fb1);
+      interleave();
+      read_frags(sa, sb, 3, fa1, fb1);
+      mma_step(fa0, fb0);
+      interleave();
+      // step boundary: this thread's reads of step kt are in registers and its
+      // loads of step kt+1 have landed (only the A half of step kt+2 may still
+      // be in flight); past the barrier the same holds for every thread, so the
+      // two halves of step kt are free: they receive B of kt+2 and A of kt+3.
+      wait_vmcnt_lgkm0<NH>();
+      __builtin_amdgcn_s_barrier();
+      issue_half(2 * kt + 5);
+      issue_half(2 * kt + 6);
+      ia = ia + 2 >= NSLOT ? ia + 2 - NSLOT : ia + 2;
+      ib = ib + 2 >= NSLOT ? ib + 2 - NSLOT : ib + 2;
+      read_frags(smem + ia * HALF, smem + ib * HALF, 0, fa0, fb0);
+      mma_step(fa1, fb1);
+      interleave();
+    }
+  };
+  // wave-uniform count of this wave's 32-row blocks that hold expert rows
+  const int tmv = min(TM, max(0, (te.rows - wm * WTM + 31) >> 5));
+  if (tmv >= TM) main_loop(std::integral_constant<int, TM>{});
+  else if (tmv == 3) main_loop(std::integral_constant<int, 3>{});
+  else if (tmv == 2) main_loop(std::integral_constant<int, 2>{});
+  else if (tmv == 1) main_loop(std::integral_constant<int, 1>{});
+  else main_loop(std::integral_constant<int, 0>{});
   // no LDS-DMA may still be writing when the LDS is reused or the workgroup retires
   wait_vmcnt<0>();
   wait_lgkm0();
