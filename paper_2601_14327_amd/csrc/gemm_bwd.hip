@@ -236,9 +236,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-
-  if (nk > 0) {
+  // The main loop, for a wave whose first TMV 32-row MFMA blocks hold rows of
+  // the tile (the data gradients' ragged last row tile leaves the others
+  // empty: their MFMAs and A-fragment reads are skipped, loads and barriers
+  // are not).  Weight-gradient tiles are always full.
+  auto main_loop = [&](auto tmv_tag) {
+    constexpr int TMV = decltype(tmv_tag)::value;
+    u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
     auto issue = [&](int kt) {
       char* st = smem + (kt % NS) * STAGE;
       const int kk = kt < nk ? kt : nk - 1;
@@ -249,8 +253,9 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     // k16 step s of a stage: normal operands flip the logical chunk by 2
     // (byte offset ^ 32 s); TR operands move down 16 k-rows (+ 16 * 512 s)
     auto read_step = [&](const char* st, int s, u32x4_t* fa, u32x4_t* fb) {
+      if (TMV == 0) return;
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TMV; ++i) {
         if (A_TR) fa[i] = read_tr_frag(st, a_o1[i] + s * 8192, a_o2[i] + s * 8192);
         else fa[i] = *reinterpret_cast<const u32x4_t*>(st + (a_o1[i] ^ (s << 5)));
       }
@@ -262,7 +267,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     };
     auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TMV; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -285,6 +290,20 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       mma_step(fa1, fb1);
     }
     wait_vmcnt<0>();
+  };
+
+  if (nk > 0) {
+    if (EPI == EPI_WGRAD) {
+      main_loop(std::integral_constant<int, TM>{});
+    } else {
+      static_assert(EPI == EPI_WGRAD || TM == 4, "the ragged-tile dispatch covers 0..4 blocks");
+      const int tmv = min(TM, max(0, (te.rows - wm * WTM + 31) >> 5));
+      if (tmv >= TM) main_loop(std::integral_constant<int, TM>{});
+      else if (tmv == 3) main_loop(std::integral_constant<int, 3>{});
+      else if (tmv == 2) main_loop(std::integral_constant<int, 2>{});
+      else if (tmv == 1) main_loop(std::integral_constant<int, 1>{});
+      else main_loop(std::integral_constant<int, 0>{});
+    }
   }
 
   // ---- epilogues (staged through LDS) -------------------------------------------
