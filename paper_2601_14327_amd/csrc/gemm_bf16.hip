@@ -48,17 +48,6 @@ __device__ __forceinline__ void dma_chunks(char* dst, const bf16_t* const* src, 
                                      16, 0, 0);
 }
 
-// s_waitcnt vmcnt(N) lgkmcnt(0)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt_lgkm0() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
-}
-
-// 128-byte LDS rows (8 chunks): chunk c of row r at c ^ ((r ^ r >> 3) & 7),
-// measured free of bank conflicts for the fragment reads.
-__device__ __forceinline__ int swz8(int row) { return (row ^ (row >> 3)) & 7; }
-
 // Tile of the XCD-contiguous schedule owned by this workgroup, or -1.
 __device__ __forceinline__ int xcd_tile(const GemmParams& p) {
   const int n_valid = (*p.n_entries) * p.tiles_per_entry;

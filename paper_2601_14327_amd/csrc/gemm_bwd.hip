@@ -7,17 +7,22 @@
 //             dW_gu[p] = dA^T X     -> fp32 weight gradients, one tile per expert
 //             and output block, the reduction running over the expert's rows.
 //
-// Same pipeline as the forward kernels: 256 x 256 tiles, 8 waves (2 x 4),
-// k-tiles of 32 moved by LDS-DMA through NS stages, one barrier per k-tile.
-// Operands whose K is the strided global dimension are stored in LDS as
-// [32 k][256 features] rows (512 contiguous bytes per global row segment) and
-// turned into MFMA operands with ds_read_b64_tr_b16: within each 16-lane
-// group, lane j receives feature j of four consecutive k-rows, so two such
-// reads give a lane the same 8 consecutive k values a ds_read_b128 gives for
-// a K-contiguous operand.  The 32-byte block b of k-row r is stored at
-// b ^ ((r & 7) << 1), so the four k-rows a group reads fall in different
-// banks.  Rows past the end of an expert (the ragged reduction of the weight
-// gradient) are loaded from a zero page.
+// Same pipeline as the forward kernels: 256 x 256 tiles, 8 waves (2 x 4, each
+// 128 x 64), k-steps of 64 through a ring of five 32 KB halves (one operand's
+// k-step each), LDS-DMA loads, one barrier per k-step.  A K-contiguous
+// operand is stored as in the forward ([256 rows][64 k], 128-byte rows).
+// Operands whose K is the strided global dimension are stored as
+// [64 k][256 features] rows (512 contiguous bytes per global row segment, so
+// every request is a whole line) and turned into MFMA operands with
+// ds_read_b64_tr_b16: within each 16-lane group, lane j receives feature j of
+// four consecutive k-rows, so two such reads give a lane the same 8
+// consecutive k values a ds_read_b128 gives for a K-contiguous operand.  The
+// 32-byte block b of k-row r is stored at b ^ ((r & 7) << 1), so the four
+// k-rows a group reads fall in different banks.  Rows past the end of an
+// expert (the ragged reduction of the weight gradient) are loaded from a zero
+// page.
+#include <type_traits>
+
 #include "gemm_common.hpp"
 
 namespace laep {
@@ -26,19 +31,11 @@ namespace {
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// One operand's LDS tile for one stage (32 k).
-//   TR == false: [ROWS][32] bf16, 64-byte rows, chunk c of row r at c ^ pswz(r)
-//   TR == true : [32][ROWS] bf16, 2*ROWS-byte rows, 32-byte block b of row r at
-//                b ^ ((r & 7) << 1)
-template <int ROWS, int NT, bool TR>
-struct OperandTile {
-  static constexpr int BYTES = ROWS * 64;
-  static constexpr int NC = ROWS * 4 / NT;    // 16-byte chunks per thread per stage
-  static constexpr int CPR = ROWS / 8;        // 16-byte chunks per k-row (TR)
-  static constexpr int RB = ROWS * 2;         // bytes per k-row (TR)
-  static_assert(!TR || ROWS == 256, "transposed tiles are 256 features wide");
-  static_assert((ROWS * 4) % NT == 0, "chunks must divide over the threads");
-};
+constexpr int kRingRowB = 128;              // K-contiguous half: bytes per row (64 k)
+constexpr int kRingHalf = 256 * kRingRowB;   // one operand's k-step: 32 KB
+constexpr int kRingSlots = 5;
+constexpr int kTrRowB = 512;                 // K-strided half: bytes per k-row (256 features)
+constexpr int kTrCpr = kTrRowB / 16;         // 16-byte chunks per k-row
 
 // LDS slot q of a TR tile -> (k-row, element column within the tile)
 __device__ __forceinline__ void tr_slot(int q, int cpr, int& r, int& col) {
@@ -65,39 +62,40 @@ __device__ __forceinline__ u32x4_t read_tr_frag(const char* st, int off1, int of
   return v;
 }
 
-// One k-tile of LDS-DMA loads of one operand.  base[i] is chunk i's global
-// address at k-tile 0; kstep the element stride between k-tiles; for TR
-// operands rows at or past kvalid come from the zero page.
+// One half (one operand's k-step ks) of LDS-DMA loads: NC 16-byte chunks per
+// thread, chunk i of thread tid in LDS slot i * NT + tid.  base[i] is the
+// chunk's global address at k-step 0 and kstep the element stride between
+// k-steps; for K-strided operands k-rows at or past kvalid come from the zero
+// page (a device function, not a lambda: the host pass must not see the
+// LDS-DMA builtin inside a lambda).
 template <int NC, int NT, bool TR>
-__device__ __forceinline__ void dma_operand(char* st, const bf16_t* const* base, const int* krow,
-                                            long long kstep, int kt, int kvalid,
-                                            const bf16_t* zero, int wave) {
+__device__ __forceinline__ void dma_half(char* dst, const bf16_t* const* base, const int* krow,
+                                         long long kstep, int ks, int kvalid, const bf16_t* zero,
+                                         int wave) {
 #pragma unroll
   for (int i = 0; i < NC; ++i) {
-    const bf16_t* src = base[i] + kstep * kt;
-    if (TR && kt * 32 + krow[i] >= kvalid) src = zero;
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(st + (i * NT + wave * 64) * 16), 16, 0, 0);
+    const bf16_t* src = base[i] + kstep * ks;
+    if (TR && ks * 64 + krow[i] >= kvalid) src = zero;
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(dst + (i * NT + wave * 64) * 16), 16, 0,
+                                     0);
   }
 }
 
-template <int BM, int BN, int NWM, int NWN, int NS, int EPI, bool A_TR, bool B_TR>
+template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) {
   constexpr int NT = 64 * NWM * NWN;
   constexpr int WTM = BM / NWM, WTN = BN / NWN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  using OA = OperandTile<BM, NT, A_TR>;
-  using OB = OperandTile<BN, NT, B_TR>;
-  constexpr int A_BYTES = OA::BYTES;
-  constexpr int STAGE = OA::BYTES + OB::BYTES;
-  constexpr int NLD = OA::NC + OB::NC;
-  static_assert(NS >= 3, "at least three stages");
-  static_assert(NWM == 2 && BM == 256, "the staged epilogues process one wave row per pass");
+  constexpr int NH = kRingHalf / 16 / NT;  // 16-byte chunks per thread per half
+  static_assert(BM == 256 && BN == 256 && NT == 512, "ring halves are 256 x 64 / 64 x 256");
+  static_assert(NWM == 2, "the staged epilogues process one wave row per pass");
   constexpr int PITCH16 = BN * 2 + 16;   // bf16 staging pitch
   constexpr int PITCH32 = BN * 4 + 16;   // fp32 staging pitch
   constexpr int EPI_BYTES = (EPI == EPI_WGRAD)  ? 128 * PITCH32
                             : (EPI == EPI_GU_BWD) ? 3 * 64 * PITCH16
                                                   : BM * PITCH16;
-  constexpr int SMEM = NS * STAGE > EPI_BYTES ? NS * STAGE : EPI_BYTES;
+  constexpr int RING = kRingSlots * kRingHalf;
+  constexpr int SMEM = RING > EPI_BYTES ? RING : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
 
   // ---- tile schedule --------------------------------------------------------
@@ -142,62 +140,62 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave / NWN, wn = wave % NWN;
 
-  // reduction extent of this tile
+  // reduction extent of this tile (a multiple of 64 for the data gradients)
   const int kext = (EPI == EPI_WGRAD) ? te.rows : p.K;
-  const int nk = (kext + 31) / 32;
+  const int nk = (kext + 63) / 64;
 
-  // ---- per-thread DMA sources ---------------------------------------------------
-  const bf16_t* a_base[OA::NC];
-  int a_krow[OA::NC];
-  long long a_kstep;
+  // ---- per-thread DMA sources (k-step 0) ----------------------------------------
+  const bf16_t* a_base[NH];
+  int a_krow[NH];
 #pragma unroll
-  for (int i = 0; i < OA::NC; ++i) {
+  for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
     if (A_TR) {  // weight gradient: [routed rows][Mw], k = row, feature = mt*BM + col
       int r, col;
-      tr_slot(q, OA::CPR, r, col);
+      tr_slot(q, kTrCpr, r, col);
       int c = mt * BM + col;
       c = c < p.Mw ? c : p.Mw - 8;  // columns past Mw: any valid column (not stored)
       a_krow[i] = r;
       a_base[i] = p.A + (long long)(te.row0 + r) * p.lda + c;
     } else {     // data gradient: expert rows, K contiguous
-      const int r = q >> 2;
-      const int lc = (q & 3) ^ pswz(r);
-      const int rr = r < te.rows ? r : te.rows - 1;
+      const int r = q >> 3;
+      const int lc = (q & 7) ^ swz8(r);
+      const int rr = r < te.rows ? r : te.rows - 1;  // rows past the expert: any valid row
       a_krow[i] = 0;
       a_base[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
     }
   }
-  a_kstep = A_TR ? 32LL * p.lda : 32LL;
-  const bf16_t* b_base[OB::NC];
-  int b_krow[OB::NC];
-  long long b_kstep;
+  const long long a_kstep = A_TR ? 64LL * p.lda : 64LL;
+  // B is K-strided in every backward product: [K][N] rows, feature nt*BN + col
+  // (clamped to the last valid column block)
+  const bf16_t* b_base[NH];
+  int b_krow[NH];
   const bf16_t* Bw = (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb
                                         : p.B + (long long)te.phys * p.strideB;
 #pragma unroll
-  for (int i = 0; i < OB::NC; ++i) {
+  for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
-    if (B_TR) {  // [K][N] rows, feature = nt*BN + col (clamped to the last valid column block)
-      int r, col;
-      tr_slot(q, OB::CPR, r, col);
-      int c = nt * BN + col;
-      c = c < p.N ? c : p.N - 8;
-      b_krow[i] = r;
-      b_base[i] = Bw + (long long)r * p.ldb + c;
-    } else {
-      const int r = q >> 2;
-      const int lc = (q & 3) ^ pswz(r);
-      int row = nt * BN + r;
-      row = row < p.N ? row : p.N - 1;
-      b_krow[i] = 0;
-      b_base[i] = Bw + (long long)row * p.ldb + lc * 8;
-    }
+    int r, col;
+    tr_slot(q, kTrCpr, r, col);
+    int c = nt * BN + col;
+    c = c < p.N ? c : p.N - 8;
+    b_krow[i] = r;
+    b_base[i] = Bw + (long long)r * p.ldb + c;
   }
-  b_kstep = B_TR ? 32LL * p.ldb : 32LL;
+  const long long b_kstep = 64LL * p.ldb;
   const int kvalid_a = A_TR ? kext : (1 << 30);
-  const int kvalid_b = (B_TR && EPI == EPI_WGRAD) ? kext : (1 << 30);
+  const int kvalid_b = (EPI == EPI_WGRAD) ? kext : (1 << 30);
+  // half h: A of k-step h/2 (h even) or B (h odd), in slot h % 5.  Past the
+  // end the last k-step is loaded again (never read), so every iteration
+  // issues the same number of loads and one constant vmcnt serves every wait.
+  auto issue_half = [&](int h) {
+    const int ks = min(h >> 1, nk - 1);
+    char* dst = smem + (h % kRingSlots) * kRingHalf;
+    if (h & 1) dma_half<NH, NT, true>(dst, b_base, b_krow, b_kstep, ks, kvalid_b, p.zero, wave);
+    else dma_half<NH, NT, A_TR>(dst, a_base, a_krow, a_kstep, ks, kvalid_a, p.zero, wave);
+  };
 
-  // ---- fragment offsets -------------------------------------------------------------
+  // ---- fragment offsets within a half, k16 sub-step 0 -------------------------------
   const int lc0 = lane >> 5;
   const int gh = (lane >> 4) & 1;
   const int li = lane & 15;
@@ -211,21 +209,15 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       a_o2[i] = tr_off(rk + 4, mf, gh, li);
     } else {
       const int r = wm * WTM + i * 32 + (lane & 31);
-      a_o1[i] = r * PROW + ((lc0 ^ pswz(r)) << 4);
+      a_o1[i] = r * kRingRowB + ((lc0 ^ swz8(r)) << 4);
       a_o2[i] = 0;
     }
   }
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
-    if (B_TR) {
-      const int mf = wn * WTN + j * 32;
-      b_o1[j] = A_BYTES + tr_off(rk, mf, gh, li);
-      b_o2[j] = A_BYTES + tr_off(rk + 4, mf, gh, li);
-    } else {
-      const int r = wn * WTN + j * 32 + (lane & 31);
-      b_o1[j] = A_BYTES + r * PROW + ((lc0 ^ pswz(r)) << 4);
-      b_o2[j] = 0;
-    }
+    const int mf = wn * WTN + j * 32;
+    b_o1[j] = tr_off(rk, mf, gh, li);
+    b_o2[j] = tr_off(rk + 4, mf, gh, li);
   }
 
   f32x16_t acc[TM][TN];
@@ -243,26 +235,17 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   auto main_loop = [&](auto tmv_tag) {
     constexpr int TMV = decltype(tmv_tag)::value;
     u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
-    auto issue = [&](int kt) {
-      char* st = smem + (kt % NS) * STAGE;
-      const int kk = kt < nk ? kt : nk - 1;
-      dma_operand<OA::NC, NT, A_TR>(st, a_base, a_krow, a_kstep, kk, kvalid_a, p.zero, wave);
-      dma_operand<OB::NC, NT, B_TR>(st + A_BYTES, b_base, b_krow, b_kstep, kk, kvalid_b, p.zero,
-                                    wave);
-    };
-    // k16 step s of a stage: normal operands flip the logical chunk by 2
-    // (byte offset ^ 32 s); TR operands move down 16 k-rows (+ 16 * 512 s)
-    auto read_step = [&](const char* st, int s, u32x4_t* fa, u32x4_t* fb) {
+    // k16 sub-step s of a k-step: K-contiguous fragments flip the logical
+    // chunk by 2 (byte offset ^ 32 s); TR fragments move down 16 k-rows
+    auto read_frags = [&](const char* sa, const char* sb, int s, u32x4_t* fa, u32x4_t* fb) {
       if (TMV == 0) return;
 #pragma unroll
-      for (int i = 0; i < TMV; ++i) {
-        if (A_TR) fa[i] = read_tr_frag(st, a_o1[i] + s * 8192, a_o2[i] + s * 8192);
-        else fa[i] = *reinterpret_cast<const u32x4_t*>(st + (a_o1[i] ^ (s << 5)));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        if (B_TR) fb[j] = read_tr_frag(st, b_o1[j] + s * 8192, b_o2[j] + s * 8192);
-        else fb[j] = *reinterpret_cast<const u32x4_t*>(st + (b_o1[j] ^ (s << 5)));
+      for (int i = 0; i < (TMV > TN ? TMV : TN); ++i) {
+        if (i < TN) fb[i] = read_tr_frag(sb, b_o1[i] + s * 16 * kTrRowB, b_o2[i] + s * 16 * kTrRowB);
+        if (i < TMV) {
+          if (A_TR) fa[i] = read_tr_frag(sa, a_o1[i] + s * 16 * kTrRowB, a_o2[i] + s * 16 * kTrRowB);
+          else fa[i] = *reinterpret_cast<const u32x4_t*>(sa + (a_o1[i] ^ (s << 5)));
+        }
       }
     };
     auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
@@ -274,21 +257,37 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
               __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
               0, 0, 0);
     };
+
+    // prologue: halves 0 .. 4 in flight, step 0 (halves 0, 1) landed
 #pragma unroll
-    for (int t = 0; t < NS - 1; ++t) issue(t);
-    wait_vmcnt<(NS - 2) * NLD>();
+    for (int h = 0; h < kRingSlots; ++h) issue_half(h);
+    wait_vmcnt<3 * NH>();
     __builtin_amdgcn_s_barrier();
-    read_step(smem, 0, fa0, fb0);
+    int ia = 0, ib = 1;  // slots of the current step's A and B halves
+    read_frags(smem, smem + kRingHalf, 0, fa0, fb0);
     for (int kt = 0; kt < nk; ++kt) {
-      const char* st = smem + (kt % NS) * STAGE;
-      read_step(st, 1, fa1, fb1);
+      const char* sa = smem + ia * kRingHalf;
+      const char* sb = smem + ib * kRingHalf;
+      read_frags(sa, sb, 1, fa1, fb1);
       mma_step(fa0, fb0);
-      wait_vmcnt<(NS - 3) * NLD>();
+      read_frags(sa, sb, 2, fa0, fb0);
+      mma_step(fa1, fb1);
+      read_frags(sa, sb, 3, fa1, fb1);
+      mma_step(fa0, fb0);
+      // step boundary: this thread's reads of step kt are in registers and its
+      // loads of step kt+1 have landed (only the A half of step kt+2 may still
+      // be in flight); past the barrier the same holds for every thread, so the
+      // two halves of step kt are free: they receive B of kt+2 and A of kt+3.
+      wait_vmcnt_lgkm0<NH>();
       __builtin_amdgcn_s_barrier();
-      issue(kt + NS - 1);
-      read_step(smem + ((kt + 1) % NS) * STAGE, 0, fa0, fb0);
+      issue_half(2 * kt + 5);
+      issue_half(2 * kt + 6);
+      ia = ia + 2 >= kRingSlots ? ia + 2 - kRingSlots : ia + 2;
+      ib = ib + 2 >= kRingSlots ? ib + 2 - kRingSlots : ib + 2;
+      read_frags(smem + ia * kRingHalf, smem + ib * kRingHalf, 0, fa0, fb0);
       mma_step(fa1, fb1);
     }
+    // no LDS-DMA may still be writing when the LDS is reused for staging
     wait_vmcnt<0>();
   };
 
@@ -455,11 +454,11 @@ __global__ void zero_page_kernel(uint32_t* z, int n) {
 constexpr int kBwdBM = 256, kBwdBN = 256;
 constexpr int kZeroBytes = 1024;
 
-template <int EPI, bool A_TR, bool B_TR>
+template <int EPI, bool A_TR>
 hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, 5, EPI, A_TR, B_TR>),
-                     dim3(round8(grid)), dim3(512), 0, s, p);
+  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, EPI, A_TR>), dim3(round8(grid)),
+                     dim3(512), 0, s, p);
   return hipGetLastError();
 }
 
@@ -517,7 +516,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.out = dA;
   g.out2 = Hb;
   g.aux = static_cast<const bf16_t*>(act_save);
-  hipError_t err = launch_bwd<EPI_GU_BWD, false, true>(g, max_ragged * g.n_tiles_n, s);
+  hipError_t err = launch_bwd<EPI_GU_BWD, false>(g, max_ragged * g.n_tiles_n, s);
   if (err != hipSuccess) return err;
 
   // dgrad 2: dX = dA W_gu
@@ -534,7 +533,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.ldo = d;
   g.out2 = nullptr;
   g.aux = nullptr;
-  err = launch_bwd<EPI_STORE, false, true>(g, max_ragged * g.n_tiles_n, s);
+  err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
   if (err != hipSuccess) return err;
 
   // wgrad W_d: dW_d[p] [d, f] = dY^T H_b over the expert's rows
@@ -555,7 +554,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   w.wout = dw_d;
   w.strideW = (long long)d * f;
   w.accumulate = accumulate;
-  err = launch_bwd<EPI_WGRAD, true, true>(w, E * w.tiles_per_entry, s);
+  err = launch_bwd<EPI_WGRAD, true>(w, E * w.tiles_per_entry, s);
   if (err != hipSuccess) return err;
 
   // wgrad W_gu: dW_gu[p] [2f, d] = dA^T X
@@ -569,7 +568,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   w.tiles_per_entry = ceil_div(2 * f, kBwdBM) * w.n_tiles_n;
   w.wout = dw_gu;
   w.strideW = (long long)2 * f * d;
-  return launch_bwd<EPI_WGRAD, true, true>(w, E * w.tiles_per_entry, s);
+  return launch_bwd<EPI_WGRAD, true>(w, E * w.tiles_per_entry, s);
 }
 
 }  // namespace laep

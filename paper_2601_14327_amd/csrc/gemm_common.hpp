@@ -60,10 +60,10 @@ __device__ __forceinline__ void load_bf16x4(const bf16_t* p, float v[4]) {
   v[3] = hi_bf16(w[1]);
 }
 
-constexpr int PBK = 32;          // k per pipeline stage
-constexpr int PROW = PBK * 2;    // bytes per LDS row
-
-__device__ __forceinline__ int pswz(int row) { return (row >> 2) & 3; }
+// 128-byte LDS rows (64 k of bf16, 8 chunks of 16 bytes): chunk c of row r
+// at c ^ ((r ^ r >> 3) & 7), measured free of bank conflicts for the
+// ds_read_b128 fragment reads.
+__device__ __forceinline__ int swz8(int row) { return (row ^ (row >> 3)) & 7; }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -78,6 +78,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// s_waitcnt vmcnt(N) lgkmcnt(0)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
 
 inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 inline int round8(int v) { return (v + 7) & ~7; }
