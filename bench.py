@@ -4,7 +4,7 @@
 Default workload ("balanced"): T=8192 tokens, d_model=2048, 64 experts,
 top-8 renormalised softmax gating, SwiGLU d_ff=1024, bf16 with fp32
 accumulation.  One step = one forward pass of the whole layer:
-route -> expert counts -> dispatch + grouped SwiGLU FFN (one call, the
+route + expert counts (one call) -> dispatch + grouped SwiGLU FFN (one call, the
 dispatch folded into the FFN's operand loads) -> combine, every call a kernel
 of the C-ABI library; three input sets rotate over the steps so the
 activations are not cache-resident.  Training steps (shard_bwd) keep the
@@ -21,8 +21,8 @@ Prints ONE JSON line:
   breakdown    every call: mean / median / p10 / p90 microseconds over the timed
                steps and its rate on algorithmic bytes or flops
   attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
-  supplementary  moe_expert_counts at T x {1, 8, 64} tokens, and route followed
-               by counts as one timed pair
+  supplementary  moe_expert_counts at T x {1, 8, 64} tokens; route, counts, the
+               two back to back, and the fused moe_route_count, each timed alone
   cpu_baseline the float64 CPU oracle timed on a bounded token sample
 
 Other workloads: skewed, skewed_mild (routed, pruned every step), shard (16
@@ -199,14 +199,13 @@ class Setup:
         x = self.xs[i % self.n_sets]
         R = w.T * w.k
         out = []
-        if w.routed:
-            route = lambda alive=None: L.moe_route(x, self.wr, w.k, bias=self.bias, alive=alive,
-                                                   renorm=w.renorm, topk_idx=p.topk_idx,
-                                                   topk_gate=p.topk_gate)
-            out += [("route", route), ("counts", p.count)]
+        if w.routed:   # routing and expert counts: one call (the router writes the count masks)
+            rc = lambda alive=None: p.route_count(x, self.wr, bias=self.bias, alive=alive,
+                                                  renorm=w.renorm)
+            out += [("route_count", rc)]
             if w.prune_beta is not None and not w.prune_window:
                 out += [("prune", lambda: p.prune(w.prune_beta, w.prune_alpha)),
-                        ("route_masked", lambda: route(p.alive)), ("counts_masked", p.count)]
+                        ("route_count_masked", lambda: rc(p.alive))]
             gate = p.topk_gate
         else:
             out += [("counts", lambda: L.moe_expert_counts(self.idx, w.E, ws=p.ws_counts,
@@ -258,7 +257,8 @@ class Setup:
             # dx read + written, W_r once, x once (summed into dW_r), dgate/gates/ids, dW_r
             "route_bwd": 2 * T * d * e + E * d * e + T * d * e + 3 * T * k * 4 + E * d * 4,
         }
-        by["route_masked"], by["counts_masked"] = by["route"], by["counts"]
+        by["route_count"] = by["route"] + by["counts"]
+        by["route_count_masked"] = by["route_count"]
         fl = {"ffn_fwd": 6.0 * R * d * f, "ffn_bwd": 12.0 * R * d * f}
         return by, fl
 
@@ -342,9 +342,14 @@ def _supplementary(w, su, dev, reps=20):
     out = {"counts_T_sweep": sweep}
     if w.routed:
         p, x = su.plan, su.xs[0]
+        out["route_us"] = timed(lambda: L.moe_route(x, su.wr, w.k, bias=su.bias, renorm=w.renorm,
+                                                    topk_idx=p.topk_idx, topk_gate=p.topk_gate))
+        out["counts_us"] = timed(p.count)
         out["route_then_counts_us"] = timed(lambda: (
             L.moe_route(x, su.wr, w.k, bias=su.bias, renorm=w.renorm, topk_idx=p.topk_idx,
                         topk_gate=p.topk_gate), p.count()))
+        out["route_count_fused_us"] = timed(lambda: p.route_count(x, su.wr, bias=su.bias,
+                                                                  renorm=w.renorm))
     return out
 
 
@@ -490,8 +495,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-attainable", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
-    ap.add_argument("--profile-target", choices=["ffn_fwd", "ffn_bwd", "copy", "route", "permute",
-                                                 "combine", "counts"])
+    ap.add_argument("--profile-target", choices=["ffn_fwd", "ffn_bwd", "copy", "route_count",
+                                                 "permute", "combine", "counts"])
     ap.add_argument("--summarize-pmc")
     ap.add_argument("--summarize-trace")
     ap.add_argument("--profile-call", default="ffn_fwd")

@@ -124,6 +124,24 @@ int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E,
                       size_t ws_bytes, void* stream);
 
 /*
+ * moe_route_count -- moe_route and moe_expert_counts in one call: the router
+ * kernel also records, per 64-token tile and expert, which tokens chose the
+ * expert, so the counting pass starts at its scan (one kernel and one read
+ * of topk_idx fewer).  Outputs are bit-identical to moe_route followed by
+ * moe_expert_counts on the same arguments.
+ *
+ *   Arguments as in moe_route (x .. topk_gate) and moe_expert_counts
+ *   (counts .. etn_accum).  Workspace: moe_workspace_bytes(LAEP_CALL_COUNTS,
+ *   T, k, E, 0, 0), the counting workspace.
+ */
+int moe_route_count(const void* x, const void* w_router, const float* bias,
+                    const uint8_t* alive, int dtype, int T, int d_model, int E,
+                    int k, int renorm, float* logits, int32_t* topk_idx,
+                    float* topk_gate, int32_t* counts, int32_t* offsets,
+                    int32_t* dest_row, int32_t* row_src, int64_t* etn_accum,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
  * laep_prune_mask -- the LAEP prune decision for one layer and one counted
  * batch (Section 3.2, Eqs. (1) and (2); Algorithm 1, Step 2 with ITER = 1).
  *

@@ -5,6 +5,7 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
 
     moe_route            router scoring + top-k gating
     moe_expert_counts    per-expert token loads (ETN), offsets, dispatch rows
+    moe_route_count      the two above in one call (the router writes the count masks)
     laep_prune_mask      LAEP prune decision (alpha / beta thresholds)
     laep_expert_pruning  Algorithm 1 over a recorded ETN window (per-layer alpha)
     laep_compact_experts, laep_repack_experts   physical removal of pruned experts
@@ -37,6 +38,7 @@ from .api import (  # noqa: F401
     moe_permute_bwd,
     moe_route,
     moe_route_bwd,
+    moe_route_count,
     workspace_bytes,
 )
 from .layer import MoELayerPlan, layer_forward  # noqa: F401

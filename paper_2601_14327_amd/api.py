@@ -127,6 +127,35 @@ def moe_expert_counts(topk_idx: torch.Tensor, E: int, *, want_row_src: bool = Fa
     return out + (row_src,) if want_row_src else out
 
 
+def moe_route_count(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=None, alive=None,
+                    renorm: bool = True, want_logits: bool = False, want_row_src: bool = False,
+                    etn_accum=None, ws=None, topk_idx=None, topk_gate=None, counts=None,
+                    offsets=None, dest_row=None, row_src=None):
+    """Routing and expert counts in one call.  Returns (topk_idx, topk_gate,
+    counts, offsets, dest_row, row_src or None, logits or None)."""
+    _dev(x, "x"), _dev(w_router, "w_router")
+    T, d = x.shape
+    E = w_router.shape[0]
+    dev = x.device
+    i32 = torch.int32
+    topk_idx = torch.empty((T, k), dtype=i32, device=dev) if topk_idx is None else topk_idx
+    topk_gate = (torch.empty((T, k), dtype=torch.float32, device=dev) if topk_gate is None
+                 else topk_gate)
+    counts = torch.empty(E, dtype=i32, device=dev) if counts is None else counts
+    offsets = torch.empty(E + 1, dtype=i32, device=dev) if offsets is None else offsets
+    dest_row = torch.empty(T * k, dtype=i32, device=dev) if dest_row is None else dest_row
+    if want_row_src and row_src is None:
+        row_src = torch.empty(T * k, dtype=i32, device=dev)
+    logits = torch.empty((T, E), dtype=torch.float32, device=dev) if want_logits else None
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_COUNTS, T, k, E), dev)
+    check(lib().moe_route_count(_ptr(x), _ptr(w_router), _ptr(bias), _ptr(alive), _dtype_code(x),
+                                T, d, E, k, int(renorm), _ptr(logits), _ptr(topk_idx),
+                                _ptr(topk_gate), _ptr(counts), _ptr(offsets), _ptr(dest_row),
+                                _ptr(row_src), _ptr(etn_accum), _ptr(ws), ws.numel(),
+                                _stream(dev)))
+    return topk_idx, topk_gate, counts, offsets, dest_row, row_src, logits
+
+
 def laep_prune_mask(counts: torch.Tensor, total: int, alpha: float = math.inf,
                     beta: float = 0.0, *, alive=None, n_pruned=None):
     """LAEP prune decision.  Returns (alive [E] uint8, n_pruned [1] int32)."""

@@ -129,7 +129,7 @@ int moe_route(const void* x, const void* w_router, const float* bias, const uint
   REQUIRE(aligned16(x) && aligned16(w_router), LAEP_ERR_INVALID_ARG,
           "moe_route: x and w_router must be 16-byte aligned");
   return hip_status(laep::launch_route(x, w_router, bias, alive, dtype, T, d_model, E, k,
-                                       renorm != 0, logits, topk_idx, topk_gate,
+                                       renorm != 0, logits, topk_idx, topk_gate, nullptr,
                                        as_stream(stream)),
                     "moe_route");
 }
@@ -152,6 +152,37 @@ int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E, int32_t* cou
   return hip_status(laep::launch_counts(topk_idx, T, k, E, counts, offsets, dest_row, row_src,
                                         etn_accum, ws, as_stream(stream)),
                     "moe_expert_counts");
+}
+
+int moe_route_count(const void* x, const void* w_router, const float* bias, const uint8_t* alive,
+                    int dtype, int T, int d_model, int E, int k, int renorm, float* logits,
+                    int32_t* topk_idx, float* topk_gate, int32_t* counts, int32_t* offsets,
+                    int32_t* dest_row, int32_t* row_src, int64_t* etn_accum, void* ws,
+                    size_t ws_bytes, void* stream) {
+  int rc = check_dtype(dtype);
+  if (rc) return rc;
+  if ((rc = check_experts(E, k))) return rc;
+  if ((rc = check_rows(T, k, d_model))) return rc;
+  REQUIRE(counts && offsets, LAEP_ERR_INVALID_ARG,
+          "moe_route_count: counts and offsets must be non-null");
+  if (T > 0) {
+    REQUIRE(x && w_router && topk_idx && topk_gate && dest_row, LAEP_ERR_INVALID_ARG,
+            "moe_route_count: x, w_router, topk_idx, topk_gate and dest_row must be non-null");
+    REQUIRE(aligned16(x) && aligned16(w_router), LAEP_ERR_INVALID_ARG,
+            "moe_route_count: x and w_router must be 16-byte aligned");
+  }
+  const size_t need = laep::counts_ws_bytes(T, k, E);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_route_count: workspace %zu < %zu bytes",
+          ws_bytes, need);
+  REQUIRE(need == 0 || ws, LAEP_ERR_INVALID_ARG, "moe_route_count: ws must be non-null");
+  const hipStream_t s = as_stream(stream);
+  hipError_t e = laep::launch_route(x, w_router, bias, alive, dtype, T, d_model, E, k,
+                                    renorm != 0, logits, topk_idx, topk_gate,
+                                    T > 0 ? laep::counts_masks(ws) : nullptr, s);
+  if (e == hipSuccess)
+    e = laep::launch_counts(topk_idx, T, k, E, counts, offsets, dest_row, row_src, etn_accum, ws,
+                            s, /*masks_ready=*/true);
+  return hip_status(e, "moe_route_count");
 }
 
 int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha, double beta,

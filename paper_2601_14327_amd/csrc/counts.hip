@@ -8,6 +8,8 @@
 //     base[w][e] = offsets[e] + sum_{w' < w} popc(masks[w'][e]).
 //  3. scatter: dest_row[t*k + j] = base[w][e] + popc(masks[w][e] & lanes < t),
 //     i.e. rows grouped by expert, ordered by token inside a group.
+// The router can write the masks itself (moe_route_count); the counting pass
+// then starts at the scan.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -127,9 +129,11 @@ size_t counts_ws_bytes(int T, int k, int E) {
   return align_up(n_wt * E * sizeof(uint64_t), 256) + align_up(n_wt * E * sizeof(int32_t), 256);
 }
 
+uint32_t* counts_masks(void* ws) { return static_cast<uint32_t*>(ws); }
+
 hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* counts,
                          int32_t* offsets, int32_t* dest_row, int32_t* row_src, int64_t* etn,
-                         void* ws, hipStream_t s) {
+                         void* ws, hipStream_t s, bool masks_ready) {
   const int n_wt = (T + 63) / 64;
   uint64_t* masks = static_cast<uint64_t*>(ws);
   int32_t* base = reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
@@ -138,7 +142,7 @@ hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* count
   while (E_pad < E) E_pad <<= 1;
   const int wt_per_block = kCountThreads / 64;
   const int blocks = (n_wt + wt_per_block - 1) / wt_per_block;
-  if (n_wt > 0)
+  if (n_wt > 0 && !masks_ready)
     hipLaunchKernelGGL(count_masks_kernel, dim3(blocks), dim3(kCountThreads), 0, s, idx, T, k, E,
                        n_wt, masks);
   hipLaunchKernelGGL(count_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, masks, n_wt, E, E_pad,

@@ -16,12 +16,15 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 hipError_t launch_route(const void* x, const void* w, const float* bias, const uint8_t* alive,
                         int dtype, int T, int d, int E, int k, int renorm, float* logits,
-                        int32_t* idx, float* gate, hipStream_t s);
+                        int32_t* idx, float* gate, uint32_t* masks32, hipStream_t s);
 
 size_t counts_ws_bytes(int T, int k, int E);
+// masks_ready: the router already wrote the expert masks into ws
 hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* counts,
                          int32_t* offsets, int32_t* dest_row, int32_t* row_src, int64_t* etn,
-                         void* ws, hipStream_t s);
+                         void* ws, hipStream_t s, bool masks_ready = false);
+// the expert-mask area of the counting workspace (uint64 [ceil(T/64)][E])
+uint32_t* counts_masks(void* ws);
 
 hipError_t launch_prune(const int32_t* counts, int E, int64_t total, double alpha, double beta,
                         uint8_t* alive, int32_t* n_pruned, hipStream_t s);

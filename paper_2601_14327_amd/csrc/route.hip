@@ -16,6 +16,9 @@
 //     descending logit, ties to the lower expert index.
 //  3. gates: exp(l_j - l_max) divided by the sum over the selected k
 //     (renorm) or over all alive experts.
+//  4. optionally (moe_route_count), the expert masks of the counting pass:
+//     for each expert, the 32-bit set of this workgroup's tokens that chose
+//     it, written as its half of the 64-token wave tile's mask.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -130,7 +133,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     const T* __restrict__ x, const T* __restrict__ w, const float* __restrict__ bias,
     const uint8_t* __restrict__ alive, int n_tok, int d, int E, int k, int renorm,
     float* __restrict__ logits_out, int32_t* __restrict__ idx_out,
-    float* __restrict__ gate_out) {
+    float* __restrict__ gate_out, uint32_t* __restrict__ masks32) {
   constexpr int EP = 32 * NB;        // experts padded to 32
   constexpr int LD = EP + 1;         // LDS row stride (floats)
   constexpr int EPL = EP / 16;       // experts owned per top-k lane
@@ -139,6 +142,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   __shared__ __attribute__((aligned(1024))) char s_stage[StageBytes<NB, KC>::value];
   __shared__ float s_bias[EP];
   __shared__ uint8_t s_alive[EP];
+  __shared__ uint32_t s_mask[EP];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -148,6 +152,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   for (int e = tid; e < EP; e += kRouteThreads) {
     s_bias[e] = (bias != nullptr && e < E) ? bias[e] : 0.0f;
     s_alive[e] = (e < E) ? (alive == nullptr ? 1 : (alive[e] != 0)) : 0;
+    s_mask[e] = 0u;
   }
 
   // ---- 1. router GEMM -----------------------------------------------------
@@ -375,9 +380,22 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     if (g == 0) {
       s_ex[ti * k + j] = ex;
       if (write_ok) idx_out[(size_t)t_glob * k + j] = found ? be : -1;
+      if (masks32 != nullptr && write_ok && found) atomicOr(&s_mask[be], 1u << ti);
     }
   }
   __syncthreads();
+  if (masks32 != nullptr) {
+    // mask word of (wave tile blockIdx/2, expert e): tokens 0-31 of the tile
+    // in the low word, 32-63 in the high word; a last even workgroup also
+    // clears the high word (no tokens there)
+    const size_t wt = blockIdx.x >> 1;
+    const int half = blockIdx.x & 1;
+    const bool clear_hi = half == 0 && blockIdx.x == gridDim.x - 1;
+    for (int e = tid; e < E; e += kRouteThreads) {
+      masks32[2 * (wt * E + e) + half] = s_mask[e];
+      if (clear_hi) masks32[2 * (wt * E + e) + 1] = 0u;
+    }
+  }
   const float denom = renorm ? s_sel : s_all;
   const float inv_ok = (denom > 0.0f) ? 1.0f : 0.0f;
   if (write_ok) {
@@ -391,16 +409,16 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
 template <typename T, int NB, int KC>
 void launch_route_nb(dim3 grid, hipStream_t s, const void* x, const void* w, const float* bias,
                      const uint8_t* alive, int T_, int d, int E, int k, int renorm, float* logits,
-                     int32_t* idx, float* gate) {
+                     int32_t* idx, float* gate, uint32_t* masks32) {
   hipLaunchKernelGGL((route_kernel<T, NB, KC>), grid, dim3(kRouteThreads), 0, s,
                      static_cast<const T*>(x), static_cast<const T*>(w), bias, alive, T_, d, E, k,
-                     renorm, logits, idx, gate);
+                     renorm, logits, idx, gate, masks32);
 }
 
 template <typename T>
 hipError_t launch_route_t(const void* x, const void* w, const float* bias, const uint8_t* alive,
                           int T_, int d, int E, int k, int renorm, float* logits, int32_t* idx,
-                          float* gate, hipStream_t s) {
+                          float* gate, uint32_t* masks32, hipStream_t s) {
   const int nb = (E + 31) / 32;
   const dim3 grid((T_ + kRouteTokens - 1) / kRouteTokens);
   // bf16 with up to 128 experts: LDS-staged chunks of 256 (NB <= 2) or 128 columns
@@ -409,7 +427,7 @@ hipError_t launch_route_t(const void* x, const void* w, const float* bias, const
     if (nb <= 2 && d % 256 == 0) kc = 256;
     else if (d % 128 == 0) kc = 128;
   }
-#define LAEP_ROUTE_ARGS grid, s, x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate
+#define LAEP_ROUTE_ARGS grid, s, x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate, masks32
   if constexpr (sizeof(T) == 2) {
     if (kc == 256) {
       if (nb == 1) launch_route_nb<T, 1, 256>(LAEP_ROUTE_ARGS);
@@ -445,11 +463,13 @@ hipError_t launch_route_t(const void* x, const void* w, const float* bias, const
 
 hipError_t launch_route(const void* x, const void* w, const float* bias, const uint8_t* alive,
                         int dtype, int T_, int d, int E, int k, int renorm, float* logits,
-                        int32_t* idx, float* gate, hipStream_t s) {
+                        int32_t* idx, float* gate, uint32_t* masks32, hipStream_t s) {
   if (T_ == 0) return hipSuccess;
   if (dtype == kDtypeBf16)
-    return launch_route_t<bf16_t>(x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate, s);
-  return launch_route_t<float>(x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate, s);
+    return launch_route_t<bf16_t>(x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate,
+                                  masks32, s);
+  return launch_route_t<float>(x, w, bias, alive, T_, d, E, k, renorm, logits, idx, gate, masks32,
+                               s);
 }
 
 }  // namespace laep

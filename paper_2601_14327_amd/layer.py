@@ -93,6 +93,13 @@ class MoELayerPlan:
                               offsets=self.offsets, dest_row=self.dest_row,
                               row_src=self.row_src, etn_accum=etn_accum)
 
+    def route_count(self, x, w_router, bias=None, alive=None, renorm=True, etn_accum=None):
+        """route + count in one call (the router also writes the count masks)."""
+        api.moe_route_count(x, w_router, self.k, bias=bias, alive=alive, renorm=renorm,
+                            etn_accum=etn_accum, ws=self.ws_counts, topk_idx=self.topk_idx,
+                            topk_gate=self.topk_gate, counts=self.counts, offsets=self.offsets,
+                            dest_row=self.dest_row, row_src=self.row_src)
+
     def prune(self, beta: float, alpha: float = math.inf):
         api.laep_prune_mask(self.counts, self.T * self.k, alpha, beta, alive=self.alive,
                             n_pruned=self.n_pruned)
@@ -115,12 +122,10 @@ class MoELayerPlan:
     # -- whole passes ----------------------------------------------------------
     def forward(self, x, w_router, w_gate_up, w_down, bias=None, renorm=True,
                 prune_beta: Optional[float] = None, prune_alpha: float = math.inf):
-        self.route(x, w_router, bias=bias, renorm=renorm)
-        self.count()
+        self.route_count(x, w_router, bias=bias, renorm=renorm)
         if prune_beta is not None:
             self.prune(prune_beta, prune_alpha)
-            self.route(x, w_router, bias=bias, alive=self.alive, renorm=renorm)
-            self.count()
+            self.route_count(x, w_router, bias=bias, alive=self.alive, renorm=renorm)
         return self.experts_and_combine(x, w_gate_up, w_down)
 
     def forward_given_routing(self, x, topk_idx, topk_gate, w_gate_up, w_down):

@@ -75,6 +75,57 @@ def test_route_with_alive_mask_and_too_few_alive():
     np.testing.assert_allclose(gate[:, :2].sum(1), 1.0, rtol=1e-6)
 
 
+@pytest.mark.parametrize("T,d,E,k,dtype,renorm,dead", [
+    (8192, 2048, 64, 8, "bf16", True, False),   # LDS-staged router, whole tiles
+    (100, 256, 64, 8, "bf16", True, True),      # ragged: 4 workgroups, last tile half empty
+    (33, 128, 16, 4, "bf16", False, False),     # odd number of workgroups
+    (1, 64, 8, 2, "f32", True, False),
+    (300, 384, 200, 6, "bf16", True, True),     # register path (7 expert blocks)
+    (257, 96, 40, 5, "f32", False, True),
+])
+def test_route_count_matches_route_then_counts(T, d, E, k, dtype, renorm, dead):
+    """moe_route_count is bit-identical to moe_route followed by moe_expert_counts."""
+    c = random_case(T + 3 * E, T=T, d_model=d, E=E, k=k, d_ff=64, dtype=dtype, bias_std=1.0,
+                    weight_std=0.05)
+    td = TD[dtype]
+    x, w = dev(c["x"], td), dev(c["w_router"], td)
+    bias = dev(c["bias"], torch.float32)
+    alive = None
+    if dead:
+        a = np.ones(E, np.uint8)
+        a[np.random.default_rng(E).choice(E, E // 4, replace=False)] = 0
+        alive = dev(a, torch.uint8)
+    case(f"route_count T={T} d={d} E={E} k={k} {dtype} renorm={renorm} dead={dead}")
+    idx, gate, logits = laep.moe_route(x, w, k, bias=bias, alive=alive, renorm=renorm,
+                                       want_logits=True)
+    etn1 = torch.full((E,), 3, dtype=torch.int64, device="cuda")
+    counts, offsets, dest, row_src = laep.moe_expert_counts(idx, E, want_row_src=True,
+                                                           etn_accum=etn1)
+    etn2 = torch.full((E,), 3, dtype=torch.int64, device="cuda")
+    f = laep.moe_route_count(x, w, k, bias=bias, alive=alive, renorm=renorm, want_logits=True,
+                             want_row_src=True, etn_accum=etn2)
+    torch.cuda.synchronize()
+    for got, ref, name in zip(f, (idx, gate, counts, offsets, dest, row_src, logits),
+                              ("idx", "gate", "counts", "offsets", "dest_row", "row_src",
+                               "logits")):
+        assert torch.equal(got, ref), name
+    assert torch.equal(etn1, etn2)
+    rc, ro, rd = om.expert_counts(host(idx), E)
+    np.testing.assert_array_equal(host(f[2]), rc)
+    np.testing.assert_array_equal(host(f[4]), rd)
+
+
+def test_route_count_empty_and_validation():
+    x = torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda")
+    w = dev(np.ones((8, 64), np.float32), torch.bfloat16)
+    case("route_count T=0")
+    idx, gate, counts, offsets, dest, _, _ = laep.moe_route_count(x, w, 2)
+    torch.cuda.synchronize()
+    assert host(counts).tolist() == [0] * 8 and host(offsets).tolist() == [0] * 9
+    with pytest.raises(laep.LaepError):
+        laep.moe_route_count(dev(np.ones((4, 64), np.float32), torch.bfloat16), w, 9)
+
+
 # ---------------------------------------------------------------------------
 # counts / offsets / dispatch permutation
 # ---------------------------------------------------------------------------
