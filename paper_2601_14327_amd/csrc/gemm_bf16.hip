@@ -94,17 +94,25 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
   const int lrow = lane & 31;
   const int lcol = (lane >> 5) * 4;
   // staged [BM][BN] bf16 -> global rows: staged columns [scol0, scol0 + ncols)
-  // go to dst + row * ld (rows < te.rows only)
-  auto flush = [&](bf16_t* dst, long long ld, int ncols, int scol0) {
-    const int chunks_per_row = ncols / 8;
-    const int total = BM * chunks_per_row;
-    for (int c = tid; c < total; c += NT) {
-      const int r = c / chunks_per_row, cc = c % chunks_per_row;
-      if (r < te.rows) {
-        const u32x4_t v =
-            *reinterpret_cast<const u32x4_t*>(smem + r * PITCH + (scol0 + cc * 8) * 2);
-        *reinterpret_cast<u32x4_t*>(dst + (te.row0 + r) * ld + cc * 8) = v;
-      }
+  // go to dst + row * ld (rows < te.rows only).  NCMAX (>= ncols) fixes the
+  // trip count, so all of a thread's LDS reads are issued before one wait.
+  auto flush = [&](auto ncmax_tag, bf16_t* dst, long long ld, int ncols, int scol0) {
+    constexpr int CPR = decltype(ncmax_tag)::value / 8;
+    constexpr int ITERS = BM * CPR / NT;
+    static_assert(BM * CPR % NT == 0, "flush chunks must divide over the threads");
+    u32x4_t v[ITERS];
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      const int r = c / CPR, cc = c % CPR;
+      v[it] = *reinterpret_cast<const u32x4_t*>(smem + r * PITCH + (scol0 + cc * 8) * 2);
+    }
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      const int r = c / CPR, cc = c % CPR;
+      if (r < te.rows && cc * 8 < ncols)
+        *reinterpret_cast<u32x4_t*>(dst + (te.row0 + r) * ld + cc * 8) = v[it];
     }
   };
   auto stage = [&](int row, int col, float a, float b, float c, float d) {
@@ -135,8 +143,8 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
       }
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
-      flush(p.out2 + fbase, 2LL * f, fcols, 0);
-      flush(p.out2 + f + fbase, 2LL * f, fcols, BN / 2);
+      flush(std::integral_constant<int, BN / 2>{}, p.out2 + fbase, 2LL * f, fcols, 0);
+      flush(std::integral_constant<int, BN / 2>{}, p.out2 + f + fbase, 2LL * f, fcols, BN / 2);
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
     }
@@ -159,7 +167,7 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
     }
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
-    flush(p.out + fbase, f, fcols, 0);
+    flush(std::integral_constant<int, BN / 2>{}, p.out + fbase, f, fcols, 0);
   } else {
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -173,7 +181,7 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
     }
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
-    flush(p.out + nt * BN, p.ldo, min(BN, p.N - nt * BN), 0);
+    flush(std::integral_constant<int, BN>{}, p.out + nt * BN, p.ldo, min(BN, p.N - nt * BN), 0);
   }
 }
 

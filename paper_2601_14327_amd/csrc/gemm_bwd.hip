@@ -332,15 +332,24 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       }
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
+      // fixed trip count (BN columns): every LDS read of a thread before one wait
+      constexpr int CPR = BN / 4, ITERS = 128 * CPR / NT;
       const int cpr = ncols / 4;
-      for (int c = tid; c < 128 * cpr; c += NT) {
-        const int r = c / cpr, cc = c % cpr;
+      f32x4_t v[ITERS];
+#pragma unroll
+      for (int it = 0; it < ITERS; ++it) {
+        const int c = it * NT + tid;
+        v[it] = *reinterpret_cast<const f32x4_t*>(smem + (c / CPR) * PITCH32 + (c % CPR) * 16);
+      }
+#pragma unroll
+      for (int it = 0; it < ITERS; ++it) {
+        const int c = it * NT + tid;
+        const int r = c / CPR, cc = c % CPR;
         const int row = mt * BM + pass * 128 + r;
-        if (row < p.Mw) {
-          f32x4_t v = *reinterpret_cast<const f32x4_t*>(smem + r * PITCH32 + cc * 16);
+        if (row < p.Mw && cc < cpr) {
           f32x4_t* dst = reinterpret_cast<f32x4_t*>(W + (long long)row * p.N + nt * BN + cc * 4);
-          if (p.accumulate) v += *dst;
-          *dst = v;
+          if (p.accumulate) v[it] += *dst;
+          *dst = v[it];
         }
       }
       wait_lgkm0();
@@ -359,12 +368,28 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     for (int pass = 0; pass < 4; ++pass) {
       const int prow0 = pass * 64;
       const int prows = min(64, te.rows - prow0);
-      for (int c = tid; c < 64 * cpr; c += NT) {  // stage A_g and A_u
-        const int r = c / cpr, cc = c % cpr;
-        if (r < prows) {
-          const bf16_t* src = p.aux + (long long)(te.row0 + prow0 + r) * 2 * f + nt * BN + cc * 8;
-          *reinterpret_cast<u32x4_t*>(G + r * PITCH16 + cc * 16) = *reinterpret_cast<const u32x4_t*>(src);
-          *reinterpret_cast<u32x4_t*>(U + r * PITCH16 + cc * 16) = *reinterpret_cast<const u32x4_t*>(src + f);
+      // stage A_g and A_u: every load of a thread issued before the first wait
+      constexpr int CPR = BN / 8, ITERS = 64 * CPR / NT;
+      {
+        u32x4_t g[ITERS], u[ITERS];
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          const int r = c / CPR, cc = c % CPR;
+          if (r < prows && cc < cpr) {
+            const bf16_t* src = p.aux + (long long)(te.row0 + prow0 + r) * 2 * f + nt * BN + cc * 8;
+            g[it] = *reinterpret_cast<const u32x4_t*>(src);
+            u[it] = *reinterpret_cast<const u32x4_t*>(src + f);
+          }
+        }
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          const int r = c / CPR, cc = c % CPR;
+          if (r < prows && cc < cpr) {
+            *reinterpret_cast<u32x4_t*>(G + r * PITCH16 + cc * 16) = g[it];
+            *reinterpret_cast<u32x4_t*>(U + r * PITCH16 + cc * 16) = u[it];
+          }
         }
       }
       wait_lgkm0();
@@ -404,15 +429,27 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       }
       wait_lgkm0();
       __syncthreads();
-      for (int c = tid; c < 64 * cpr; c += NT) {  // dA (gate and up halves) and H_b
-        const int r = c / cpr, cc = c % cpr;
-        if (r < prows) {
-          const long long row = te.row0 + prow0 + r;
-          bf16_t* dst = p.out + row * 2 * f + nt * BN + cc * 8;
-          *reinterpret_cast<u32x4_t*>(dst) = *reinterpret_cast<const u32x4_t*>(G + r * PITCH16 + cc * 16);
-          *reinterpret_cast<u32x4_t*>(dst + f) = *reinterpret_cast<const u32x4_t*>(U + r * PITCH16 + cc * 16);
-          *reinterpret_cast<u32x4_t*>(p.out2 + row * f + nt * BN + cc * 8) =
-              *reinterpret_cast<const u32x4_t*>(Hs + r * PITCH16 + cc * 16);
+      {  // dA (gate and up halves) and H_b: LDS reads first, then the stores
+        u32x4_t g[ITERS], u[ITERS], h[ITERS];
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          const int r = c / CPR, cc = c % CPR;
+          g[it] = *reinterpret_cast<const u32x4_t*>(G + r * PITCH16 + cc * 16);
+          u[it] = *reinterpret_cast<const u32x4_t*>(U + r * PITCH16 + cc * 16);
+          h[it] = *reinterpret_cast<const u32x4_t*>(Hs + r * PITCH16 + cc * 16);
+        }
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          const int r = c / CPR, cc = c % CPR;
+          if (r < prows && cc < cpr) {
+            const long long row = te.row0 + prow0 + r;
+            bf16_t* dst = p.out + row * 2 * f + nt * BN + cc * 8;
+            *reinterpret_cast<u32x4_t*>(dst) = g[it];
+            *reinterpret_cast<u32x4_t*>(dst + f) = u[it];
+            *reinterpret_cast<u32x4_t*>(p.out2 + row * f + nt * BN + cc * 8) = h[it];
+          }
         }
       }
       wait_lgkm0();
@@ -436,11 +473,20 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     __syncthreads();
     const int ncols = min(BN, p.N - nt * BN);
     const int cpr = ncols / 8;
-    for (int c = tid; c < BM * cpr; c += NT) {
-      const int r = c / cpr, cc = c % cpr;
-      if (r < te.rows) {
+    constexpr int CPR = BN / 8, ITERS = BM * CPR / NT;
+    u32x4_t v[ITERS];
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      v[it] = *reinterpret_cast<const u32x4_t*>(smem + (c / CPR) * PITCH16 + (c % CPR) * 16);
+    }
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      const int r = c / CPR, cc = c % CPR;
+      if (r < te.rows && cc < cpr) {
         bf16_t* dst = p.out + (long long)(te.row0 + r) * p.ldo + nt * BN + cc * 8;
-        *reinterpret_cast<u32x4_t*>(dst) = *reinterpret_cast<const u32x4_t*>(smem + r * PITCH16 + cc * 16);
+        *reinterpret_cast<u32x4_t*>(dst) = v[it];
       }
     }
   }
