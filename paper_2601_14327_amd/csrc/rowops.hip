@@ -5,6 +5,9 @@
 //   moe_combine_bwd  dgate[t, j] = <dout[t], y[row]>, dy[row] = g[t, j] * dout[t]
 // All are HBM-bound.  Rows move as 16-byte vectors; consecutive threads own
 // consecutive vectors of a row, so every wave access is one contiguous run.
+// Rows read once go through streaming (non-temporal) loads, and x_perm
+// through streaming stores; outputs the next call reads (out, dx, dy) keep
+// ordinary stores, so they stay in the caches for it.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -28,10 +31,10 @@ __global__ __launch_bounds__(kRowThreads) void permute_kernel(
     const int t = t_lo + i / vec_per_row;
     const int v = i % vec_per_row;
     if (t >= n_tok) break;
-    const u32x4_t val = x[(size_t)t * vec_per_row + v];
+    const u32x4_t val = ld_stream(x + (size_t)t * vec_per_row + v);
     for (int j = 0; j < k; ++j) {
       const int r = dest_row[(size_t)t * k + j];
-      if (r >= 0) x_perm[(size_t)r * vec_per_row + v] = val;
+      if (r >= 0) st_stream(x_perm + (size_t)r * vec_per_row + v, val);
     }
   }
 }
@@ -43,7 +46,7 @@ template <> struct RawRow<bf16_t> {
   typedef u32x4_t type;
   __device__ static __forceinline__ type load(const bf16_t* p, bool ok) {
     type v = {0u, 0u, 0u, 0u};
-    if (ok) v = *reinterpret_cast<const u32x4_t*>(p);
+    if (ok) v = ld_stream(reinterpret_cast<const u32x4_t*>(p));
     return v;
   }
   __device__ static __forceinline__ void fma8(float acc[8], float g, const type& v) {
@@ -61,8 +64,8 @@ template <> struct RawRow<float> {
     v.a = f32x4_t{0.f, 0.f, 0.f, 0.f};
     v.b = v.a;
     if (ok) {
-      v.a = *reinterpret_cast<const f32x4_t*>(p);
-      v.b = *reinterpret_cast<const f32x4_t*>(p + 4);
+      v.a = ld_stream(reinterpret_cast<const f32x4_t*>(p));
+      v.b = ld_stream(reinterpret_cast<const f32x4_t*>(p + 4));
     }
     return v;
   }
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
     for (int v = threadIdx.x; v < vec_per_row; v += kRowThreads) {
       float dv[8], yv[8], o[8];
       Elem<T>::load8(drow + (size_t)v * 8, dv);
-      Elem<T>::load8(y + (size_t)r * d + (size_t)v * 8, yv);
+      Elem<T>::load8_stream(y + (size_t)r * d + (size_t)v * 8, yv);
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         part += dv[q] * yv[q];
