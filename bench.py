@@ -23,7 +23,9 @@ Prints ONE JSON line:
   attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
   supplementary  moe_expert_counts at T x {1, 8, 64} tokens; route, counts, the
                two back to back, and the fused moe_route_count, each timed alone
-  cpu_baseline the float64 CPU oracle timed on a bounded token sample
+  cpu_baseline the float64 CPU oracle timed on a bounded token sample (all BLAS
+               threads, and one thread on a smaller sample)
+  warm         the step with the same input set every step
 
 Other workloads: skewed, skewed_mild (routed, pruned every step), shard (16
 experts, given Zipf routing), shard_bwd (shard forward + backward),
@@ -109,10 +111,20 @@ def _cpu_baseline(w, c, budget_s: float, keep=None):
             break
         n = int(min(w.T, max(2 * n, n * (budget_s * 0.6) / max(dt, 1e-3))))
         dt = run(n)
+    # the same oracle with its BLAS held to one thread, on a smaller sample
+    n1 = max(16, min(n, int(n * (budget_s * 0.25) / max(dt * threads, 1e-3))))
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            dt1 = run(n1)
+        one = {"value": n1 / dt1, "sample": f"{n1} {'tokens' if w.routed else 'rows'} ({dt1:.1f} s)"}
+    except Exception as e:  # pragma: no cover
+        one = {"error": str(e)}
     unit = "tokens/s" if w.routed else "rows/s"
     return {"value": n / dt, "unit": unit, "cores": threads, "kind": "oracle",
             "sample": f"{n} of {w.T} {'tokens' if w.routed else 'rows'} of the same workload, "
-                      f"layer forward in float64 NumPy ({dt:.1f} s)"}
+                      f"layer forward in float64 NumPy ({dt:.1f} s)",
+            "one_thread": one}
 
 
 # ---------------------------------------------------------------------------------------
@@ -542,6 +554,18 @@ def main():
     wall = time.perf_counter() - t0
     ms = wall * 1e3 / args.steps
 
+    # warm: the same input set every step (x can stay in the caches between
+    # steps); reported beside the primary, rotating-input number
+    for _, fn in su.calls(0):
+        fn()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(args.steps):
+        for _, fn in su.calls(0):
+            fn()
+    torch.cuda.synchronize()
+    warm_ms = (time.perf_counter() - t1) * 1e3 / args.steps
+
     by, fl = su.algorithmic()
     breakdown = {}
     for j, n in enumerate(names):
@@ -596,6 +620,8 @@ def main():
                      "algorithmic_flops_per_call": fl[dom], "mean_call_us": dom_us},
         "cpu_baseline": cpu,
         "attainable": attain,
+        "warm": {"ms_per_step": warm_ms, "value": w.T / (warm_ms * 1e-3),
+                 "note": "same input set every step"},
         "pruning": su.pruning,
         "supplementary": supp,
         "breakdown": breakdown,
