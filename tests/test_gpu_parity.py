@@ -148,6 +148,28 @@ def test_counts_bit_exact(T, E, k):
     np.testing.assert_array_equal(host(etn), rc + 5)
 
 
+@pytest.mark.parametrize("T,E,k", [(32769, 64, 8), (40000, 5, 2), (131072, 256, 4),
+                                   (70000, 16, 1)])
+def test_counts_two_level_scan(T, E, k):
+    """More than 512 wave tiles: the counting pass scans in two levels (block
+    partials, one workgroup over the blocks, then the tile bases)."""
+    rng = np.random.default_rng(T + 3 * E)
+    idx = np.argsort(rng.random((T, E)), axis=1)[:, :k].astype(np.int32)
+    idx[rng.random(T) < 0.01, -1] = -1          # a few unrouted slots
+    case(f"counts two-level T={T} E={E} k={k}")
+    etn = torch.full((E,), 7, dtype=torch.int64, device="cuda")
+    counts, offsets, dest, row_src = laep.moe_expert_counts(
+        dev(idx, torch.int32), E, want_row_src=True, etn_accum=etn)
+    torch.cuda.synchronize()
+    rc, ro, rd = om.expert_counts(idx, E)
+    np.testing.assert_array_equal(host(counts), rc)
+    np.testing.assert_array_equal(host(offsets), ro)
+    np.testing.assert_array_equal(host(dest), rd)
+    routed = rd >= 0
+    np.testing.assert_array_equal(host(row_src)[rd[routed]], np.nonzero(routed)[0])
+    np.testing.assert_array_equal(host(etn), rc + 7)
+
+
 def test_counts_skew_unrouted_and_empty_experts():
     rng = np.random.default_rng(3)
     T, E, k = 3000, 32, 4
