@@ -413,6 +413,60 @@ def test_tiny_layer_end_to_end():
     assert rownorm_err(host(out)[ok], ref["out"][ok]) <= TOL_F32
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_layer_fuzz(seed):
+    """Random shapes through the whole forward (route + counts, dispatch, FFN,
+    combine): routing against the oracle (near-ties allowed), outputs
+    teacher-forced on the GPU's routing.  Every fourth case keeps exactly k
+    experts alive, every fourth (offset 2) lets one expert take every token."""
+    rng = np.random.default_rng(900 + seed)
+    E = int(rng.integers(1, 65))
+    k = int(rng.integers(1, min(E, 8) + 1))
+    T = int(rng.integers(1, 700))
+    d = int(rng.choice([64, 128, 192, 256]))
+    f = int(rng.choice([64, 128, 192]))
+    dtype = "f32" if seed % 3 == 0 else "bf16"
+    renorm = bool(seed % 2)
+    td = TD[dtype]
+    c = random_case(5000 + seed, T=T, d_model=d, E=E, k=k, d_ff=f, dtype=dtype,
+                    bias_std=float(rng.choice([0.0, 1.0, 3.0])), weight_std=0.05)
+    bias = c["bias"].copy() if "bias" in c else np.zeros(E, np.float32)
+    alive = None
+    if seed % 4 == 1 and E > k:        # every expert pruned except k
+        alive = np.zeros(E, bool)
+        alive[rng.choice(E, k, replace=False)] = True
+    if seed % 4 == 2:                  # one expert takes every token
+        bias[int(rng.integers(E))] += 100.0
+    case(f"layer fuzz seed={seed} T={T} d={d} E={E} k={k} f={f} {dtype} renorm={renorm}")
+    x = dev(c["x"], td)
+    idx, gate, counts, offsets, dest, row_src, logits = laep.moe_route_count(
+        x, dev(c["w_router"], td), k, bias=dev(bias, torch.float32),
+        alive=None if alive is None else dev(alive.astype(np.uint8), torch.uint8),
+        renorm=renorm, want_logits=True, want_row_src=True)
+    wgu, wd = dev(c["w_gate_up"], td), dev(c["w_down"], td)
+    xp = laep.moe_permute(x, dest, k)
+    y, _ = laep.moe_grouped_ffn_fwd(xp, wgu, wd, offsets, save_act=False)
+    out = laep.moe_combine(y, gate, dest)
+    if dtype == "bf16":   # the dispatch folded into the operand loads gives the same bits
+        yg, _ = laep.moe_grouped_ffn_fwd_gather(x, row_src, k, wgu, wd, offsets, rows=T * k)
+    torch.cuda.synchronize()
+    ridx, rgate, _, rlog = om.route(c["x"], c["w_router"], k, bias=bias, alive=alive,
+                                   renorm=renorm)
+    check_routing(host(idx), host(gate), ridx, rgate, rlog, k, alive)
+    gi, gg = host(idx), host(gate)
+    rc, ro, rd = om.expert_counts(gi, E)
+    np.testing.assert_array_equal(host(counts), rc)
+    np.testing.assert_array_equal(host(dest), rd)
+    ry, _ = om.grouped_ffn_fwd(om.permute(c["x"], rd, k), c["w_gate_up"], c["w_down"], ro,
+                               dtype=dtype)
+    rout = om.combine(ry, gg, rd, k, dtype=dtype)
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    assert rownorm_err(host(y), ry) <= tol
+    assert rownorm_err(host(out), rout) <= tol
+    if dtype == "bf16":
+        assert torch.equal(yg, y)
+
+
 def test_determinism():
     w = WORKLOADS["balanced"]
     c = random_case(11, T=1500, d_model=512, E=64, k=8, d_ff=256, dtype="bf16")
