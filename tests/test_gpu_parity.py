@@ -393,6 +393,43 @@ def test_ffn_bwd_parity(counts, d, f):
     assert rownorm_err(host(dwd).reshape(E, -1), (2 * rd).reshape(E, -1)) <= TOL_F32
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_ffn_bwd_fuzz(seed):
+    """Random ragged expert loads (empty experts, single rows, one heavy
+    expert) through the backward products, teacher-forced like the parity
+    test above: dA, H_b and dX against the oracle at the GPU's act_save, the
+    fp32 weight gradients at the GPU's dA and H_b."""
+    rng = np.random.default_rng(700 + seed)
+    E = int(rng.integers(1, 13))
+    counts = [int(v) for v in rng.choice([0, 1, 3, 64, 255, 256, 257, 600], size=E)]
+    if sum(counts) == 0:
+        counts[0] = 5
+    d = int(rng.choice([64, 128, 192, 320]))
+    f = int(rng.choice([64, 128, 192, 256]))
+    x, wgu, wd, offsets = _ffn_inputs(800 + seed, counts, d, f, "bf16")
+    R = int(offsets[-1])
+    bf = torch.bfloat16
+    xt, wgut, wdt = dev(x, bf), dev(wgu, bf), dev(wd, bf)
+    off = dev(offsets.astype(np.int32), torch.int32)
+    case(f"ffn bwd fuzz seed={seed} counts={counts} d={d} f={f}")
+    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off)
+    dy = dev(rng.standard_normal((R, d)).astype(np.float32), bf)
+    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, return_ws=True)
+    torch.cuda.synchronize()
+    dA_g, hb_g = laep.ffn_bwd_ws_views(ws, R, f, bf)
+    act_h, dy_h, dA_h, hb_h = host(act), host(dy), host(dA_g), host(hb_g)
+    rdx, rdA, rhb = om.grouped_ffn_dgrad(dy_h, act_h, wgu, wd, offsets, dtype="bf16",
+                                         dA_given=dA_h)
+    assert rownorm_err(dA_h, rdA) <= TOL_BF16
+    assert rownorm_err(hb_h, rhb) <= TOL_BF16
+    assert rownorm_err(host(dx), rdx) <= TOL_BF16
+    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, hb_h, offsets, E)
+    got_gu, got_d = host(dwgu), host(dwd)
+    for e in range(E):
+        assert rownorm_err(got_gu[e], rgu[e]) <= TOL_F32, e
+        assert rownorm_err(got_d[e], rd[e]) <= TOL_F32, e
+
+
 # ---------------------------------------------------------------------------
 # the whole layer, end to end, tiny fp32 workload
 # ---------------------------------------------------------------------------
