@@ -520,9 +520,8 @@ def main():
     if args.summarize_trace:
         return summarize_trace(args)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): this build has no "
-              f"multi-GPU expert-parallel path; the sharding design is described in DESIGN.md.",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the library has no "
+              f"multi-GPU expert-parallel path.", file=sys.stderr)
         sys.exit(2)
     if args.profile_target:
         return profile_target(args)

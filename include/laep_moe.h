@@ -55,7 +55,7 @@ extern "C" {
 /* return codes */
 #define LAEP_OK 0
 #define LAEP_ERR_INVALID_ARG 1 /* null pointer, bad size, misaligned pointer */
-#define LAEP_ERR_UNSUPPORTED 2 /* dtype or shape this build does not handle  */
+#define LAEP_ERR_UNSUPPORTED 2 /* dtype or shape the library does not handle */
 #define LAEP_ERR_WORKSPACE 3   /* ws_bytes smaller than moe_workspace_bytes() */
 #define LAEP_ERR_HIP 4         /* a HIP launch reported an error              */
 #define LAEP_ERR_INFEASIBLE 5  /* the request cannot be met (e.g. capacity)   */
@@ -67,7 +67,7 @@ extern "C" {
 #define LAEP_CALL_FFN_BWD 3
 #define LAEP_CALL_ROUTE_BWD 4
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define LAEP_MAX_EXPERTS 256
 #define LAEP_MAX_LAYERS 256
 
