@@ -18,8 +18,10 @@ Prints ONE JSON line:
                its stream in every timed step.  `traffic` is the HBM bytes per
                call from the committed rocprofv3 counter summary, reported only
                while the kernel sources still match the ones it was taken on.
-  breakdown    every call: mean / median / p10 / p90 microseconds over the timed
-               steps and its rate on algorithmic bytes or flops
+  breakdown    every call: mean / median / p10 / p90 microseconds over a second
+               pass of the same steps with events around every call, and its rate
+               on algorithmic bytes or flops (the timed pass brackets only the
+               dominant call, since each event marker costs the GPU a few us)
   attainable   what a plain copy kernel and a bf16 MFMA loop reach on this GPU
   supplementary  moe_expert_counts at T x {1, 8, 64} tokens; route, counts, the
                two back to back, and the fused moe_route_count, each timed alone
@@ -541,17 +543,35 @@ def main():
             fn()
     torch.cuda.synchronize()
     names = [n for n, _ in su.calls(0)]
+    dom = "ffn_bwd" if w.backward else "ffn_fwd"   # the dominant call
+    # Timed region: wall clock over the steps gives `value`; HIP events on the
+    # calls' stream bracket the dominant call only (an event marker between
+    # two calls costs the GPU about 5 us, so events around every call would
+    # inflate the step time).
+    dom_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        for n, fn in su.calls(i):
+            if n == dom:
+                dom_ev[i][0].record(stream)
+                fn()
+                dom_ev[i][1].record(stream)
+            else:
+                fn()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = wall * 1e3 / args.steps
+
+    # Per-call breakdown: the same steps again, with events around every call
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in names] for _ in range(args.steps)]
-    t0 = time.perf_counter()
     for i in range(args.steps):
         for j, (_, fn) in enumerate(su.calls(i)):
             ev[i][j][0].record(stream)
             fn()
             ev[i][j][1].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = wall * 1e3 / args.steps
 
     # warm: the same input set every step (x can stay in the caches between
     # steps); reported beside the primary, rotating-input number
@@ -577,9 +597,10 @@ def main():
             st["frac_mfma_peak"] = round(st["TFLOPs"] / PEAK_BF16_TFLOPS, 3)
         breakdown[n] = st
 
-    # the dominant call: the grouped FFN (backward when the step has one)
-    dom = "ffn_bwd" if w.backward else "ffn_fwd"
-    dom_us = breakdown[dom]["mean_us"]
+    # the dominant call (the grouped FFN, backward when the step has one), timed
+    # inside the timed region
+    dom_st = _stats([dom_ev[i][0].elapsed_time(dom_ev[i][1]) for i in range(args.steps)])
+    dom_us = dom_st["mean_us"]
     achieved = fl[dom] / (dom_us * 1e-6) / 1e12
     traffic, traffic_src = _traffic(f"{dom}_{w.name}",
                                     FFN_BWD_SOURCES if dom == "ffn_bwd" else FFN_FWD_SOURCES)
@@ -616,7 +637,8 @@ def main():
                      "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "traffic_source": traffic_src,
-                     "algorithmic_flops_per_call": fl[dom], "mean_call_us": dom_us},
+                     "algorithmic_flops_per_call": fl[dom], "mean_call_us": dom_us,
+                     "call_us_stats": dom_st},
         "cpu_baseline": cpu,
         "attainable": attain,
         "warm": {"ms_per_step": warm_ms, "value": w.T / (warm_ms * 1e-3),
