@@ -25,8 +25,8 @@ FFN.  The readings used here:
 
 Rounding points (the layer dtype "bf16" or "f32"; "f64" = none):
 act_save = round(A); H = round(silu(A_g) * A_u) from the unrounded A;
-Y = round(H W_d^T); out = round(sum_j g_j Y_j).  Gates, dgate and weight
-gradients are float32.
+Y = round(H W_d^T); out = round(sum_j g_j Y_j).  Backward: dH = round(dY W_d)
+before the SwiGLU backward.  Gates, dgate and weight gradients are float32.
 """
 from __future__ import annotations
 
@@ -302,9 +302,11 @@ def grouped_ffn_dgrad(dy_perm, act_save, w_gate_up, w_down, offsets,
                       expert_map=None, dtype: str = "bf16", dA_given=None):
     """Data gradient of the grouped FFN.
 
-    Per expert: dH = dY W_d; (dA, H_b) = swiglu_bwd(dH, act_save);
-    dX = round(dA W_gu).  ``dA_given`` (teacher forcing) replaces the dA
-    computed here as the input of dX.  Returns (dx_perm, dA, H_b).
+    Per expert: dH = round(dY W_d); (dA, H_b) = swiglu_bwd(dH, act_save);
+    dX = round(dA W_gu).  (The paper fixes no rounding points; dH is taken
+    in the layer dtype, as the first data-gradient product stores it.)
+    ``dA_given`` (teacher forcing) replaces the dA computed here as the input
+    of dX.  Returns (dx_perm, dA, H_b).
     """
     rnd = rounder(dtype)
     R, d = dy_perm.shape
@@ -318,7 +320,7 @@ def grouped_ffn_dgrad(dy_perm, act_save, w_gate_up, w_down, offsets,
         if hi == lo:
             continue
         p = _phys(expert_map, e)
-        dH = np.asarray(dy_perm[lo:hi], F64) @ np.asarray(w_down[p], F64)
+        dH = rnd(np.asarray(dy_perm[lo:hi], F64) @ np.asarray(w_down[p], F64))
         dA[lo:hi], Hb[lo:hi] = swiglu_bwd(dH, act_save[lo:hi], dtype)
         src = dA[lo:hi] if dA_given is None else np.asarray(dA_given[lo:hi], F64)
         dx[lo:hi] = rnd(src @ np.asarray(w_gate_up[p], F64))

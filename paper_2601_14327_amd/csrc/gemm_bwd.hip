@@ -1,7 +1,10 @@
 // Backward grouped GEMMs of the SwiGLU expert FFN (moe_grouped_ffn_bwd) on
 // the gfx950 matrix cores:
-//   dgrad 1   dH = dY W_d[p]        (A = dY rows, K contiguous; B = W_d [K=d][N=f])
-//             -> SwiGLU backward epilogue at the saved pre-activations: dA, H_b
+//   dgrad 1   dH = dY W_d[p]        (A = dY rows, K contiguous; B = W_d [K=d][N=f]),
+//             stored as bf16; then an elementwise pass computes the SwiGLU
+//             backward at the saved pre-activations: dA, H_b
+//             (a fused epilogue that read the pre-activations there cost about
+//             55 us per tile: every CU reads and writes ~640 KB at once)
 //   dgrad 2   dX = dA W_gu[p]       (A = dA rows; B = W_gu [K=2f][N=d])
 //   wgrad     dW_d[p]  = dY^T H_b   (both operands [K = routed rows][features])
 //             dW_gu[p] = dA^T X     -> fp32 weight gradients, one tile per expert
@@ -93,9 +96,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   static_assert(NWM == 2, "the staged epilogues process one wave row per pass");
   constexpr int PITCH16 = BN * 2 + 16;   // bf16 staging pitch
   constexpr int PITCH32 = BN * 4 + 16;   // fp32 staging pitch
-  constexpr int EPI_BYTES = (EPI == EPI_WGRAD)  ? 128 * PITCH32
-                            : (EPI == EPI_GU_BWD) ? 3 * 64 * PITCH16
-                                                  : BM * PITCH16;
+  constexpr int EPI_BYTES = (EPI == EPI_WGRAD) ? 128 * PITCH32 : BM * PITCH16;
   constexpr int RING = kRingSlots * kRingHalf;
   constexpr int SMEM = RING > EPI_BYTES ? RING : EPI_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -357,107 +358,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       wait_lgkm0();
       __builtin_amdgcn_s_barrier();
     }
-  } else if (EPI == EPI_GU_BWD) {
-    // dH tile (columns = f-columns nt*BN ...), 64 rows per pass (half of one
-    // wave row).  Stage the saved pre-activations of those rows, compute
-    // dA_g, dA_u and H_b, and write all three back with whole-row stores.
-    const int f = p.f;
-    const int ncols = min(BN, f - nt * BN);
-    const int cpr = ncols / 8;
-    char* G = smem;
-    char* U = smem + 64 * PITCH16;
-    char* Hs = smem + 128 * PITCH16;
-    for (int pass = 0; pass < 4; ++pass) {
-      const int prow0 = pass * 64;
-      const int prows = min(64, te.rows - prow0);
-      // stage A_g and A_u: every load of a thread issued before the first wait
-      constexpr int CPR = BN / 8, ITERS = 64 * CPR / NT;
-      {
-        u32x4_t g[ITERS], u[ITERS];
-#pragma unroll
-        for (int it = 0; it < ITERS; ++it) {
-          const int c = it * NT + tid;
-          const int r = c / CPR, cc = c % CPR;
-          if (r < prows && cc < cpr) {
-            const bf16_t* src = p.aux + (long long)(te.row0 + prow0 + r) * 2 * f + nt * BN + cc * 8;
-            g[it] = *reinterpret_cast<const u32x4_t*>(src);
-            u[it] = *reinterpret_cast<const u32x4_t*>(src + f);
-          }
-        }
-#pragma unroll
-        for (int it = 0; it < ITERS; ++it) {
-          const int c = it * NT + tid;
-          const int r = c / CPR, cc = c % CPR;
-          if (r < prows && cc < cpr) {
-            *reinterpret_cast<u32x4_t*>(G + r * PITCH16 + cc * 16) = g[it];
-            *reinterpret_cast<u32x4_t*>(U + r * PITCH16 + cc * 16) = u[it];
-          }
-        }
-      }
-      wait_lgkm0();
-      __syncthreads();
-      if (wm == (pass >> 1)) {
-        const int i0 = (pass & 1) * (TM / 2);
-#pragma unroll
-        for (int ii = 0; ii < TM / 2; ++ii)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int i = i0 + ii;
-              const int r = ii * 32 + lrow;
-              const int c = wn * WTN + j * 32 + q * 8 + lcol;
-              const u32x2_t gw = *reinterpret_cast<const u32x2_t*>(G + r * PITCH16 + c * 2);
-              const u32x2_t uw = *reinterpret_cast<const u32x2_t*>(U + r * PITCH16 + c * 2);
-              const float ag[4] = {lo_bf16(gw[0]), hi_bf16(gw[0]), lo_bf16(gw[1]), hi_bf16(gw[1])};
-              const float au[4] = {lo_bf16(uw[0]), hi_bf16(uw[0]), lo_bf16(uw[1]), hi_bf16(uw[1])};
-              float dag[4], dau[4], hb[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const float dh = acc[i][j][q * 4 + e];
-                const float s = fast_sigmoid(ag[e]);
-                const float sl = ag[e] * s;
-                dag[e] = dh * au[e] * s * (1.0f + ag[e] * (1.0f - s));
-                dau[e] = dh * sl;
-                hb[e] = sl * au[e];
-              }
-              u32x2_t wg = {pack_bf16x2(dag[0], dag[1]), pack_bf16x2(dag[2], dag[3])};
-              u32x2_t wu = {pack_bf16x2(dau[0], dau[1]), pack_bf16x2(dau[2], dau[3])};
-              u32x2_t wh = {pack_bf16x2(hb[0], hb[1]), pack_bf16x2(hb[2], hb[3])};
-              *reinterpret_cast<u32x2_t*>(G + r * PITCH16 + c * 2) = wg;
-              *reinterpret_cast<u32x2_t*>(U + r * PITCH16 + c * 2) = wu;
-              *reinterpret_cast<u32x2_t*>(Hs + r * PITCH16 + c * 2) = wh;
-            }
-      }
-      wait_lgkm0();
-      __syncthreads();
-      {  // dA (gate and up halves) and H_b: LDS reads first, then the stores
-        u32x4_t g[ITERS], u[ITERS], h[ITERS];
-#pragma unroll
-        for (int it = 0; it < ITERS; ++it) {
-          const int c = it * NT + tid;
-          const int r = c / CPR, cc = c % CPR;
-          g[it] = *reinterpret_cast<const u32x4_t*>(G + r * PITCH16 + cc * 16);
-          u[it] = *reinterpret_cast<const u32x4_t*>(U + r * PITCH16 + cc * 16);
-          h[it] = *reinterpret_cast<const u32x4_t*>(Hs + r * PITCH16 + cc * 16);
-        }
-#pragma unroll
-        for (int it = 0; it < ITERS; ++it) {
-          const int c = it * NT + tid;
-          const int r = c / CPR, cc = c % CPR;
-          if (r < prows && cc < cpr) {
-            const long long row = te.row0 + prow0 + r;
-            bf16_t* dst = p.out + row * 2 * f + nt * BN + cc * 8;
-            st_stream(reinterpret_cast<u32x4_t*>(dst), g[it]);
-            st_stream(reinterpret_cast<u32x4_t*>(dst + f), u[it]);
-            st_stream(reinterpret_cast<u32x4_t*>(p.out2 + row * f + nt * BN + cc * 8), h[it]);
-          }
-        }
-      }
-      wait_lgkm0();
-      __syncthreads();
-    }
-  } else {  // EPI_STORE (bf16 rows, dX)
+  } else {  // EPI_STORE (bf16 rows: dH, dX)
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int r = wm * WTM + i * 32 + lrow;
@@ -492,6 +393,47 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       }
     }
   }
+}
+
+// SwiGLU backward at the saved pre-activations, one 8-column vector of one
+// routed row per thread: with s = sigmoid(A_g),
+//   dA_g = dH A_u s (1 + A_g (1 - s)),  dA_u = dH silu(A_g),  H_b = silu(A_g) A_u.
+// dH arrives in the H_b buffer and is replaced there.  Streaming accesses:
+// every element is read and written once.
+__global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restrict__ act,
+                                                         int64_t R, int f,
+                                                         u32x4_t* __restrict__ dA,
+                                                         u32x4_t* __restrict__ hb) {
+  const int vpr = f / 8;  // vectors per row of dH / H_b
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= R * vpr) return;
+  const long long r = i / vpr;
+  const int v = (int)(i % vpr);
+  const u32x4_t dh = ld_stream(hb + i);
+  const u32x4_t g = ld_stream(act + r * 2 * vpr + v);
+  const u32x4_t u = ld_stream(act + r * 2 * vpr + vpr + v);
+  u32x4_t og, ou, oh;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    float dag[2], dau[2], h[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const float d = e ? hi_bf16(dh[w]) : lo_bf16(dh[w]);
+      const float ag = e ? hi_bf16(g[w]) : lo_bf16(g[w]);
+      const float au = e ? hi_bf16(u[w]) : lo_bf16(u[w]);
+      const float sg = fast_sigmoid(ag);
+      const float sl = ag * sg;
+      dag[e] = d * au * sg * (1.0f + ag * (1.0f - sg));
+      dau[e] = d * sl;
+      h[e] = sl * au;
+    }
+    og[w] = pack_bf16x2(dag[0], dag[1]);
+    ou[w] = pack_bf16x2(dau[0], dau[1]);
+    oh[w] = pack_bf16x2(h[0], h[1]);
+  }
+  st_stream(dA + r * 2 * vpr + v, og);
+  st_stream(dA + r * 2 * vpr + vpr + v, ou);
+  st_stream(hb + i, oh);
 }
 
 // zero page for the ragged-K loads, and the tile tables
@@ -544,7 +486,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   hipLaunchKernelGGL(zero_page_kernel, dim3(1), dim3(256), 0, s, reinterpret_cast<uint32_t*>(zero),
                      kZeroBytes / 4);
 
-  // dgrad 1: dH = dY W_d, SwiGLU backward epilogue -> dA, H_b
+  // dgrad 1: dH = dY W_d (bf16, into the H_b buffer), then the SwiGLU backward -> dA, H_b
   const int group = tile_group("LAEP_TILE_GROUP_BWD", 8);
   GemmParams g = {};
   g.group = group;
@@ -561,11 +503,17 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.K = d;
   g.n_tiles_n = ceil_div(f, kBwdBN);
   g.tiles_per_entry = g.n_tiles_n;
-  g.out = dA;
-  g.out2 = Hb;
-  g.aux = static_cast<const bf16_t*>(act_save);
-  hipError_t err = launch_bwd<EPI_GU_BWD, false>(g, max_ragged * g.n_tiles_n, s);
+  g.out = Hb;
+  g.ldo = f;
+  hipError_t err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
   if (err != hipSuccess) return err;
+  if (R > 0) {
+    const long long n_vec = R * (long long)(f / 8);
+    hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n_vec + 255) / 256)), dim3(256), 0, s,
+                       static_cast<const u32x4_t*>(act_save), (int64_t)R, f,
+                       reinterpret_cast<u32x4_t*>(dA), reinterpret_cast<u32x4_t*>(Hb));
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  }
 
   // dgrad 2: dX = dA W_gu
   g.A = dA;

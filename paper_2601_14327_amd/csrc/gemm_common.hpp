@@ -10,7 +10,7 @@
 namespace laep {
 namespace {
 
-enum { EPI_GU = 0, EPI_STORE = 1, EPI_GU_BWD = 2, EPI_WGRAD = 3 };
+enum { EPI_GU = 0, EPI_STORE = 1, EPI_WGRAD = 3 };
 
 struct GemmParams {
   const bf16_t* A;
