@@ -289,7 +289,9 @@ int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T,
  *   (offsets[E] <= R); expert_map device [E] int32 or NULL (identity), -1 =
  *   pruned (such experts must have no rows; the map must not repeat a slot);
  *   y_perm device [R, d_model]; act_save device [R, 2*d_ff] or NULL.
- *   Constraints: d_model % 64 == 0, d_ff % 64 == 0, R < 2^31.
+ *   Constraints: d_model % 64 == 0, d_ff % 64 == 0, R < 2^31; bf16: one
+ *   expert's w_gate_up under 2 GiB (4*d_ff*d_model bytes), since the GEMMs
+ *   address it with 32-bit offsets (LAEP_ERR_UNSUPPORTED otherwise).
  *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff)
  *   (holds H and the tile table).
  */
@@ -309,8 +311,9 @@ int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
  *
  *   x device [T, d_model] bf16; row_src device [R] int32 (every entry in
  *   [0, T*k)); the other arguments and the workspace are those of
- *   moe_grouped_ffn_fwd.  dtype must be LAEP_BF16 (LAEP_ERR_UNSUPPORTED
- *   otherwise).
+ *   moe_grouped_ffn_fwd.  dtype must be LAEP_BF16 and x under 2 GiB
+ *   (T*d_model*2 bytes: its rows are addressed with 32-bit offsets);
+ *   LAEP_ERR_UNSUPPORTED otherwise.
  */
 int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
                                int k, const void* w_gate_up,

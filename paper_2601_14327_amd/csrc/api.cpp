@@ -67,6 +67,9 @@ size_t elem_bytes(int dtype) { return dtype == LAEP_BF16 ? 2 : 4; }
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+// extent of a buffer the bf16 GEMMs address with 32-bit byte offsets
+constexpr int64_t kMaxBufferBytes = (int64_t)1 << 31;
+
 int check_ffn_shape(int dtype, int E, int d_model, int d_ff, int64_t R) {
   int rc = check_dtype(dtype);
   if (rc) return rc;
@@ -78,6 +81,9 @@ int check_ffn_shape(int dtype, int E, int d_model, int d_ff, int64_t R) {
           d_model, d_ff);
   REQUIRE(d_model % 64 == 0 && d_ff % 64 == 0, LAEP_ERR_UNSUPPORTED,
           "d_model=%d and d_ff=%d must be multiples of 64", d_model, d_ff);
+  // the bf16 GEMMs address one expert's weights with 32-bit byte offsets
+  REQUIRE(dtype != LAEP_BF16 || (int64_t)4 * d_ff * d_model < kMaxBufferBytes,
+          LAEP_ERR_UNSUPPORTED, "bf16: one expert's w_gate_up (2*d_ff*d_model) must be under 2 GiB");
   return LAEP_OK;
 }
 
@@ -359,6 +365,8 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T, int
   REQUIRE(T >= 0 && k >= 1, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: T=%d, k=%d", T, k);
   REQUIRE(R <= (int64_t)T * k, LAEP_ERR_INVALID_ARG,
           "moe_grouped_ffn_fwd_gather: R=%lld exceeds T*k", (long long)R);
+  REQUIRE((int64_t)T * d_model * 2 < kMaxBufferBytes, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_fwd_gather: x (T*d_model bf16) must be under 2 GiB");
   REQUIRE(offsets, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: offsets must be non-null");
   if (R == 0) return ok();
   REQUIRE(x && row_src && w_gate_up && w_down && y_perm && ws, LAEP_ERR_INVALID_ARG,

@@ -3,7 +3,7 @@
 //   gate/up   A = X_e [M_e, d]  x W_gu[p]^T [2f, d]  -> SwiGLU epilogue (H, act_save)
 //   down      A = H_e [M_e, f]  x W_d[p]^T  [d, f]   -> Y
 // Both operands are K-contiguous, so global -> LDS moves are LDS-DMA
-// (global_load_lds_dwordx4, no register staging): one wave instruction fills
+// (buffer_load_dwordx4 with the LDS flag, no register staging): one wave instruction fills
 // 1 KB of LDS contiguously, lane i at +16 i, so any LDS swizzle is applied on
 // the global side (each lane fetches the chunk that belongs in its slot).
 //
@@ -37,15 +37,23 @@
 namespace laep {
 namespace {
 
-// Global -> LDS copy of NC 16-byte chunks per thread (a device function, not a
-// lambda: the host pass of a kernel must not see the LDS-DMA builtin inside a
-// lambda, or the kernel's launch stub is dropped).
+// fourth word of a raw buffer resource: 32-bit data format, no swizzle
+constexpr int kBufferFlags = 0x00020000;
+
+// Global -> LDS copy of NC 16-byte chunks per thread through buffer loads
+// with the LDS flag: chunk i of this thread is at byte voff[i] + soff of the
+// operand's buffer.  (The global-segment form of the same copy makes the
+// compiler drain every outstanding LDS read, lgkmcnt(0), before each fragment
+// use in the loop; with the buffer form it counts them in order.)  A device
+// function, not a lambda: the host pass of a kernel must not see the LDS-DMA
+// builtin inside a lambda, or the kernel's launch stub is dropped.
 template <int NC, int NT>
-__device__ __forceinline__ void dma_chunks(char* dst, const bf16_t* const* src, int k0, int wave) {
+__device__ __forceinline__ void dma_chunks(char* dst, __amdgpu_buffer_rsrc_t rsrc,
+                                           const uint32_t* voff, int soff, int wave) {
 #pragma unroll
   for (int i = 0; i < NC; ++i)
-    __builtin_amdgcn_global_load_lds(src[i] + k0, (lds_void_t*)(dst + (i * NT + wave * 64) * 16),
-                                     16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)(dst + (i * NT + wave * 64) * 16),
+                                             16, voff[i], soff, 0, 0);
 }
 
 // Tile of the XCD-contiguous schedule owned by this workgroup, or -1.
@@ -215,10 +223,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave / NWN, wn = wave % NWN;
 
-  // per-thread global source of each LDS chunk it fills (k-step 0)
-  const bf16_t* a_src[NH];
-  const bf16_t* b_src[NH];
-  const bf16_t* Bw = p.B + (long long)te.phys * p.strideB;
+  // per-thread byte offset of each LDS chunk it fills (k-step 0) within the
+  // operand's buffer: A from the tile's first row (gathered rows: from x),
+  // B from the expert's weight matrix
+  const char* a_base = GATHER ? reinterpret_cast<const char*>(p.A)
+                              : reinterpret_cast<const char*>(p.A + (long long)te.row0 * p.lda);
+  const char* b_base = reinterpret_cast<const char*>(p.B + (long long)te.phys * p.strideB);
+  uint32_t a_voff[NH], b_voff[NH];
 #pragma unroll
   for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
@@ -226,11 +237,14 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
     const int lc = (q & 7) ^ swz8(r);
     const int rr = r < te.rows ? r : te.rows - 1;  // rows past the expert: any valid row
     // gathered rows: the token row of routed row te.row0 + rr (dispatch folded in)
-    const long long arow = GATHER ? (long long)(p.row_src[te.row0 + rr] / p.slots_k)
-                                  : (long long)(te.row0 + rr);
-    a_src[i] = p.A + arow * p.lda + lc * 8;
-    b_src[i] = Bw + (long long)weight_row<BN, GU_ROWS>(p, nt, r) * p.ldb + lc * 8;
+    const long long arow = GATHER ? (long long)(p.row_src[te.row0 + rr] / p.slots_k) : rr;
+    a_voff[i] = (uint32_t)((arow * p.lda + lc * 8) * 2);
+    b_voff[i] = (uint32_t)(((long long)weight_row<BN, GU_ROWS>(p, nt, r) * p.ldb + lc * 8) * 2);
   }
+  const __amdgpu_buffer_rsrc_t a_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a_base), 0, -1, kBufferFlags);
+  const __amdgpu_buffer_rsrc_t b_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(b_base), 0, -1, kBufferFlags);
   const int nk = p.K / 64;
   // half h: A of k-step h/2 (h even) or B (h odd), in slot h % 5.  Past the
   // end the last k-step is loaded again (never read), so every iteration
@@ -238,8 +252,8 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
   auto issue_half = [&](int h) {
     const int ks = min(h >> 1, nk - 1);
     char* dst = smem + (h % NSLOT) * HALF;
-    if (h & 1) dma_chunks<NH, NT>(dst, b_src, ks * 64, wave);
-    else dma_chunks<NH, NT>(dst, a_src, ks * 64, wave);
+    if (h & 1) dma_chunks<NH, NT>(dst, b_rsrc, b_voff, ks * 128, wave);
+    else dma_chunks<NH, NT>(dst, a_rsrc, a_voff, ks * 128, wave);
   };
 
   // fragment LDS byte offsets within a half for k16 sub-step 0; sub-step s

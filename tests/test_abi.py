@@ -107,6 +107,12 @@ def test_ffn_validation(L):
     assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 96, 128, 64, p, None, p, 1 << 30, None) == 2
     assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 128, 128, 64, p, None, p, 16, None) == 3
     assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 5, 8, 128, 128, 64, p, None, p, 1 << 30, None) == 2
+    # bf16: one expert's weights are addressed with 32-bit offsets (under 2 GiB)
+    assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 32768, 16384, 64, p, None, p, 16,
+                                 None) == 2
+    assert "2 GiB" in _err(L)
+    assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 32768, 16320, 64, p, None, p, 16,
+                                 None) == 3
     # backward: only bf16
     assert L.moe_grouped_ffn_bwd(p, p, p, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0, p,
                                  1 << 30, None) == 2
@@ -118,6 +124,9 @@ def test_ffn_validation(L):
                                         p, 1 << 30, None) == 1
     assert L.moe_grouped_ffn_fwd_gather(p, None, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, p, None,
                                         p, 1 << 30, None) == 1
+    # x addressed with 32-bit offsets: T * d_model * 2 bytes under 2 GiB
+    assert L.moe_grouped_ffn_fwd_gather(p, p, 1 << 19, 2, p, p, p, None, 1, 8, 2048, 128, 20, p,
+                                        None, p, 1 << 30, None) == 2
 
 
 def test_route_bwd_validation(L):
