@@ -22,10 +22,11 @@
 // consecutive k values a ds_read_b128 gives for a K-contiguous operand.  The
 // 32-byte block b of k-row r is stored at b ^ ((r & 7) << 1), so the four
 // k-rows a group reads fall in different banks.  Rows past the end of an
-// expert (the ragged reduction of the weight gradient) are loaded from a zero
-// page.  The epilogues write with streaming (non-temporal) stores: every
-// output (dA, H_b, dX, the fp32 weight gradients) is far larger than the
-// caches (measured 3 % faster on the backward call).
+// expert (the ragged reduction of the weight gradient) fall outside the
+// buffer range of the k-step's load and read as zeros.  The epilogues write
+// with streaming (non-temporal) stores: every output (dA, H_b, dX, the fp32
+// weight gradients) is far larger than the caches (measured 3 % faster on the
+// backward call).
 #include <type_traits>
 
 #include "gemm_common.hpp"
@@ -41,6 +42,8 @@ constexpr int kRingHalf = 256 * kRingRowB;   // one operand's k-step: 32 KB
 constexpr int kRingSlots = 5;
 constexpr int kTrRowB = 512;                 // K-strided half: bytes per k-row (256 features)
 constexpr int kTrCpr = kTrRowB / 16;         // 16-byte chunks per k-row
+// fourth word of a raw buffer resource: 32-bit data format, no swizzle
+constexpr int kBufferFlags = 0x00020000;
 
 // LDS slot q of a TR tile -> (k-row, element column within the tile)
 __device__ __forceinline__ void tr_slot(int q, int cpr, int& r, int& col) {
@@ -67,23 +70,25 @@ __device__ __forceinline__ u32x4_t read_tr_frag(const char* st, int off1, int of
   return v;
 }
 
-// One half (one operand's k-step ks) of LDS-DMA loads: NC 16-byte chunks per
-// thread, chunk i of thread tid in LDS slot i * NT + tid.  base[i] is the
-// chunk's global address at k-step 0 and kstep the element stride between
-// k-steps; for K-strided operands k-rows at or past kvalid come from the zero
-// page (a device function, not a lambda: the host pass must not see the
-// LDS-DMA builtin inside a lambda).
-template <int NC, int NT, bool TR>
-__device__ __forceinline__ void dma_half(char* dst, const bf16_t* const* base, const int* krow,
-                                         long long kstep, int ks, int kvalid, const bf16_t* zero,
-                                         int wave) {
+// One half (one operand's k-step) of LDS-DMA loads, through buffer loads with
+// the LDS flag: NC 16-byte chunks per thread, chunk i of thread tid in LDS
+// slot i * NT + tid, at byte voff[i] of the k-step's buffer.  The buffer
+// starts at the k-step's first element and ends where the operand's valid
+// rows end, so loads past that (the weight gradient's rows past the end of
+// the expert) return zeros.  (The global-segment form of this copy makes the
+// compiler drain every outstanding LDS read, lgkmcnt(0), before each fragment
+// use in the loop; with the buffer form it counts them in order.)  A device
+// function, not a lambda: the host pass must not see the LDS-DMA builtin
+// inside a lambda.
+template <int NC, int NT>
+__device__ __forceinline__ void dma_half(char* dst, const char* base, uint32_t extent,
+                                         const uint32_t* voff, int wave) {
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, (int)extent, kBufferFlags);
 #pragma unroll
-  for (int i = 0; i < NC; ++i) {
-    const bf16_t* src = base[i] + kstep * ks;
-    if (TR && ks * 64 + krow[i] >= kvalid) src = zero;
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(dst + (i * NT + wave * 64) * 16), 16, 0,
-                                     0);
-  }
+  for (int i = 0; i < NC; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)(dst + (i * NT + wave * 64) * 16),
+                                             16, voff[i], 0, 0, 0);
 }
 
 template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR>
@@ -147,34 +152,31 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   const int kext = (EPI == EPI_WGRAD) ? te.rows : p.K;
   const int nk = (kext + 63) / 64;
 
-  // ---- per-thread DMA sources (k-step 0) ----------------------------------------
-  const bf16_t* a_base[NH];
-  int a_krow[NH];
+  // ---- per-thread DMA offsets within a k-step's buffer ----------------------------
+  // A: weight gradient [routed rows][Mw] (k = row, feature = mt*BM + col), or
+  // the data gradient's expert rows (K contiguous), from the tile's first row
+  uint32_t a_voff[NH];
 #pragma unroll
   for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
-    if (A_TR) {  // weight gradient: [routed rows][Mw], k = row, feature = mt*BM + col
+    if (A_TR) {
       int r, col;
       tr_slot(q, kTrCpr, r, col);
       int c = mt * BM + col;
       c = c < p.Mw ? c : p.Mw - 8;  // columns past Mw: any valid column (not stored)
-      a_krow[i] = r;
-      a_base[i] = p.A + (long long)(te.row0 + r) * p.lda + c;
-    } else {     // data gradient: expert rows, K contiguous
+      a_voff[i] = (uint32_t)(((long long)r * p.lda + c) * 2);
+    } else {
       const int r = q >> 3;
       const int lc = (q & 7) ^ swz8(r);
       const int rr = r < te.rows ? r : te.rows - 1;  // rows past the expert: any valid row
-      a_krow[i] = 0;
-      a_base[i] = p.A + (long long)(te.row0 + rr) * p.lda + lc * 8;
+      a_voff[i] = (uint32_t)(((long long)rr * p.lda + lc * 8) * 2);
     }
   }
-  const long long a_kstep = A_TR ? 64LL * p.lda : 64LL;
+  const char* a_tile = reinterpret_cast<const char*>(p.A + (long long)te.row0 * p.lda);
+  const long long a_kstep = A_TR ? 128LL * p.lda : 128LL;  // bytes per k-step
   // B is K-strided in every backward product: [K][N] rows, feature nt*BN + col
   // (clamped to the last valid column block)
-  const bf16_t* b_base[NH];
-  int b_krow[NH];
-  const bf16_t* Bw = (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb
-                                        : p.B + (long long)te.phys * p.strideB;
+  uint32_t b_voff[NH];
 #pragma unroll
   for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
@@ -182,20 +184,26 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     tr_slot(q, kTrCpr, r, col);
     int c = nt * BN + col;
     c = c < p.N ? c : p.N - 8;
-    b_krow[i] = r;
-    b_base[i] = Bw + (long long)r * p.ldb + c;
+    b_voff[i] = (uint32_t)(((long long)r * p.ldb + c) * 2);
   }
-  const long long b_kstep = 64LL * p.ldb;
-  const int kvalid_a = A_TR ? kext : (1 << 30);
-  const int kvalid_b = (EPI == EPI_WGRAD) ? kext : (1 << 30);
+  const char* b_tile = reinterpret_cast<const char*>(
+      (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb : p.B + (long long)te.phys * p.strideB);
+  const long long b_kstep = 128LL * p.ldb;
   // half h: A of k-step h/2 (h even) or B (h odd), in slot h % 5.  Past the
   // end the last k-step is loaded again (never read), so every iteration
   // issues the same number of loads and one constant vmcnt serves every wait.
+  // A K-strided operand of the weight gradient ends with the expert's rows.
+  auto extent = [&](int ks, int ld) -> uint32_t {
+    if (EPI != EPI_WGRAD) return 0xffffffffu;
+    const int rem = kext - ks * 64;
+    return rem > 0 ? (uint32_t)((long long)min(rem, 64) * ld * 2) : 0u;
+  };
   auto issue_half = [&](int h) {
     const int ks = min(h >> 1, nk - 1);
     char* dst = smem + (h % kRingSlots) * kRingHalf;
-    if (h & 1) dma_half<NH, NT, true>(dst, b_base, b_krow, b_kstep, ks, kvalid_b, p.zero, wave);
-    else dma_half<NH, NT, A_TR>(dst, a_base, a_krow, a_kstep, ks, kvalid_a, p.zero, wave);
+    if (h & 1) dma_half<NH, NT>(dst, b_tile + b_kstep * ks, extent(ks, p.ldb), b_voff, wave);
+    else dma_half<NH, NT>(dst, a_tile + a_kstep * ks, A_TR ? extent(ks, p.lda) : 0xffffffffu,
+                          a_voff, wave);
   };
 
   // ---- fragment offsets within a half, k16 sub-step 0 -------------------------------
@@ -436,13 +444,7 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restri
   st_stream(hb + i, oh);
 }
 
-// zero page for the ragged-K loads, and the tile tables
-__global__ void zero_page_kernel(uint32_t* z, int n) {
-  for (int i = threadIdx.x; i < n; i += blockDim.x) z[i] = 0u;
-}
-
 constexpr int kBwdBM = 256, kBwdBN = 256;
-constexpr int kZeroBytes = 1024;
 
 template <int EPI, bool A_TR>
 hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
@@ -463,7 +465,7 @@ size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
   (void)d;
   const size_t elem = dtype == kDtypeBf16 ? 2 : 4;
   return ffn_bwd_hb_offset(R, f, dtype) + align_up((size_t)R * f * elem, 256) +
-         table_bytes(ceil_div(R, kBwdBM) + E) + table_bytes(E) + kZeroBytes;
+         table_bytes(ceil_div(R, kBwdBM) + E) + table_bytes(E);
 }
 
 hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
@@ -478,13 +480,10 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   const int max_ragged = ceil_div(R, kBwdBM) + E;
   TableWs tr = carve_table(tables, max_ragged);
   TableWs te = carve_table(tables + table_bytes(max_ragged), E);
-  bf16_t* zero = reinterpret_cast<bf16_t*>(tables + table_bytes(max_ragged) + table_bytes(E));
   hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
                      E, kBwdBM, 0, max_ragged, tr.n_entries, tr.table);
   hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
                      E, kBwdBM, 1, E, te.n_entries, te.table);
-  hipLaunchKernelGGL(zero_page_kernel, dim3(1), dim3(256), 0, s, reinterpret_cast<uint32_t*>(zero),
-                     kZeroBytes / 4);
 
   // dgrad 1: dH = dY W_d (bf16, into the H_b buffer), then the SwiGLU backward -> dA, H_b
   const int group = tile_group("LAEP_TILE_GROUP_BWD", 8);
@@ -493,7 +492,6 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.table = tr.table;
   g.n_entries = tr.n_entries;
   g.f = f;
-  g.zero = zero;
   g.A = static_cast<const bf16_t*>(dy);
   g.lda = d;
   g.B = static_cast<const bf16_t*>(w_d);
@@ -538,7 +536,6 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   w.table = te.table;
   w.n_entries = te.n_entries;
   w.f = f;
-  w.zero = zero;
   w.A = static_cast<const bf16_t*>(dy);
   w.lda = d;
   w.B = Hb;

@@ -33,7 +33,6 @@ struct GemmParams {
   float* wout;
   long long strideW;
   int accumulate;
-  const bf16_t* zero;  // >= 1 KB of zeros (ragged-K tail loads of the weight gradient)
   const int32_t* row_src;  // gathered A rows: row r of the product is A row row_src[r] / slots_k
   int slots_k;
   int group;               // row tiles per rasterisation group (backward products)
