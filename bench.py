@@ -7,7 +7,9 @@ accumulation.  One step = one forward pass of the whole layer:
 route + expert counts (one call) -> dispatch + grouped SwiGLU FFN (one call, the
 dispatch folded into the FFN's operand loads) -> combine, every call a kernel
 of the C-ABI library; three input sets rotate over the steps so the
-activations are not cache-resident.  Training steps (shard_bwd) keep the
+activations are not cache-resident.  With one slot per token (shard) the
+combine folds into the FFN call as well (the down projection writes each row,
+times its gate, to its token row).  Training steps (shard_bwd) keep the
 separate permute, because the weight gradient reads x_perm.
 
 Prints ONE JSON line:
@@ -227,7 +229,11 @@ class Setup:
                                                            dest_row=p.dest_row,
                                                            row_src=p.row_src))]
             gate = self.gate
-        if p.fused:   # dispatch folded into the FFN's operand loads
+        if p.fused_combine:   # one slot per token: dispatch and combine folded into the FFN
+            out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather_combine(
+                x, p.row_src, gate, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
+                out=p.out, save_act=p.act_save is not None, act_save=p.act_save))]
+        elif p.fused:   # dispatch folded into the FFN's operand loads
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather(
                 x, p.row_src, w.k, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
                 y_perm=p.y_perm, save_act=p.act_save is not None, act_save=p.act_save))]
@@ -236,7 +242,8 @@ class Setup:
                     ("ffn_fwd", lambda: L.moe_grouped_ffn_fwd(
                         p.x_perm, self.wgu, self.wd, p.offsets, ws=p.ws_ffn, y_perm=p.y_perm,
                         save_act=p.act_save is not None, act_save=p.act_save))]
-        out += [("combine", lambda: L.moe_combine(p.y_perm, gate, p.dest_row, out=p.out))]
+        if not p.fused_combine:
+            out += [("combine", lambda: L.moe_combine(p.y_perm, gate, p.dest_row, out=p.out))]
         if w.backward:
             if p.dw_gate_up is None:
                 import torch

@@ -324,6 +324,33 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
                                size_t ws_bytes, void* stream);
 
 /*
+ * moe_grouped_ffn_fwd_gather_combine -- moe_grouped_ffn_fwd_gather followed
+ * by moe_combine, for one slot per token (k = 1: an expert-parallel rank's
+ * local rows, each returned to its sender scaled by its gate).  The down
+ * projection's epilogue writes each routed row r straight to its token row:
+ *   out[t] = round(topk_gate[t] * y_r)   with t = row_src[r] (k = 1),
+ * where y_r is the rounded FFN output row, in the combine's arithmetic, so
+ * out is bit-identical to the three calls.  y_perm is written too when
+ * non-NULL (the backward's moe_combine_bwd reads it), else never.
+ *
+ *   topk_gate device [T] fp32; out device [T, d_model] bf16 (must not alias
+ *   x or y_perm); y_perm device [R, d_model] bf16 or NULL; the other
+ *   arguments and the workspace are those of moe_grouped_ffn_fwd_gather.
+ *   Rows of out whose token has no routed row (topk_idx == -1, which with
+ *   k = 1 happens only when no expert is alive) are not written; moe_combine
+ *   would write zeros there.
+ *   Errors: k != 1 or dtype != LAEP_BF16 -> LAEP_ERR_UNSUPPORTED.
+ */
+int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
+                                       int T, int k, const void* w_gate_up,
+                                       const void* w_down, const int32_t* offsets,
+                                       const int32_t* expert_map,
+                                       const float* topk_gate, int dtype, int E,
+                                       int d_model, int d_ff, int64_t R, void* out,
+                                       void* y_perm, void* act_save, void* ws,
+                                       size_t ws_bytes, void* stream);
+
+/*
  * moe_grouped_ffn_bwd -- backward of moe_grouped_ffn_fwd (data and weight
  * gradients), evaluated at the saved pre-activations act_save (Â):
  *

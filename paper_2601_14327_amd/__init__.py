@@ -12,6 +12,8 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     moe_permute          dispatch of token rows to expert order
     moe_grouped_ffn_fwd  grouped SwiGLU expert FFN (bf16 MFMA)
     moe_grouped_ffn_fwd_gather   the same with the dispatch folded into the operand loads
+    moe_grouped_ffn_fwd_gather_combine   and, for one slot per token, the combine folded
+                         into the down projection's epilogue
     moe_combine          gate-weighted combine
     moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
     moe_route_bwd        router / gate backward (softmax Jacobian, dW_r, dx)
@@ -34,6 +36,7 @@ from .api import (  # noqa: F401
     moe_grouped_ffn_bwd,
     moe_grouped_ffn_fwd,
     moe_grouped_ffn_fwd_gather,
+    moe_grouped_ffn_fwd_gather_combine,
     moe_permute,
     moe_permute_bwd,
     moe_route,

@@ -305,6 +305,40 @@ def moe_grouped_ffn_fwd_gather(x: torch.Tensor, row_src: torch.Tensor, k: int,
     return y_perm, act_save
 
 
+def moe_grouped_ffn_fwd_gather_combine(x: torch.Tensor, row_src: torch.Tensor,
+                                       topk_gate: torch.Tensor, w_gate_up: torch.Tensor,
+                                       w_down: torch.Tensor, offsets: torch.Tensor, *,
+                                       rows: Optional[int] = None, expert_map=None,
+                                       keep_y: bool = False, save_act: bool = False, ws=None,
+                                       out=None, y_perm=None, act_save=None):
+    """moe_grouped_ffn_fwd_gather + moe_combine for one slot per token (bf16):
+    routed row r goes straight to token row row_src[r], times its gate.
+    Returns (out, y_perm or None, act_save or None)."""
+    for t, n in ((x, "x"), (row_src, "row_src"), (topk_gate, "topk_gate"),
+                 (w_gate_up, "w_gate_up"), (w_down, "w_down"), (offsets, "offsets")):
+        _dev(t, n)
+    T, d = x.shape
+    R = T if rows is None else rows
+    f = w_down.shape[2]
+    E = offsets.shape[0] - 1
+    dev = x.device
+    out = torch.empty((T, d), dtype=x.dtype, device=dev) if out is None else out
+    if keep_y and y_perm is None:
+        y_perm = torch.empty((R, d), dtype=x.dtype, device=dev)
+    if not keep_y:
+        y_perm = None
+    if save_act and act_save is None:
+        act_save = torch.empty((R, 2 * f), dtype=x.dtype, device=dev)
+    if not save_act:
+        act_save = None
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d, f), dev)
+    check(lib().moe_grouped_ffn_fwd_gather_combine(
+        _ptr(x), _ptr(row_src), T, 1, _ptr(w_gate_up), _ptr(w_down), _ptr(offsets),
+        _ptr(expert_map), _ptr(topk_gate), _dtype_code(x), E, d, f, R, _ptr(out), _ptr(y_perm),
+        _ptr(act_save), _ptr(ws), ws.numel(), _stream(dev)))
+    return out, y_perm, act_save
+
+
 def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *,
                         expert_map=None, dw_gate_up=None, dw_down=None, accumulate=False,
                         ws=None, dx_perm=None, return_ws: bool = False):

@@ -384,6 +384,44 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T, int
                     "moe_grouped_ffn_fwd_gather");
 }
 
+int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src, int T, int k,
+                                       const void* w_gate_up, const void* w_down,
+                                       const int32_t* offsets, const int32_t* expert_map,
+                                       const float* topk_gate, int dtype, int E, int d_model,
+                                       int d_ff, int64_t R, void* out, void* y_perm,
+                                       void* act_save, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
+  if (rc) return rc;
+  REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_fwd_gather_combine: only LAEP_BF16 is supported");
+  REQUIRE(k == 1, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_fwd_gather_combine: k=%d, only one slot per token is supported", k);
+  REQUIRE(T >= 0, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather_combine: T=%d < 0", T);
+  REQUIRE(R <= (int64_t)T, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: R=%lld exceeds T", (long long)R);
+  REQUIRE((int64_t)T * d_model * 2 < kMaxBufferBytes, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_fwd_gather_combine: x and out (T*d_model bf16) must be under 2 GiB");
+  REQUIRE(offsets, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: offsets must be non-null");
+  if (R == 0) return ok();
+  REQUIRE(x && row_src && w_gate_up && w_down && topk_gate && out && ws, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: x, row_src, w_gate_up, w_down, topk_gate, out "
+          "and ws must be non-null");
+  REQUIRE(aligned16(x) && aligned16(w_gate_up) && aligned16(w_down) && aligned16(out) &&
+              aligned16(y_perm) && aligned16(act_save) && aligned16(ws),
+          LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: buffers must be 16-byte aligned");
+  REQUIRE(out != y_perm && out != x, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: out must not alias x or y_perm");
+  const size_t need = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, dtype);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE,
+          "moe_grouped_ffn_fwd_gather_combine: workspace %zu < %zu bytes", ws_bytes, need);
+  return hip_status(laep::launch_ffn_fwd_bf16(x, w_gate_up, w_down, offsets, expert_map, E,
+                                              d_model, d_ff, R, y_perm, act_save, ws,
+                                              as_stream(stream), row_src, k, topk_gate, out),
+                    "moe_grouped_ffn_fwd_gather_combine");
+}
+
 int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act_save,
                         const void* w_gate_up, const void* w_down, const int32_t* offsets,
                         const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,

@@ -189,7 +189,42 @@ __device__ __forceinline__ void fwd_epilogue(const GemmParams& p, const TileEntr
     }
     wait_lgkm0();
     __builtin_amdgcn_s_barrier();
-    flush(std::integral_constant<int, BN>{}, p.out + nt * BN, p.ldo, min(BN, p.N - nt * BN), 0);
+    const int ncols = min(BN, p.N - nt * BN);
+    if (!p.out_tok) {
+      flush(std::integral_constant<int, BN>{}, p.out + nt * BN, p.ldo, ncols, 0);
+      return;
+    }
+    // scatter: routed row r also goes to its token's row of out_tok, times its
+    // gate, with the combine's arithmetic (fp32 0 + g * y, one rounding); y
+    // rows are written too when p.out is set (the backward reads them)
+    constexpr int CPR = BN / 8, ITERS = BM * CPR / NT;
+    u32x4_t v[ITERS];
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      v[it] = *reinterpret_cast<const u32x4_t*>(smem + (c / CPR) * PITCH + (c % CPR) * 16);
+    }
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int c = it * NT + tid;
+      const int r = c / CPR, cc = c % CPR;
+      if (r < te.rows && cc * 8 < ncols) {
+        const long long row = (long long)te.row0 + r;
+        if (p.out) *reinterpret_cast<u32x4_t*>(p.out + row * p.ldo + nt * BN + cc * 8) = v[it];
+        const int src = p.row_src[row];
+        const float g = p.gate[src];
+        u32x4_t o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          float lo = 0.0f, hi = 0.0f;
+          lo += g * lo_bf16(v[it][w]);
+          hi += g * hi_bf16(v[it][w]);
+          o[w] = pack_bf16x2(lo, hi);
+        }
+        *reinterpret_cast<u32x4_t*>(p.out_tok + (long long)(src / p.slots_k) * p.ldo + nt * BN +
+                                    cc * 8) = o;
+      }
+    }
   }
 }
 
@@ -397,7 +432,8 @@ size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
 hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
-                               hipStream_t s, const int32_t* row_src, int slots_k) {
+                               hipStream_t s, const int32_t* row_src, int slots_k,
+                               const float* gate, void* out_tok) {
   bf16_t* H = static_cast<bf16_t*>(ws);
   const int nt_gu = ceil_div(f, kFwdBN / 2), nt_d = ceil_div(d, kFwdBN);
   const int max_gu = fwd_list_max(R, E, nt_gu), max_d = fwd_list_max(R, E, nt_d);
@@ -448,7 +484,9 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.out = static_cast<bf16_t*>(y_perm);
   g.ldo = d;
   g.out2 = nullptr;
-  g.row_src = nullptr;
+  g.row_src = out_tok ? row_src : nullptr;  // the scatter's token rows (A is H here)
+  g.gate = gate;
+  g.out_tok = static_cast<bf16_t*>(out_tok);
   return launch_fwd<EPI_STORE, false>(g, max_d, s);
 }
 

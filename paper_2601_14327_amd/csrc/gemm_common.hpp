@@ -35,6 +35,10 @@ struct GemmParams {
   int accumulate;
   const int32_t* row_src;  // gathered A rows: row r of the product is A row row_src[r] / slots_k
   int slots_k;
+  // gate-scaled scatter of the down product (one slot per token): routed row r
+  // also goes to out_tok row row_src[r] / slots_k, times gate[row_src[r]]
+  const float* gate;
+  bf16_t* out_tok;
   int group;               // row tiles per rasterisation group (backward products)
 };
 

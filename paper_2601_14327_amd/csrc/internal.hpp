@@ -50,11 +50,14 @@ hipError_t launch_combine_bwd(const void* dout, const void* y, const float* gate
 
 // Grouped SwiGLU FFN.
 size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
-// row_src != NULL: the gate/up A rows are gathered (row r = x_perm row row_src[r] / slots_k)
+// row_src != NULL: the gate/up A rows are gathered (row r = x_perm row row_src[r] / slots_k).
+// out_tok != NULL (one slot per token): routed row r also goes to out_tok row
+// row_src[r] / slots_k, times gate[row_src[r]]; y_perm may then be NULL.
 hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
-                               hipStream_t s, const int32_t* row_src = nullptr, int slots_k = 1);
+                               hipStream_t s, const int32_t* row_src = nullptr, int slots_k = 1,
+                               const float* gate = nullptr, void* out_tok = nullptr);
 hipError_t launch_ffn_fwd_f32(const void* x_perm, const void* w_gu, const void* w_d,
                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
                               int f, int64_t R, void* y_perm, void* act_save, void* ws,

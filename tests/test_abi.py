@@ -39,7 +39,8 @@ def test_header_declares_the_hot_path_calls():
               "moe_grouped_ffn_fwd", "moe_grouped_ffn_bwd", "moe_combine", "moe_combine_bwd",
               "moe_permute_bwd", "moe_workspace_bytes", "laep_rearrange", "laep_last_error",
               "moe_route_bwd", "laep_expert_pruning", "laep_compact_experts",
-              "laep_repack_experts"]:
+              "laep_repack_experts", "moe_grouped_ffn_fwd_gather",
+              "moe_grouped_ffn_fwd_gather_combine"]:
         assert n in names, n
 
 
@@ -124,6 +125,20 @@ def test_ffn_validation(L):
                                         p, 1 << 30, None) == 1
     assert L.moe_grouped_ffn_fwd_gather(p, None, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, p, None,
                                         p, 1 << 30, None) == 1
+    # gather + combine: one slot per token only, R <= T, out not aliasing y_perm
+    gc = L.moe_grouped_ffn_fwd_gather_combine
+    assert gc(p, p, 10, 2, p, p, p, None, p, 1, 8, 128, 128, 20, p, None, None, p, 1 << 30,
+              None) == 2
+    assert "one slot per token" in _err(L)
+    assert gc(p, p, 10, 1, p, p, p, None, p, 0, 8, 128, 128, 10, p, None, None, p, 1 << 30,
+              None) == 2
+    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 11, p, None, None, p, 1 << 30,
+              None) == 1
+    assert gc(p, p, 10, 1, p, p, p, None, None, 1, 8, 128, 128, 10, p, None, None, p, 1 << 30,
+              None) == 1
+    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 10, p, p, None, p, 1 << 30,
+              None) == 1
+    assert "alias" in _err(L)
     # x addressed with 32-bit offsets: T * d_model * 2 bytes under 2 GiB
     assert L.moe_grouped_ffn_fwd_gather(p, p, 1 << 19, 2, p, p, p, None, 1, 8, 2048, 128, 20, p,
                                         None, p, 1 << 30, None) == 2

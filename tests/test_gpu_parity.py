@@ -351,6 +351,49 @@ def test_ffn_fwd_gather_matches_permute_then_ffn(T, k, E, d, f, mapped):
     assert rownorm_err(host(a2), ract) <= TOL_BF16
 
 
+@pytest.mark.parametrize("T,E,d,f,mapped,keep_y", [
+    (300, 8, 256, 128, False, False),   # ragged tiles, an empty expert
+    (1, 3, 128, 256, False, True),      # a single token
+    (777, 12, 192, 192, True, True),    # expert_map with unused slots, f % 128 = 64
+    (2100, 40, 320, 128, False, False),  # many small experts, d % 256 = 64
+])
+def test_ffn_fwd_gather_combine_matches_three_calls(T, E, d, f, mapped, keep_y):
+    """One slot per token: the combine folded into the down projection's
+    epilogue is bit-identical to gather + FFN + combine, and matches the
+    oracle's permute + FFN + combine."""
+    rng = np.random.default_rng(T + 7 * E)
+    c = random_case(T + E + 1, T=T, d_model=d, E=E + 2 if mapped else E, k=1, d_ff=f,
+                    dtype="bf16")
+    w = np.r_[3.0, np.ones(E - 2), 0.0]
+    ids = rng.choice(E, size=(T, 1), p=w / w.sum())
+    gates = rng.uniform(0.05, 1.0, size=(T, 1)).astype(np.float32)
+    bf = torch.bfloat16
+    x, wgu, wd = dev(c["x"], bf), dev(c["w_gate_up"], bf), dev(c["w_down"], bf)
+    emap = dev(np.array([e + 2 for e in range(E)], np.int32), torch.int32) if mapped else None
+    idx = dev(ids.astype(np.int32), torch.int32)
+    g = dev(gates, torch.float32)
+    case(f"ffn fwd gather+combine T={T} E={E} d={d} f={f} mapped={mapped} keep_y={keep_y}")
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+    y1, a1 = laep.moe_grouped_ffn_fwd_gather(x, row_src, 1, wgu, wd, offsets, expert_map=emap,
+                                            save_act=True)
+    out1 = laep.moe_combine(y1, g, dest_row)
+    out2, y2, a2 = laep.moe_grouped_ffn_fwd_gather_combine(
+        x, row_src, g, wgu, wd, offsets, expert_map=emap, keep_y=keep_y, save_act=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out1, out2)
+    assert torch.equal(a1, a2)
+    if keep_y:
+        assert torch.equal(y1, y2)
+    else:
+        assert y2 is None
+    rc, ro, rd = om.expert_counts(ids, E)
+    xp = om.permute(c["x"], rd, 1)
+    ry, _ = om.grouped_ffn_fwd(xp, c["w_gate_up"], c["w_down"], ro,
+                               expert_map=host(emap) if mapped else None, dtype="bf16")
+    rout = om.combine(ry, gates, rd, 1)
+    assert rownorm_err(host(out2), rout) <= TOL_BF16
+
+
 @pytest.mark.parametrize("counts,d,f", [
     ([60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
     ([300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),
@@ -486,6 +529,9 @@ def test_layer_fuzz(seed):
     out = laep.moe_combine(y, gate, dest)
     if dtype == "bf16":   # the dispatch folded into the operand loads gives the same bits
         yg, _ = laep.moe_grouped_ffn_fwd_gather(x, row_src, k, wgu, wd, offsets, rows=T * k)
+    if dtype == "bf16" and k == 1:   # and so does the combine folded into the epilogue
+        og, _, _ = laep.moe_grouped_ffn_fwd_gather_combine(
+            x, row_src, gate, wgu, wd, offsets, rows=T, out=torch.zeros_like(out))
     torch.cuda.synchronize()
     ridx, rgate, _, rlog = om.route(c["x"], c["w_router"], k, bias=bias, alive=alive,
                                    renorm=renorm)
@@ -502,6 +548,8 @@ def test_layer_fuzz(seed):
     assert rownorm_err(host(out), rout) <= tol
     if dtype == "bf16":
         assert torch.equal(yg, y)
+    if dtype == "bf16" and k == 1:
+        assert torch.equal(og, out)
 
 
 def test_determinism():
