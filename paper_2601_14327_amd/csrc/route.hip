@@ -4,7 +4,9 @@
 //  1. logits[32 x EP] = x_tile . W_r^T on the matrix cores.  The reduction
 //     dimension is split over the 8 waves; each wave holds a 32 x 32 fp32
 //     block per 32 experts.  The eight partial blocks are summed through LDS
-//     in wave order, so the result is deterministic.
+//     in a fixed order, so the result is deterministic: in one round (all
+//     eight blocks staged, each thread summing its elements over the waves)
+//     where the stage buffers hold them, else as a tree.
 //     bf16 with up to 128 experts: x and W_r go through LDS in chunks of 256
 //     (or 128) columns by LDS-DMA, 3-4 stages deep, so every global request
 //     is a whole 128-byte line (in the MFMA operand layout a direct load
@@ -107,10 +109,10 @@ template <int CTRL>
 __device__ __forceinline__ void argmax_step(float& bv, int& be) {
   const float ov = dpp_f<CTRL>(bv);
   const int oe = dpp_i<CTRL>(be);
-  if (ov > bv || (ov == bv && oe < be)) {
-    bv = ov;
-    be = oe;
-  }
+  // bitwise, so the compiler keeps it a select rather than branches
+  const bool take = (ov > bv) | ((ov == bv) & (oe < be));
+  bv = take ? ov : bv;
+  be = take ? oe : be;
 }
 
 template <int NCH>
@@ -251,7 +253,30 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     t = (r >> 2) * 8 + kh * 4 + (r & 3);
     e = nb * 32 + row;
   };
-  if constexpr (KC > 0) {
+  constexpr bool kOneRound = KC > 0 && kRouteWaves * 32 * EP * 4 <= StageBytes<NB, KC>::value;
+  if constexpr (kOneRound) {
+    // every wave's partial block to the idle stage buffers, then each thread
+    // sums its elements over the waves in wave order and adds the bias
+    float* part = reinterpret_cast<float*>(s_stage);
+    constexpr int SL = 32 * EP;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int t, e;
+        tile_at(nb, r, t, e);
+        part[wave * SL + t * EP + e] = acc[nb][r];
+      }
+    __syncthreads();
+    for (int i = tid * 4; i < SL; i += kRouteThreads * 4) {
+      f32x4_t sum = *reinterpret_cast<const f32x4_t*>(part + i);
+#pragma unroll
+      for (int wv = 1; wv < kRouteWaves; ++wv) sum += *reinterpret_cast<const f32x4_t*>(part + wv * SL + i);
+      const int t = i / EP, e = i % EP;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s_log[t * LD + e + q] = sum[q] + s_bias[e + q];
+    }
+  } else if constexpr (KC > 0) {
     // a tree over the waves (8 -> 4 -> 2 -> 1) through the idle stage buffers
     static_assert(4 * 32 * EP * 4 <= StageBytes<NB, KC>::value, "partials must fit the stages");
     float* part = reinterpret_cast<float*>(s_stage);
@@ -290,6 +315,11 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
           s_log[t * LD + e] = acc[nb][r];
         }
     }
+    __syncthreads();
+    for (int i = tid; i < kRouteTokens * EP; i += kRouteThreads) {
+      const int t = i / EP, e = i % EP;
+      s_log[t * LD + e] += s_bias[e];
+    }
   } else {
     for (int wv = 0; wv < kRouteWaves; ++wv) {
       __syncthreads();
@@ -305,15 +335,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
           }
       }
     }
+    __syncthreads();
+    for (int i = tid; i < kRouteTokens * EP; i += kRouteThreads) {
+      const int t = i / EP, e = i % EP;
+      s_log[t * LD + e] += s_bias[e];
+    }
   }
   __syncthreads();
 
-  // bias, optional logits output
-  for (int i = tid; i < kRouteTokens * EP; i += kRouteThreads) {
-    const int t = i / EP, e = i % EP;
-    s_log[t * LD + e] += s_bias[e];
-  }
-  __syncthreads();
   if (logits_out != nullptr) {
     for (int i = tid; i < kRouteTokens * E; i += kRouteThreads) {
       const int t = i / E, e = i % E;
