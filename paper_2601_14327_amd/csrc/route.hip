@@ -191,8 +191,12 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     // end the last chunk is loaded again into the free stage (never read), so
     // one constant vmcnt serves every wait.
     constexpr int NS = St::NS;
+    // Workgroups on one XCD (block i runs on XCD i % 8) start at different
+    // chunks, so they do not all request the same W_r lines at once.
+    const int rot = (int)((blockIdx.x >> 3) % n_chunks);
     auto issue = [&](int c) {
-      const int cc = c < n_chunks ? c : n_chunks - 1;
+      const int cl = c < n_chunks ? c : n_chunks - 1;
+      const int cc = cl + rot < n_chunks ? cl + rot : cl + rot - n_chunks;
       route_dma<St::NCH>(s_stage + (c % NS) * St::BYTES, src, cc * KC, wave);
     };
 #pragma unroll
