@@ -7,9 +7,9 @@ accumulation.  One step = one forward pass of the whole layer:
 route + expert counts (one call) -> dispatch + grouped SwiGLU FFN (one call, the
 dispatch folded into the FFN's operand loads) -> combine, every call a kernel
 of the C-ABI library; three input sets rotate over the steps so the
-activations are not cache-resident.  With one slot per token (shard) the
-combine folds into the FFN call as well (the down projection writes each row,
-times its gate, to its token row).  Training steps (shard_bwd) keep the
+activations are not cache-resident.  With one slot per token (shard,
+shard_bwd) the combine folds into the FFN call as well (the down projection
+writes each row, times its gate, to its token row).  Training steps keep the
 separate permute, because the weight gradient reads x_perm.
 
 Prints ONE JSON line:
@@ -230,9 +230,12 @@ class Setup:
                                                            row_src=p.row_src))]
             gate = self.gate
         if p.fused_combine:   # one slot per token: dispatch and combine folded into the FFN
+            if p.x_perm is not None:   # training: the weight gradient reads x_perm
+                out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm))]
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather_combine(
                 x, p.row_src, gate, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
-                out=p.out, save_act=p.act_save is not None, act_save=p.act_save))]
+                out=p.out, keep_y=p.y_perm is not None, y_perm=p.y_perm,
+                save_act=p.act_save is not None, act_save=p.act_save))]
         elif p.fused:   # dispatch folded into the FFN's operand loads
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather(
                 x, p.row_src, w.k, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,

@@ -9,9 +9,10 @@ Forward (given routing, one device's expert shard with k = 1):
 With fused dispatch (bf16 forward-only plans, the default there),
 moe_permute + moe_grouped_ffn_fwd become one moe_grouped_ffn_fwd_gather
 call that reads the token rows through row_src; x_perm is never written.
-With one slot per token (k = 1) the combine folds in as well
+With one slot per token (k = 1, bf16) the combine folds in as well
 (moe_grouped_ffn_fwd_gather_combine): the down projection writes each row,
-times its gate, to its token row, and y_perm is never written.
+times its gate, to its token row; y_perm is written only for a backward pass,
+whose plans also keep moe_permute (the weight gradient reads x_perm).
 Backward:
     moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
       [-> moe_route_bwd, accumulating the router's dx]   (router path)
@@ -62,9 +63,10 @@ class MoELayerPlan:
         # router backward sums dW_r over it
         self.row_src = (torch.empty(R, dtype=i32, device=dev) if self.fused or backward
                         else None)
-        # one slot per token: the combine folds into the down projection's epilogue
-        self.fused_combine = self.fused and k == 1
-        self.y_perm = (None if self.fused_combine else
+        # one slot per token (bf16): the combine folds into the down projection's
+        # epilogue; y_perm is then written only for the backward (combine_bwd)
+        self.fused_combine = k == 1 and dtype == torch.bfloat16 and (self.fused or backward)
+        self.y_perm = (None if self.fused_combine and not backward else
                        torch.empty((R, d_model), dtype=dtype, device=dev))
         self.act_save = (torch.empty((R, 2 * d_ff), dtype=dtype, device=dev) if save_act
                          else None)
@@ -112,9 +114,12 @@ class MoELayerPlan:
 
     def experts_and_combine(self, x, w_gate_up, w_down, expert_map=None):
         if self.fused_combine:
+            if self.x_perm is not None:   # the weight gradient reads x_perm
+                api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
             api.moe_grouped_ffn_fwd_gather_combine(
                 x, self.row_src, self.topk_gate, w_gate_up, w_down, self.offsets, rows=self.R,
                 expert_map=expert_map, ws=self.ws_ffn, out=self.out,
+                keep_y=self.y_perm is not None, y_perm=self.y_perm,
                 save_act=self.act_save is not None, act_save=self.act_save)
             return self.out
         if self.fused:

@@ -157,10 +157,14 @@ def test_shard_forward_full_size():
 def test_shard_backward_full_size():
     w, c, plan, x, wgu, wd, idx, gate = _shard_plan("shard_bwd", backward=True)
     case("full-size expert shard forward + backward")
-    plan.forward_given_routing(x, idx, gate, wgu, wd)
+    out_fwd = plan.forward_given_routing(x, idx, gate, wgu, wd).clone()
+    # k = 1: the combine is folded into the FFN call; it must equal moe_combine
+    assert plan.fused_combine and plan.y_perm is not None
+    ref_out = laep.moe_combine(plan.y_perm, plan.topk_gate, plan.dest_row)
     dout = dev(c["dout"], BF)
     plan.backward(dout, wgu, wd)
     torch.cuda.synchronize()
+    assert torch.equal(out_fwd, ref_out)
     R, d, f = w.T, w.d_model, w.d_ff
     offsets = hint(plan.offsets).astype(np.int64)
     dest = hint(plan.dest_row)
