@@ -263,8 +263,9 @@ int moe_route_bwd(const float* dgate, const int32_t* topk_idx,
                   void* ws, size_t ws_bytes, void* stream);
 
 /*
- * moe_permute -- dispatch: x_perm[dest_row[t*k + j]] = x[t] (a copy; slots
- * with dest_row == -1 are skipped).
+ * moe_permute -- dispatch (under expert parallelism, Section 3.3, the rows
+ * sent to each expert's device): x_perm[dest_row[t*k + j]] = x[t] (a copy;
+ * slots with dest_row == -1 are skipped).
  *   x device [T, d_model] dtype; dest_row device [T * k] int32;
  *   x_perm device [rows, d_model] dtype, rows = number of routed slots.
  *   d_model % 8 == 0.
@@ -326,7 +327,7 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
 /*
  * moe_grouped_ffn_fwd_gather_combine -- moe_grouped_ffn_fwd_gather followed
  * by moe_combine, for one slot per token (k = 1: an expert-parallel rank's
- * local rows, each returned to its sender scaled by its gate).  The down
+ * local rows, Section 3.3, each returned to its sender scaled by its gate).  The down
  * projection's epilogue writes each routed row r straight to its token row:
  *   out[t] = round(topk_gate[t] * y_r)   with t = row_src[r] (k = 1),
  * where y_r is the rounded FFN output row, in the combine's arithmetic, so
@@ -383,7 +384,8 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
 size_t laep_ws_hb_offset(int64_t R, int d_ff, int dtype);
 
 /*
- * moe_combine -- gate-weighted combine (return path of the dispatch):
+ * moe_combine -- gate-weighted combine (return path of the dispatch,
+ * Section 3.3):
  *   out[t] = round(sum_j topk_gate[t, j] * y_perm[dest_row[t*k + j]])
  *   (fp32 accumulation in slot order; slots with dest_row == -1 skipped).
  *   y_perm device [rows, d_model]; topk_gate device [T, k] fp32;
