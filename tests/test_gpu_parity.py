@@ -170,6 +170,28 @@ def test_counts_two_level_scan(T, E, k):
     np.testing.assert_array_equal(host(etn), rc + 7)
 
 
+@pytest.mark.parametrize("T,E,k", [(16384, 64, 8), (16385, 64, 8), (4096, 256, 8),
+                                   (4097, 256, 8), (9000, 3, 2), (130, 256, 1)])
+def test_counts_mid_sizes(T, E, k):
+    """Mid sizes around 16384 (wave tile, expert) pairs, up to 256 experts and
+    down to 3, with unrouted slots."""
+    rng = np.random.default_rng(T * 7 + E)
+    idx = np.argsort(rng.random((T, E)), axis=1)[:, :k].astype(np.int32)
+    idx[rng.random(T) < 0.02, -1] = -1
+    case(f"counts mid sizes T={T} E={E} k={k}")
+    etn = torch.full((E,), 3, dtype=torch.int64, device="cuda")
+    counts, offsets, dest, row_src = laep.moe_expert_counts(
+        dev(idx, torch.int32), E, want_row_src=True, etn_accum=etn)
+    torch.cuda.synchronize()
+    rc, ro, rd = om.expert_counts(idx, E)
+    np.testing.assert_array_equal(host(counts), rc)
+    np.testing.assert_array_equal(host(offsets), ro)
+    np.testing.assert_array_equal(host(dest), rd)
+    routed = rd >= 0
+    np.testing.assert_array_equal(host(row_src)[rd[routed]], np.nonzero(routed)[0])
+    np.testing.assert_array_equal(host(etn), rc + 3)
+
+
 def test_counts_skew_unrouted_and_empty_experts():
     rng = np.random.default_rng(3)
     T, E, k = 3000, 32, 4
