@@ -371,6 +371,10 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  *   On return the workspace holds dA [R, 2*d_ff] (dtype) at byte offset 0 and
  *   H_b [R, d_ff] (dtype) at byte offset laep_ws_hb_offset(R, d_ff, dtype).
  *   Only LAEP_BF16 is supported.
+ *   Streams: the weight gradients run on a library-owned side stream of the
+ *   current device (created on the first call, default priority), forked
+ *   from `stream` after the SwiGLU backward and joined back with events, so
+ *   the call is ordered on `stream` as a whole and may be graph-captured.
  */
 int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
                         const void* act_save, const void* w_gate_up,
