@@ -257,6 +257,7 @@ class Setup:
                                                               dgate=p.dgate)),
                     ("ffn_bwd", lambda: L.moe_grouped_ffn_bwd(
                         p.dy_perm, p.x_perm, p.act_save, self.wgu, self.wd, p.offsets,
+                        h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
                         dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,
                         dx_perm=p.dx_perm)),
                     ("permute_bwd", lambda: L.moe_permute_bwd(p.dx_perm, p.dest_row, w.T, w.k,

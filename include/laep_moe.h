@@ -294,7 +294,8 @@ int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T,
  *   expert's w_gate_up under 2 GiB (4*d_ff*d_model bytes), since the GEMMs
  *   address it with 32-bit offsets (LAEP_ERR_UNSUPPORTED otherwise).
  *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff)
- *   (holds H and the tile table).
+ *   (holds H and the tile table; on return H [R, d_ff] (dtype) is at byte
+ *   offset 0, which moe_grouped_ffn_bwd can take as h_fwd).
  */
 int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
                         const void* w_down, const int32_t* offsets,
@@ -360,28 +361,36 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  *   dA_u = dH * silu(Â_g)                      dA = round([dA_g, dA_u])
  *   H_b  = round(silu(Â_g) * Â_u)
  *   dX   = round(dA W_gu[p])                   -> dx_perm
- *   dW_gu[p] (+)= dA^T X,   dW_d[p] (+)= dY^T H_b   (fp32; `accumulate` adds)
+ *   dW_gu[p] (+)= dA^T X,   dW_d[p] (+)= dY^T H   (fp32; `accumulate` adds)
+ *   where H is h_fwd, the H the forward computed and the down projection
+ *   consumed (exact), or when h_fwd is NULL H_b recomputed at Â.
  *   Slots p of experts without rows get zero gradient (or keep their value
  *   when accumulating).
  *
  *   dy_perm, x_perm device [R, d_model]; act_save device [R, 2*d_ff];
- *   dx_perm device [R, d_model]; dw_gate_up device fp32 [E_phys, 2*d_ff, d_model];
+ *   h_fwd device [R, d_ff] or NULL (moe_grouped_ffn_fwd leaves H in its
+ *   workspace at byte offset 0); dx_perm device [R, d_model];
+ *   dw_gate_up device fp32 [E_phys, 2*d_ff, d_model];
  *   dw_down device fp32 [E_phys, d_model, d_ff].
  *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d_model, d_ff).
- *   On return the workspace holds dA [R, 2*d_ff] (dtype) at byte offset 0 and
- *   H_b [R, d_ff] (dtype) at byte offset laep_ws_hb_offset(R, d_ff, dtype).
+ *   On return the workspace holds dA [R, 2*d_ff] (dtype) at byte offset 0 and,
+ *   at byte offset laep_ws_hb_offset(R, d_ff, dtype), H_b [R, d_ff] (dtype)
+ *   when h_fwd is NULL, else dH.
  *   Only LAEP_BF16 is supported.
  *   Streams: the weight gradients run on a library-owned side stream of the
  *   current device (created on the first call, default priority), forked
- *   from `stream` after the SwiGLU backward and joined back with events, so
- *   the call is ordered on `stream` as a whole and may be graph-captured.
+ *   from `stream` (dW_d at the start when h_fwd is given, so it overlaps the
+ *   first data gradient; otherwise after the SwiGLU backward) and joined back
+ *   with events, so the call is ordered on `stream` as a whole and may be
+ *   graph-captured.
  */
 int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
-                        const void* act_save, const void* w_gate_up,
-                        const void* w_down, const int32_t* offsets,
-                        const int32_t* expert_map, int dtype, int E,
-                        int d_model, int d_ff, int64_t R, void* dx_perm,
-                        float* dw_gate_up, float* dw_down, int accumulate,
+                        const void* act_save, const void* h_fwd,
+                        const void* w_gate_up, const void* w_down,
+                        const int32_t* offsets, const int32_t* expert_map,
+                        int dtype, int E, int d_model, int d_ff, int64_t R,
+                        void* dx_perm, float* dw_gate_up, float* dw_down,
+                        int accumulate,
                         void* ws, size_t ws_bytes, void* stream);
 
 /* Byte offset of H_b inside the moe_grouped_ffn_bwd workspace. */

@@ -210,15 +210,17 @@ def expert_ffn(x_rows, w_gu, w_d, dtype: str):
 
 
 def grouped_ffn_fwd(x_perm, w_gate_up, w_down, offsets, expert_map=None,
-                    dtype: str = "bf16"):
+                    dtype: str = "bf16", return_h: bool = False):
     """Per expert e with rows [offsets[e], offsets[e+1]): the SwiGLU FFN
     with that expert's weights (physical slot expert_map[e]).
-    Returns (y_perm, act_save)."""
+    Returns (y_perm, act_save), and H (the rounded activation the down
+    projection consumes) when ``return_h``."""
     x_perm = np.asarray(x_perm)
     R, d = x_perm.shape
     f = w_down.shape[2]
     y = np.zeros((R, d), F64)
     act = np.zeros((R, 2 * f), F64)
+    h = np.zeros((R, f), F64)
     E = len(offsets) - 1
     for e in range(E):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
@@ -227,9 +229,9 @@ def grouped_ffn_fwd(x_perm, w_gate_up, w_down, offsets, expert_map=None,
         p = _phys(expert_map, e)
         if p < 0:
             raise ValueError(f"expert {e} has rows but no weight slot")
-        y[lo:hi], act[lo:hi], _ = expert_ffn(x_perm[lo:hi], w_gate_up[p],
-                                             w_down[p], dtype)
-    return y, act
+        y[lo:hi], act[lo:hi], h[lo:hi] = expert_ffn(x_perm[lo:hi], w_gate_up[p],
+                                                    w_down[p], dtype)
+    return (y, act, h) if return_h else (y, act)
 
 
 def combine(y_perm, gate, dest_row, k: int, dtype: str = "bf16"):
@@ -330,7 +332,9 @@ def grouped_ffn_dgrad(dy_perm, act_save, w_gate_up, w_down, offsets,
 def grouped_ffn_wgrad(dy_perm, x_perm, dA, Hb, offsets, n_phys: int,
                       expert_map=None, out_f32: bool = True):
     """Weight gradients (float32): per expert with rows,
-    dW_gu = dA^T X and dW_d = dY^T H_b over the expert's rows.
+    dW_gu = dA^T X and dW_d = dY^T H over the expert's rows, where ``Hb`` is
+    the H to use: the forward's (the activation the down projection
+    consumed) or H_b recomputed at the saved pre-activations.
     Weight slots that receive no rows get zero gradient."""
     R, d = x_perm.shape
     f = Hb.shape[1]

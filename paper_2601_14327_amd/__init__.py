@@ -20,9 +20,11 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     laep_rearrange       host utility: balanced expert placement
     laep_calib_copy, laep_calib_mfma   measurement kernels (attained peaks)
 """
-from ._lib import LAEP_BF16, LAEP_F32, LaepError, LIB_PATH, lib  # noqa: F401
+from ._lib import (  # noqa: F401
+    LAEP_BF16, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD, LAEP_F32, LaepError, LIB_PATH, lib)
 from .api import (  # noqa: F401
     ffn_bwd_ws_views,
+    ffn_fwd_h_view,
     laep_calib_copy,
     laep_calib_mfma,
     laep_compact_experts,

@@ -340,12 +340,16 @@ def moe_grouped_ffn_fwd_gather_combine(x: torch.Tensor, row_src: torch.Tensor,
 
 
 def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *,
-                        expert_map=None, dw_gate_up=None, dw_down=None, accumulate=False,
-                        ws=None, dx_perm=None, return_ws: bool = False):
-    """Backward of the grouped FFN.  Returns (dx_perm, dw_gate_up, dw_down[, ws])."""
+                        h_fwd=None, expert_map=None, dw_gate_up=None, dw_down=None,
+                        accumulate=False, ws=None, dx_perm=None, return_ws: bool = False):
+    """Backward of the grouped FFN.  ``h_fwd``: the forward's H [R, f] (see
+    ffn_fwd_h_view); dW_d then uses it, else H_b recomputed at act_save.
+    Returns (dx_perm, dw_gate_up, dw_down[, ws])."""
     for t, n in ((dy_perm, "dy_perm"), (x_perm, "x_perm"), (act_save, "act_save"),
                  (w_gate_up, "w_gate_up"), (w_down, "w_down"), (offsets, "offsets")):
         _dev(t, n)
+    if h_fwd is not None:
+        _dev(h_fwd, "h_fwd")
     R, d = x_perm.shape
     f = w_down.shape[2]
     E = offsets.shape[0] - 1
@@ -356,7 +360,7 @@ def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *
     if dw_down is None:
         dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=dev)
     ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d, f), dev)
-    check(lib().moe_grouped_ffn_bwd(_ptr(dy_perm), _ptr(x_perm), _ptr(act_save),
+    check(lib().moe_grouped_ffn_bwd(_ptr(dy_perm), _ptr(x_perm), _ptr(act_save), _ptr(h_fwd),
                                     _ptr(w_gate_up), _ptr(w_down), _ptr(offsets),
                                     _ptr(expert_map), _dtype_code(x_perm), E, d, f, R,
                                     _ptr(dx_perm), _ptr(dw_gate_up), _ptr(dw_down),
@@ -365,8 +369,15 @@ def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *
     return out + (ws,) if return_ws else out
 
 
+def ffn_fwd_h_view(ws: torch.Tensor, R: int, d_ff: int, dtype: torch.dtype):
+    """H [R, f] as the forward leaves it in its workspace (byte offset 0)."""
+    esz = torch.empty((), dtype=dtype).element_size()
+    return ws.view(torch.uint8)[: R * d_ff * esz].view(dtype).view(R, d_ff)
+
+
 def ffn_bwd_ws_views(ws: torch.Tensor, R: int, d_ff: int, dtype: torch.dtype):
-    """dA [R, 2f] and H_b [R, f] as left in the backward workspace."""
+    """dA [R, 2f] and the H_b buffer [R, f] (H_b, or dH when the backward
+    used the forward's H) as left in the backward workspace."""
     code = _DT[dtype]
     esz = torch.empty((), dtype=dtype).element_size()
     off = int(lib().laep_ws_hb_offset(R, d_ff, code))

@@ -423,7 +423,8 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src, in
 }
 
 int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act_save,
-                        const void* w_gate_up, const void* w_down, const int32_t* offsets,
+                        const void* h_fwd, const void* w_gate_up, const void* w_down,
+                        const int32_t* offsets,
                         const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
                         int64_t R, void* dx_perm, float* dw_gate_up, float* dw_down,
                         int accumulate, void* ws, size_t ws_bytes, void* stream) {
@@ -435,14 +436,14 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act
           "moe_grouped_ffn_bwd: offsets, dw_gate_up, dw_down and ws must be non-null");
   REQUIRE(R == 0 || (dy_perm && x_perm && act_save && w_gate_up && w_down && dx_perm),
           LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd: activation pointers must be non-null");
-  REQUIRE(aligned16(dy_perm) && aligned16(x_perm) && aligned16(act_save) &&
+  REQUIRE(aligned16(dy_perm) && aligned16(x_perm) && aligned16(act_save) && aligned16(h_fwd) &&
               aligned16(w_gate_up) && aligned16(w_down) && aligned16(dx_perm) &&
               aligned16(dw_gate_up) && aligned16(dw_down) && aligned16(ws),
           LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd: buffers must be 16-byte aligned");
   const size_t need = laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, dtype);
   REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_grouped_ffn_bwd: workspace %zu < %zu bytes",
           ws_bytes, need);
-  return hip_status(laep::launch_ffn_bwd_bf16(dy_perm, x_perm, act_save, w_gate_up, w_down,
+  return hip_status(laep::launch_ffn_bwd_bf16(dy_perm, x_perm, act_save, h_fwd, w_gate_up, w_down,
                                               offsets, expert_map, E, d_model, d_ff, R, dx_perm,
                                               dw_gate_up, dw_down, accumulate != 0, ws,
                                               as_stream(stream)),

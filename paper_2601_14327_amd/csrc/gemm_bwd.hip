@@ -407,12 +407,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
 // SwiGLU backward at the saved pre-activations, one 8-column vector of one
 // routed row per thread: with s = sigmoid(A_g),
 //   dA_g = dH A_u s (1 + A_g (1 - s)),  dA_u = dH silu(A_g),  H_b = silu(A_g) A_u.
-// dH arrives in the H_b buffer and is replaced there.  Streaming accesses:
-// every element is read and written once.
+// dH arrives in the H_b buffer and is replaced there by H_b (write_h), or left
+// (the weight gradient then uses the forward's H).  Streaming accesses: every
+// element is read and written once.
 __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restrict__ act,
                                                          int64_t R, int f,
                                                          u32x4_t* __restrict__ dA,
-                                                         u32x4_t* __restrict__ hb) {
+                                                         u32x4_t* __restrict__ hb, int write_h) {
   const int vpr = f / 8;  // vectors per row of dH / H_b
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= R * vpr) return;
@@ -442,7 +443,7 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restri
   }
   st_stream(dA + r * 2 * vpr + v, og);
   st_stream(dA + r * 2 * vpr + vpr + v, ou);
-  st_stream(hb + i, oh);
+  if (write_h) st_stream(hb + i, oh);
 }
 
 constexpr int kBwdBM = 256, kBwdBN = 256;
@@ -501,10 +502,10 @@ size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
 }
 
 hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
-                               const void* w_gu, const void* w_d, const int32_t* offsets,
-                               const int32_t* expert_map, int E, int d, int f, int64_t R,
-                               void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
-                               void* ws, hipStream_t s) {
+                               const void* h_fwd, const void* w_gu, const void* w_d,
+                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
+                               int f, int64_t R, void* dx_perm, float* dw_gu, float* dw_d,
+                               int accumulate, void* ws, hipStream_t s) {
   char* base = static_cast<char*>(ws);
   bf16_t* dA = reinterpret_cast<bf16_t*>(base);
   bf16_t* Hb = reinterpret_cast<bf16_t*>(base + ffn_bwd_hb_offset(R, f, kDtypeBf16));
@@ -517,8 +518,54 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
                      E, kBwdBM, 1, E, te.n_entries, te.table);
 
-  // dgrad 1: dH = dY W_d (bf16, into the H_b buffer), then the SwiGLU backward -> dA, H_b
   const int group = tile_group("LAEP_TILE_GROUP_BWD", 8);
+  // weight gradients: dW_d[p] [d, f] = dY^T H over the expert's rows (H: the
+  // forward's when given, else H_b), dW_gu[p] [2f, d] = dA^T X
+  GemmParams wd = {};
+  wd.group = group;
+  wd.table = te.table;
+  wd.n_entries = te.n_entries;
+  wd.f = f;
+  wd.A = static_cast<const bf16_t*>(dy);
+  wd.lda = d;
+  wd.B = h_fwd ? static_cast<const bf16_t*>(h_fwd) : Hb;
+  wd.ldb = f;
+  wd.Mw = d;
+  wd.N = f;
+  wd.n_tiles_n = ceil_div(f, kBwdBN);
+  wd.tiles_per_entry = ceil_div(d, kBwdBM) * wd.n_tiles_n;
+  wd.wout = dw_d;
+  wd.strideW = (long long)d * f;
+  wd.accumulate = accumulate;
+  GemmParams wg = wd;
+  wg.A = dA;
+  wg.lda = 2 * f;
+  wg.B = static_cast<const bf16_t*>(x_perm);
+  wg.ldb = d;
+  wg.Mw = 2 * f;
+  wg.N = d;
+  wg.n_tiles_n = ceil_div(d, kBwdBN);
+  wg.tiles_per_entry = ceil_div(2 * f, kBwdBM) * wg.n_tiles_n;
+  wg.wout = dw_gu;
+  wg.strideW = (long long)2 * f * d;
+
+  // The weight gradients run on the side stream, concurrently with the data
+  // gradients: dW_d from the start when it uses the forward's H, else after
+  // the SwiGLU backward like dW_gu; joined back (also after an error) before
+  // the call returns.
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  SideStream* side = nullptr;
+  hipError_t err = side_stream_locked(side);
+  if (err != hipSuccess) return err;
+  const hipStream_t s2 = side->stream;
+  auto fork = [&]() -> hipError_t {
+    hipError_t e = hipEventRecord(side->fork, s);
+    return e == hipSuccess ? hipStreamWaitEvent(s2, side->fork, 0) : e;
+  };
+  if ((err = fork()) != hipSuccess) return err;
+  if (h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
+
+  // dgrad 1: dH = dY W_d (bf16, into the H_b buffer), then the SwiGLU backward -> dA (, H_b)
   GemmParams g = {};
   g.group = group;
   g.table = tr.table;
@@ -535,15 +582,19 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.tiles_per_entry = g.n_tiles_n;
   g.out = Hb;
   g.ldo = f;
-  hipError_t err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
-  if (err != hipSuccess) return err;
-  if (R > 0) {
+  if (err == hipSuccess) err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
+  if (err == hipSuccess && R > 0) {
     const long long n_vec = R * (long long)(f / 8);
     hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n_vec + 255) / 256)), dim3(256), 0, s,
                        static_cast<const u32x4_t*>(act_save), (int64_t)R, f,
-                       reinterpret_cast<u32x4_t*>(dA), reinterpret_cast<u32x4_t*>(Hb));
-    if ((err = hipGetLastError()) != hipSuccess) return err;
+                       reinterpret_cast<u32x4_t*>(dA), reinterpret_cast<u32x4_t*>(Hb),
+                       h_fwd ? 0 : 1);
+    err = hipGetLastError();
   }
+  // dA (and H_b) ready: the remaining weight gradients on the side stream
+  if (err == hipSuccess) err = fork();
+  if (err == hipSuccess && !h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
+  if (err == hipSuccess) err = launch_bwd<EPI_WGRAD, true>(wg, E * wg.tiles_per_entry, s2);
 
   // dgrad 2: dX = dA W_gu
   g.A = dA;
@@ -557,49 +608,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.tiles_per_entry = g.n_tiles_n;
   g.out = static_cast<bf16_t*>(dx_perm);
   g.ldo = d;
-  g.out2 = nullptr;
-  g.aux = nullptr;
-  // the weight gradients go to the side stream, forked after the SwiGLU
-  // backward and joined back (also after an error) before the call returns
-  std::lock_guard<std::mutex> lock(g_side_mu);
-  SideStream* side = nullptr;
-  if ((err = side_stream_locked(side)) != hipSuccess) return err;
-  if ((err = hipEventRecord(side->fork, s)) != hipSuccess) return err;
-  if ((err = hipStreamWaitEvent(side->stream, side->fork, 0)) != hipSuccess) return err;
-  const hipStream_t s2 = side->stream;
-  err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
-
-  // wgrad W_d: dW_d[p] [d, f] = dY^T H_b over the expert's rows
-  GemmParams w = {};
-  w.group = group;
-  w.table = te.table;
-  w.n_entries = te.n_entries;
-  w.f = f;
-  w.A = static_cast<const bf16_t*>(dy);
-  w.lda = d;
-  w.B = Hb;
-  w.ldb = f;
-  w.Mw = d;
-  w.N = f;
-  w.n_tiles_n = ceil_div(f, kBwdBN);
-  w.tiles_per_entry = ceil_div(d, kBwdBM) * w.n_tiles_n;
-  w.wout = dw_d;
-  w.strideW = (long long)d * f;
-  w.accumulate = accumulate;
-  if (err == hipSuccess) err = launch_bwd<EPI_WGRAD, true>(w, E * w.tiles_per_entry, s2);
-
-  // wgrad W_gu: dW_gu[p] [2f, d] = dA^T X
-  w.A = dA;
-  w.lda = 2 * f;
-  w.B = static_cast<const bf16_t*>(x_perm);
-  w.ldb = d;
-  w.Mw = 2 * f;
-  w.N = d;
-  w.n_tiles_n = ceil_div(d, kBwdBN);
-  w.tiles_per_entry = ceil_div(2 * f, kBwdBM) * w.n_tiles_n;
-  w.wout = dw_gu;
-  w.strideW = (long long)2 * f * d;
-  if (err == hipSuccess) err = launch_bwd<EPI_WGRAD, true>(w, E * w.tiles_per_entry, s2);
+  if (err == hipSuccess) err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
   hipError_t jerr = hipEventRecord(side->join, s2);
   if (jerr == hipSuccess) jerr = hipStreamWaitEvent(s, side->join, 0);
   return err != hipSuccess ? err : jerr;

@@ -65,8 +65,11 @@ hipError_t launch_ffn_fwd_f32(const void* x_perm, const void* w_gu, const void* 
 
 size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
 size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype);
+// h_fwd != NULL: dW_d uses the forward's H (and starts beside data-gradient 1);
+// else H_b, recomputed at the saved pre-activations
 hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
-                               const void* w_gu, const void* w_d, const int32_t* offsets,
+                               const void* h_fwd, const void* w_gu, const void* w_d,
+                               const int32_t* offsets,
                                const int32_t* expert_map, int E, int d, int f, int64_t R,
                                void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
                                void* ws, hipStream_t s);

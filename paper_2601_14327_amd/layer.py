@@ -173,8 +173,11 @@ class MoELayerPlan:
             self.dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32,
                                           device=self.device)
             self.dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=self.device)
+        # dW_d from the H the forward computed (left in its workspace)
+        h_fwd = api.ffn_fwd_h_view(self.ws_ffn, self.R, self.f, self.dtype)
         api.moe_grouped_ffn_bwd(self.dy_perm, self.x_perm, self.act_save, w_gate_up, w_down,
-                                self.offsets, expert_map=expert_map, dw_gate_up=self.dw_gate_up,
+                                self.offsets, h_fwd=h_fwd, expert_map=expert_map,
+                                dw_gate_up=self.dw_gate_up,
                                 dw_down=self.dw_down, accumulate=accumulate, ws=self.ws_bwd,
                                 dx_perm=self.dx_perm)
         api.moe_permute_bwd(self.dx_perm, self.dest_row, self.T, self.k, out=self.dx)

@@ -115,8 +115,8 @@ def test_ffn_validation(L):
     assert L.moe_grouped_ffn_fwd(p, p, p, p, None, 1, 8, 32768, 16320, 64, p, None, p, 16,
                                  None) == 3
     # backward: only bf16
-    assert L.moe_grouped_ffn_bwd(p, p, p, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0, p,
-                                 1 << 30, None) == 2
+    assert L.moe_grouped_ffn_bwd(p, p, p, None, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0,
+                                 p, 1 << 30, None) == 2
     assert "LAEP_BF16" in _err(L)
     # fused dispatch: bf16 only, R <= T*k, row_src required
     assert L.moe_grouped_ffn_fwd_gather(p, p, 10, 2, p, p, p, None, 0, 8, 128, 128, 20, p, None,

@@ -181,22 +181,27 @@ def test_shard_backward_full_size():
     assert np.all(np.abs(hint(plan.dgate)[toks, 0] - ref_dg) <= TOL_F32 * cond)
     from oracle.numerics import round_bf16
     assert rownorm_err(h32(plan.dy_perm[tr]), round_bf16(g[toks, None] * dq)) <= TOL_BF16
-    # dgrad on sampled rows, teacher-forced on the GPU's act_save / dY / dA
-    dA_ws, hb_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
+    # dgrad on sampled rows, teacher-forced on the GPU's act_save / dY / dA; the
+    # plan hands the backward the forward's H, so the H_b buffer keeps dH
+    dA_ws, dh_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
+    h_fwd = laep.ffn_fwd_h_view(plan.ws_ffn, R, f, BF)
     srows = _sample_rows(offsets, per_expert=2, seed=6)
     ts = torch.from_numpy(srows).cuda()
     ex = _expert_of_rows(srows, offsets)
     dy_s, act_s = h32(plan.dy_perm[ts]), h32(plan.act_save[ts])
-    dA_s, hb_s, dx_s = h32(dA_ws[ts]), h32(hb_ws[ts]), h32(plan.dx_perm[ts])
+    dA_s, dh_s, dx_s = h32(dA_ws[ts]), h32(dh_ws[ts]), h32(plan.dx_perm[ts])
+    xp_s, h_s = h32(plan.x_perm[ts]), h32(h_fwd[ts])
     for e in np.unique(ex):
         sel = ex == e
         dH = dy_s[sel].astype(np.float64) @ c["w_down"][e].astype(np.float64)
-        rdA, rhb = om.swiglu_bwd(dH, act_s[sel], "bf16")
+        assert rownorm_err(dh_s[sel], round_bf16(dH)) <= TOL_BF16
+        rdA, _ = om.swiglu_bwd(dH, act_s[sel], "bf16")
         assert rownorm_err(dA_s[sel], rdA) <= TOL_BF16
-        assert rownorm_err(hb_s[sel], rhb) <= TOL_BF16
         rdx = round_bf16(dA_s[sel].astype(np.float64) @ c["w_gate_up"][e].astype(np.float64))
         assert rownorm_err(dx_s[sel], rdx) <= TOL_BF16
-    # wgrad on sampled output rows, teacher-forced on the GPU's dA / H_b
+        _, _, rh = om.expert_ffn(xp_s[sel], c["w_gate_up"][e], c["w_down"][e], "bf16")
+        assert rownorm_err(h_s[sel], rh) <= TOL_BF16
+    # wgrad on sampled output rows, teacher-forced on the GPU's dA / forward H
     case("full-size wgrad checks")
     dwgu, dwd = plan.dw_gate_up, plan.dw_down
     for e in range(w.E):
@@ -207,8 +212,8 @@ def test_shard_backward_full_size():
         i_d = rng.choice(d, 3, replace=False)
         i_g = rng.choice(2 * f, 3, replace=False)
         dy_e = h32(plan.dy_perm[tr][:, torch.from_numpy(i_d).cuda()]).astype(np.float64)
-        hb_e = h32(hb_ws[tr]).astype(np.float64)
-        ref_d = dy_e.T @ hb_e
+        h_e = h32(h_fwd[tr]).astype(np.float64)
+        ref_d = dy_e.T @ h_e
         assert rownorm_err(h32(dwd[e][torch.from_numpy(i_d).cuda()]), ref_d) <= TOL_F32
         dA_e = h32(dA_ws[tr][:, torch.from_numpy(i_g).cuda()]).astype(np.float64)
         x_e = h32(plan.x_perm[tr]).astype(np.float64)

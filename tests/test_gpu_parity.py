@@ -416,11 +416,12 @@ def test_ffn_fwd_gather_combine_matches_three_calls(T, E, d, f, mapped, keep_y):
     assert rownorm_err(host(out2), rout) <= TOL_BF16
 
 
+@pytest.mark.parametrize("use_h", [False, True])
 @pytest.mark.parametrize("counts,d,f", [
     ([60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
     ([300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),
 ])
-def test_ffn_bwd_parity(counts, d, f):
+def test_ffn_bwd_parity(counts, d, f, use_h):
     x, wgu, wd, offsets = _ffn_inputs(len(counts) + d, counts, d, f, "bf16")
     R = int(offsets[-1])
     E = len(counts)
@@ -428,12 +429,15 @@ def test_ffn_bwd_parity(counts, d, f):
     bf = torch.bfloat16
     xt, wgut, wdt = dev(x, bf), dev(wgu, bf), dev(wd, bf)
     off = dev(offsets.astype(np.int32), torch.int32)
-    case(f"ffn bwd counts={counts} d={d} f={f}")
-    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off)
+    case(f"ffn bwd counts={counts} d={d} f={f} use_h={use_h}")
+    ws_f = torch.empty(laep.workspace_bytes(laep.LAEP_CALL_FFN_FWD, R, 1, E, d, f),
+                       dtype=torch.uint8, device="cuda")
+    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off, ws=ws_f, save_act=True)
+    h_f = laep.ffn_fwd_h_view(ws_f, R, f, bf) if use_h else None
     dy = dev(rng.standard_normal((R, d)).astype(np.float32), bf)
     dwgu = torch.full(wgut.shape, 7.0, dtype=torch.float32, device="cuda")
     dwd = torch.full(wdt.shape, 7.0, dtype=torch.float32, device="cuda")
-    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off,
+    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, h_fwd=h_f,
                                                  dw_gate_up=dwgu, dw_down=dwd, return_ws=True)
     torch.cuda.synchronize()
     dA_g, hb_g = laep.ffn_bwd_ws_views(ws, R, f, bf)
@@ -442,18 +446,25 @@ def test_ffn_bwd_parity(counts, d, f):
     rdx, rdA, rhb = om.grouped_ffn_dgrad(dy_h, act_h, wgu, wd, offsets, dtype="bf16",
                                          dA_given=dA_h)
     assert rownorm_err(dA_h, rdA) <= TOL_BF16
-    assert rownorm_err(hb_h, rhb) <= TOL_BF16
     assert rownorm_err(host(dx), rdx) <= TOL_BF16
-    # wgrad (teacher-forced on the GPU's dA and H_b), fp32
-    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, hb_h, offsets, E)
+    if use_h:
+        # the forward's H against the oracle's; the H_b buffer keeps dH
+        _, _, rh = om.grouped_ffn_fwd(x, wgu, wd, offsets, dtype="bf16", return_h=True)
+        h_used = host(h_f)
+        assert rownorm_err(h_used, rh) <= TOL_BF16
+    else:
+        assert rownorm_err(hb_h, rhb) <= TOL_BF16
+        h_used = hb_h
+    # wgrad (teacher-forced on the GPU's dA and the H it used), fp32
+    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, h_used, offsets, E)
     got_gu, got_d = host(dwgu), host(dwd)
     for e in range(E):
         assert rownorm_err(got_gu[e], rgu[e]) <= TOL_F32, e
         assert rownorm_err(got_d[e], rd[e]) <= TOL_F32, e
     # accumulate adds onto the existing gradient
     case("ffn bwd accumulate")
-    laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, dw_gate_up=dwgu, dw_down=dwd,
-                             accumulate=True)
+    laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, h_fwd=h_f, dw_gate_up=dwgu,
+                             dw_down=dwd, accumulate=True)
     torch.cuda.synchronize()
     assert rownorm_err(host(dwd).reshape(E, -1), (2 * rd).reshape(E, -1)) <= TOL_F32
 
@@ -476,19 +487,30 @@ def test_ffn_bwd_fuzz(seed):
     bf = torch.bfloat16
     xt, wgut, wdt = dev(x, bf), dev(wgu, bf), dev(wd, bf)
     off = dev(offsets.astype(np.int32), torch.int32)
-    case(f"ffn bwd fuzz seed={seed} counts={counts} d={d} f={f}")
-    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off)
+    use_h = seed % 2 == 1   # odd seeds: dW_d from the forward's H
+    case(f"ffn bwd fuzz seed={seed} counts={counts} d={d} f={f} use_h={use_h}")
+    ws_f = torch.empty(laep.workspace_bytes(laep.LAEP_CALL_FFN_FWD, R, 1, E, d, f),
+                       dtype=torch.uint8, device="cuda")
+    _, act = laep.moe_grouped_ffn_fwd(xt, wgut, wdt, off, ws=ws_f, save_act=True)
+    h_f = laep.ffn_fwd_h_view(ws_f, R, f, bf) if use_h else None
     dy = dev(rng.standard_normal((R, d)).astype(np.float32), bf)
-    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, return_ws=True)
+    dx, dwgu, dwd, ws = laep.moe_grouped_ffn_bwd(dy, xt, act, wgut, wdt, off, h_fwd=h_f,
+                                                 return_ws=True)
     torch.cuda.synchronize()
     dA_g, hb_g = laep.ffn_bwd_ws_views(ws, R, f, bf)
     act_h, dy_h, dA_h, hb_h = host(act), host(dy), host(dA_g), host(hb_g)
     rdx, rdA, rhb = om.grouped_ffn_dgrad(dy_h, act_h, wgu, wd, offsets, dtype="bf16",
                                          dA_given=dA_h)
     assert rownorm_err(dA_h, rdA) <= TOL_BF16
-    assert rownorm_err(hb_h, rhb) <= TOL_BF16
     assert rownorm_err(host(dx), rdx) <= TOL_BF16
-    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, hb_h, offsets, E)
+    if use_h:
+        _, _, rh = om.grouped_ffn_fwd(x, wgu, wd, offsets, dtype="bf16", return_h=True)
+        h_used = host(h_f)
+        assert rownorm_err(h_used, rh) <= TOL_BF16
+    else:
+        assert rownorm_err(hb_h, rhb) <= TOL_BF16
+        h_used = hb_h
+    rgu, rd = om.grouped_ffn_wgrad(dy_h, x, dA_h, h_used, offsets, E)
     got_gu, got_d = host(dwgu), host(dwd)
     for e in range(E):
         assert rownorm_err(got_gu[e], rgu[e]) <= TOL_F32, e
