@@ -118,6 +118,10 @@ def test_ffn_validation(L):
     assert L.moe_grouped_ffn_bwd(p, p, p, None, p, p, p, None, 0, 8, 128, 128, 64, p, p, p, 0,
                                  p, 1 << 30, None) == 2
     assert "LAEP_BF16" in _err(L)
+    # the forward's H (h_fwd) is optional but, when given, 16-byte aligned
+    assert L.moe_grouped_ffn_bwd(p, p, p, p + 2, p, p, p, None, 1, 8, 128, 128, 64, p, p, p, 0,
+                                 p, 1 << 30, None) == 1
+    assert "aligned" in _err(L)
     # fused dispatch: bf16 only, R <= T*k, row_src required
     assert L.moe_grouped_ffn_fwd_gather(p, p, 10, 2, p, p, p, None, 0, 8, 128, 128, 20, p, None,
                                         p, 1 << 30, None) == 2
