@@ -9,8 +9,9 @@ dispatch folded into the FFN's operand loads) -> combine, every call a kernel
 of the C-ABI library; three input sets rotate over the steps so the
 activations are not cache-resident.  With one slot per token (shard,
 shard_bwd) the combine folds into the FFN call as well (the down projection
-writes each row, times its gate, to its token row).  Training steps keep the
-separate permute, because the weight gradient reads x_perm.
+writes each row, times its gate, to its token row).  Training steps keep
+x_perm, which the weight gradient reads: with k = 1 the FFN call writes it by a
+copy beside its products, for k > 1 the permute writes it.
 
 Prints ONE JSON line:
   value        tokens/s of the whole step (wall clock over the timed steps,
@@ -229,14 +230,16 @@ class Setup:
                                                            dest_row=p.dest_row,
                                                            row_src=p.row_src))]
             gate = self.gate
+        # training plans keep x_perm (the weight gradient reads it): with k = 1 the
+        # FFN call writes it by a copy beside its products
         if p.fused_combine:   # one slot per token: dispatch and combine folded into the FFN
-            if p.x_perm is not None:   # training: the weight gradient reads x_perm
-                out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm))]
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather_combine(
                 x, p.row_src, gate, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
                 out=p.out, keep_y=p.y_perm is not None, y_perm=p.y_perm,
-                save_act=p.act_save is not None, act_save=p.act_save))]
+                save_act=p.act_save is not None, act_save=p.act_save, x_perm_out=p.x_perm))]
         elif p.fused:   # dispatch folded into the FFN's operand loads
+            if p.x_perm is not None:   # k > 1: the token-major permute reads x once
+                out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm))]
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather(
                 x, p.row_src, w.k, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
                 y_perm=p.y_perm, save_act=p.act_save is not None, act_save=p.act_save))]

@@ -316,14 +316,19 @@ int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
  *   moe_grouped_ffn_fwd.  dtype must be LAEP_BF16 and x under 2 GiB
  *   (T*d_model*2 bytes: its rows are addressed with 32-bit offsets);
  *   LAEP_ERR_UNSUPPORTED otherwise.
+ *   x_perm_out device [R, d_model] bf16 or NULL: when given, the dispatched
+ *   rows (what moe_permute writes) are also written there, for the weight
+ *   gradient, by a copy on the library's side stream (see
+ *   moe_grouped_ffn_bwd) that runs beside the FFN and is joined back before
+ *   the call ends on `stream`.  It must not alias x or y_perm.
  */
 int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
                                int k, const void* w_gate_up,
                                const void* w_down, const int32_t* offsets,
                                const int32_t* expert_map, int dtype, int E,
                                int d_model, int d_ff, int64_t R,
-                               void* y_perm, void* act_save, void* ws,
-                               size_t ws_bytes, void* stream);
+                               void* y_perm, void* act_save, void* x_perm_out,
+                               void* ws, size_t ws_bytes, void* stream);
 
 /*
  * moe_grouped_ffn_fwd_gather_combine -- moe_grouped_ffn_fwd_gather followed
@@ -336,8 +341,9 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T,
  * non-NULL (the backward's moe_combine_bwd reads it), else never.
  *
  *   topk_gate device [T] fp32; out device [T, d_model] bf16 (must not alias
- *   x or y_perm); y_perm device [R, d_model] bf16 or NULL; the other
- *   arguments and the workspace are those of moe_grouped_ffn_fwd_gather.
+ *   x, y_perm or x_perm_out); y_perm device [R, d_model] bf16 or NULL; the
+ *   other arguments (x_perm_out included) and the workspace are those of
+ *   moe_grouped_ffn_fwd_gather.
  *   Rows of out whose token has no routed row (topk_idx == -1, which with
  *   k = 1 happens only when no expert is alive) are not written; moe_combine
  *   would write zeros there.
@@ -349,8 +355,8 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
                                        const int32_t* expert_map,
                                        const float* topk_gate, int dtype, int E,
                                        int d_model, int d_ff, int64_t R, void* out,
-                                       void* y_perm, void* act_save, void* ws,
-                                       size_t ws_bytes, void* stream);
+                                       void* y_perm, void* act_save, void* x_perm_out,
+                                       void* ws, size_t ws_bytes, void* stream);
 
 /*
  * moe_grouped_ffn_bwd -- backward of moe_grouped_ffn_fwd (data and weight
@@ -377,8 +383,9 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  *   at byte offset laep_ws_hb_offset(R, d_ff, dtype), H_b [R, d_ff] (dtype)
  *   when h_fwd is NULL, else dH.
  *   Only LAEP_BF16 is supported.
- *   Streams: the weight gradients run on a library-owned side stream of the
- *   current device (created on the first call, default priority), forked
+ *   Streams: the weight gradients run on the library-owned side stream of the
+ *   current device (one per device, created on the first call that uses it,
+ *   default priority, kept until the process ends), forked
  *   from `stream` (dW_d at the start when h_fwd is given, so it overlaps the
  *   first data gradient; otherwise after the SwiGLU backward) and joined back
  *   with events, so the call is ordered on `stream` as a whole and may be

@@ -60,9 +60,9 @@ SIGNATURES = {
     "moe_permute": (_i, [_p, _i, _p, _i, _i, _i, _p, _p]),
     "moe_grouped_ffn_fwd": (_i, [_p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_fwd_gather": (_i, [_p, _p, _i, _i, _p, _p, _p, _p, _i, _i, _i, _i, _i64,
-                                        _p, _p, _p, _sz, _p]),
+                                        _p, _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_fwd_gather_combine": (_i, [_p, _p, _i, _i, _p, _p, _p, _p, _p, _i, _i, _i,
-                                                _i, _i64, _p, _p, _p, _p, _sz, _p]),
+                                                _i, _i64, _p, _p, _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_bwd": (_i, [_p, _p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p,
                                  _i, _p, _sz, _p]),
     "laep_ws_hb_offset": (_sz, [_i64, _i, _i]),

@@ -280,9 +280,10 @@ def moe_grouped_ffn_fwd_gather(x: torch.Tensor, row_src: torch.Tensor, k: int,
                                w_gate_up: torch.Tensor, w_down: torch.Tensor,
                                offsets: torch.Tensor, *, rows: Optional[int] = None,
                                expert_map=None, save_act: bool = False, ws=None, y_perm=None,
-                               act_save=None):
+                               act_save=None, x_perm_out=None):
     """moe_permute + moe_grouped_ffn_fwd in one pass (bf16): routed row r reads
-    token row row_src[r] // k.  Returns (y_perm, act_save or None)."""
+    token row row_src[r] // k; ``x_perm_out`` [R, d] (optional) also receives
+    the dispatched rows, copied beside the FFN.  Returns (y_perm, act_save or None)."""
     for t, n in ((x, "x"), (row_src, "row_src"), (w_gate_up, "w_gate_up"), (w_down, "w_down"),
                  (offsets, "offsets")):
         _dev(t, n)
@@ -300,7 +301,7 @@ def moe_grouped_ffn_fwd_gather(x: torch.Tensor, row_src: torch.Tensor, k: int,
     check(lib().moe_grouped_ffn_fwd_gather(_ptr(x), _ptr(row_src), T, k, _ptr(w_gate_up),
                                            _ptr(w_down), _ptr(offsets), _ptr(expert_map),
                                            _dtype_code(x), E, d, f, R, _ptr(y_perm),
-                                           _ptr(act_save), _ptr(ws), ws.numel(),
+                                           _ptr(act_save), _ptr(x_perm_out), _ptr(ws), ws.numel(),
                                            _stream(dev)))
     return y_perm, act_save
 
@@ -310,7 +311,7 @@ def moe_grouped_ffn_fwd_gather_combine(x: torch.Tensor, row_src: torch.Tensor,
                                        w_down: torch.Tensor, offsets: torch.Tensor, *,
                                        rows: Optional[int] = None, expert_map=None,
                                        keep_y: bool = False, save_act: bool = False, ws=None,
-                                       out=None, y_perm=None, act_save=None):
+                                       out=None, y_perm=None, act_save=None, x_perm_out=None):
     """moe_grouped_ffn_fwd_gather + moe_combine for one slot per token (bf16):
     routed row r goes straight to token row row_src[r], times its gate.
     Returns (out, y_perm or None, act_save or None)."""
@@ -335,7 +336,7 @@ def moe_grouped_ffn_fwd_gather_combine(x: torch.Tensor, row_src: torch.Tensor,
     check(lib().moe_grouped_ffn_fwd_gather_combine(
         _ptr(x), _ptr(row_src), T, 1, _ptr(w_gate_up), _ptr(w_down), _ptr(offsets),
         _ptr(expert_map), _ptr(topk_gate), _dtype_code(x), E, d, f, R, _ptr(out), _ptr(y_perm),
-        _ptr(act_save), _ptr(ws), ws.numel(), _stream(dev)))
+        _ptr(act_save), _ptr(x_perm_out), _ptr(ws), ws.numel(), _stream(dev)))
     return out, y_perm, act_save
 
 

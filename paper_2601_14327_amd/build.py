@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "liblaep_moe.so")
 
 HIP_SOURCES = ["route.hip", "route_bwd.hip", "counts.hip", "prune.hip", "compact.hip", "rowops.hip",
                "gemm_bf16.hip", "gemm_bwd.hip", "gemm_f32.hip", "calib.hip"]
-HIP_HOST_SOURCES = ["api.cpp"]          # host code that calls the HIP runtime
+HIP_HOST_SOURCES = ["api.cpp", "streams.cpp"]   # host code that calls the HIP runtime
 CXX_SOURCES = ["rearrange.cpp"]         # plain host C++
 
 ARCH = "gfx950"

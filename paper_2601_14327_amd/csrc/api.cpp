@@ -356,8 +356,8 @@ int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up, const void* w
 int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T, int k,
                                const void* w_gate_up, const void* w_down, const int32_t* offsets,
                                const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
-                               int64_t R, void* y_perm, void* act_save, void* ws, size_t ws_bytes,
-                               void* stream) {
+                               int64_t R, void* y_perm, void* act_save, void* x_perm_out,
+                               void* ws, size_t ws_bytes, void* stream) {
   int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
   if (rc) return rc;
   REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
@@ -373,14 +373,17 @@ int moe_grouped_ffn_fwd_gather(const void* x, const int32_t* row_src, int T, int
           "moe_grouped_ffn_fwd_gather: x, row_src, w_gate_up, w_down, y_perm and ws must be "
           "non-null");
   REQUIRE(aligned16(x) && aligned16(w_gate_up) && aligned16(w_down) && aligned16(y_perm) &&
-              aligned16(act_save) && aligned16(ws),
+              aligned16(act_save) && aligned16(x_perm_out) && aligned16(ws),
           LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_fwd_gather: buffers must be 16-byte aligned");
+  REQUIRE(x_perm_out != x && x_perm_out != y_perm, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather: x_perm_out must not alias x or y_perm");
   const size_t need = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, dtype);
   REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE,
           "moe_grouped_ffn_fwd_gather: workspace %zu < %zu bytes", ws_bytes, need);
   return hip_status(laep::launch_ffn_fwd_bf16(x, w_gate_up, w_down, offsets, expert_map, E,
                                               d_model, d_ff, R, y_perm, act_save, ws,
-                                              as_stream(stream), row_src, k),
+                                              as_stream(stream), row_src, k, nullptr, nullptr,
+                                              x_perm_out),
                     "moe_grouped_ffn_fwd_gather");
 }
 
@@ -389,7 +392,8 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src, in
                                        const int32_t* offsets, const int32_t* expert_map,
                                        const float* topk_gate, int dtype, int E, int d_model,
                                        int d_ff, int64_t R, void* out, void* y_perm,
-                                       void* act_save, void* ws, size_t ws_bytes, void* stream) {
+                                       void* act_save, void* x_perm_out, void* ws,
+                                       size_t ws_bytes, void* stream) {
   int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
   if (rc) return rc;
   REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
@@ -408,17 +412,21 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src, in
           "moe_grouped_ffn_fwd_gather_combine: x, row_src, w_gate_up, w_down, topk_gate, out "
           "and ws must be non-null");
   REQUIRE(aligned16(x) && aligned16(w_gate_up) && aligned16(w_down) && aligned16(out) &&
-              aligned16(y_perm) && aligned16(act_save) && aligned16(ws),
+              aligned16(y_perm) && aligned16(act_save) && aligned16(x_perm_out) && aligned16(ws),
           LAEP_ERR_INVALID_ARG,
           "moe_grouped_ffn_fwd_gather_combine: buffers must be 16-byte aligned");
-  REQUIRE(out != y_perm && out != x, LAEP_ERR_INVALID_ARG,
-          "moe_grouped_ffn_fwd_gather_combine: out must not alias x or y_perm");
+  REQUIRE(out != y_perm && out != x && out != x_perm_out, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: out must not alias x, y_perm or x_perm_out");
+  REQUIRE(x_perm_out == nullptr || (x_perm_out != x && x_perm_out != y_perm),
+          LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_fwd_gather_combine: x_perm_out must not alias x or y_perm");
   const size_t need = laep::ffn_fwd_ws_bytes(R, E, d_model, d_ff, dtype);
   REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE,
           "moe_grouped_ffn_fwd_gather_combine: workspace %zu < %zu bytes", ws_bytes, need);
   return hip_status(laep::launch_ffn_fwd_bf16(x, w_gate_up, w_down, offsets, expert_map, E,
                                               d_model, d_ff, R, y_perm, act_save, ws,
-                                              as_stream(stream), row_src, k, topk_gate, out),
+                                              as_stream(stream), row_src, k, topk_gate, out,
+                                              x_perm_out),
                     "moe_grouped_ffn_fwd_gather_combine");
 }
 

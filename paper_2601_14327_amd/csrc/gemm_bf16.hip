@@ -429,12 +429,14 @@ size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype) {
   return align_up((size_t)R * f * 4, 256) + table_bytes(ceil_div(R, 64) + E);
 }
 
-hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
-                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
-                               int f, int64_t R, void* y_perm, void* act_save, void* ws,
-                               hipStream_t s, const int32_t* row_src, int slots_k,
-                               const float* gate, void* out_tok) {
-  bf16_t* H = static_cast<bf16_t*>(ws);
+namespace {
+
+// the two products of the forward FFN (and the tile lists), on s
+hipError_t launch_ffn_fwd_products(const void* x_perm, const void* w_gu, const void* w_d,
+                                   const int32_t* offsets, const int32_t* expert_map, int E,
+                                   int d, int f, int64_t R, void* y_perm, void* act_save,
+                                   bf16_t* H, void* ws, hipStream_t s, const int32_t* row_src,
+                                   int slots_k, const float* gate, void* out_tok) {
   const int nt_gu = ceil_div(f, kFwdBN / 2), nt_d = ceil_div(d, kFwdBN);
   const int max_gu = fwd_list_max(R, E, nt_gu), max_d = fwd_list_max(R, E, nt_d);
   char* tables = static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256);
@@ -488,6 +490,39 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   g.gate = gate;
   g.out_tok = static_cast<bf16_t*>(out_tok);
   return launch_fwd<EPI_STORE, false>(g, max_d, s);
+}
+
+}  // namespace
+
+hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
+                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
+                               int f, int64_t R, void* y_perm, void* act_save, void* ws,
+                               hipStream_t s, const int32_t* row_src, int slots_k,
+                               const float* gate, void* out_tok, void* x_perm_out) {
+  bf16_t* H = static_cast<bf16_t*>(ws);
+  // x_perm for the weight gradient: written on the side stream beside the FFN
+  // (HBM-bound copy against MFMA-bound products), joined before returning
+  std::unique_lock<std::mutex> lock;
+  SideStream* side = nullptr;
+  if (x_perm_out && row_src) {
+    lock = side_stream_lock();
+    hipError_t e = side_stream_get(side);
+    if (e == hipSuccess) e = side_stream_fork(*side, s);
+    if (e == hipSuccess) e = launch_gather_rows(x_perm, row_src, slots_k, R, d, 2, x_perm_out,
+                                                side->stream);
+    if (e != hipSuccess) {
+      if (side) side_stream_join(*side, s);
+      return e;
+    }
+  }
+  const hipError_t err = launch_ffn_fwd_products(x_perm, w_gu, w_d, offsets, expert_map, E, d, f,
+                                                 R, y_perm, act_save, H, ws, s, row_src, slots_k,
+                                                 gate, out_tok);
+  if (side) {
+    const hipError_t jerr = side_stream_join(*side, s);
+    return err != hipSuccess ? err : jerr;
+  }
+  return err;
 }
 
 }  // namespace laep

@@ -27,7 +27,6 @@
 // with streaming (non-temporal) stores: every output (dA, H_b, dX, the fp32
 // weight gradients) is far larger than the caches (measured 3 % faster on the
 // backward call).
-#include <mutex>
 #include <type_traits>
 
 #include "gemm_common.hpp"
@@ -458,37 +457,6 @@ hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
 
 }  // namespace
 
-namespace {
-
-// Library-owned side stream (default priority) and fork/join events, one set
-// per device, created on first use and kept for the life of the process.  The
-// weight gradients run there concurrently with data-gradient 2: the two are
-// independent, and each alone leaves CUs idle in its last round of tiles.
-constexpr int kMaxDevices = 64;
-struct SideStream {
-  hipStream_t stream = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-};
-std::mutex g_side_mu;  // also serialises the fork/join enqueues (shared events)
-SideStream g_side[kMaxDevices];
-
-hipError_t side_stream_locked(SideStream*& out) {
-  int dev = 0;
-  hipError_t err = hipGetDevice(&dev);
-  if (err != hipSuccess) return err;
-  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  SideStream& ss = g_side[dev];
-  if (!ss.stream) {
-    if ((err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess) return err;
-    if ((err = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return err;
-    if ((err = hipEventCreateWithFlags(&ss.join, hipEventDisableTiming)) != hipSuccess) return err;
-  }
-  out = &ss;
-  return hipSuccess;
-}
-
-}  // namespace
-
 size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype) {
   const size_t elem = dtype == kDtypeBf16 ? 2 : 4;
   return align_up((size_t)R * 2 * f * elem, 256);
@@ -553,15 +521,12 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   // gradients: dW_d from the start when it uses the forward's H, else after
   // the SwiGLU backward like dW_gu; joined back (also after an error) before
   // the call returns.
-  std::lock_guard<std::mutex> lock(g_side_mu);
+  auto lock = side_stream_lock();
   SideStream* side = nullptr;
-  hipError_t err = side_stream_locked(side);
+  hipError_t err = side_stream_get(side);
   if (err != hipSuccess) return err;
   const hipStream_t s2 = side->stream;
-  auto fork = [&]() -> hipError_t {
-    hipError_t e = hipEventRecord(side->fork, s);
-    return e == hipSuccess ? hipStreamWaitEvent(s2, side->fork, 0) : e;
-  };
+  auto fork = [&]() { return side_stream_fork(*side, s); };
   if ((err = fork()) != hipSuccess) return err;
   if (h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
 
@@ -609,8 +574,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.out = static_cast<bf16_t*>(dx_perm);
   g.ldo = d;
   if (err == hipSuccess) err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
-  hipError_t jerr = hipEventRecord(side->join, s2);
-  if (jerr == hipSuccess) jerr = hipStreamWaitEvent(s, side->join, 0);
+  const hipError_t jerr = side_stream_join(*side, s);
   return err != hipSuccess ? err : jerr;
 }
 

@@ -7,12 +7,28 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 namespace laep {
 
 constexpr int kDtypeF32 = 0;
 constexpr int kDtypeBf16 = 1;
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Library-owned side stream of the current device (default priority) and its
+// fork / join events, for work a call runs beside the caller's stream.  Hold
+// side_stream_lock() from side_stream_get() through the call's join.
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::unique_lock<std::mutex> side_stream_lock();
+hipError_t side_stream_get(SideStream*& out);
+// the side stream waits for the work enqueued on s so far
+hipError_t side_stream_fork(const SideStream& ss, hipStream_t s);
+// s waits for the work enqueued on the side stream so far
+hipError_t side_stream_join(const SideStream& ss, hipStream_t s);
 
 hipError_t launch_route(const void* x, const void* w, const float* bias, const uint8_t* alive,
                         int dtype, int T, int d, int E, int k, int renorm, float* logits,
@@ -42,6 +58,9 @@ hipError_t launch_repack_scalar(const int32_t* expert_map, int E, int n_out, con
 
 hipError_t launch_permute(const void* x, int elem_bytes, const int32_t* dest_row, int T, int k,
                           int d, void* x_perm, hipStream_t s);
+// x_perm[r] = x[row_src[r] / k] for the R routed rows
+hipError_t launch_gather_rows(const void* x, const int32_t* row_src, int k, int64_t R, int d,
+                              int elem_bytes, void* x_perm, hipStream_t s);
 hipError_t launch_combine(const void* y, const float* gate, const int32_t* dest_row, int T, int k,
                           int d, int dtype, void* out, hipStream_t s);
 hipError_t launch_combine_bwd(const void* dout, const void* y, const float* gate,
@@ -53,11 +72,14 @@ size_t ffn_fwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
 // row_src != NULL: the gate/up A rows are gathered (row r = x_perm row row_src[r] / slots_k).
 // out_tok != NULL (one slot per token): routed row r also goes to out_tok row
 // row_src[r] / slots_k, times gate[row_src[r]]; y_perm may then be NULL.
+// x_perm_out != NULL (with row_src): the gathered rows are also written there,
+// on the side stream, beside the FFN.
 hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void* w_d,
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* y_perm, void* act_save, void* ws,
                                hipStream_t s, const int32_t* row_src = nullptr, int slots_k = 1,
-                               const float* gate = nullptr, void* out_tok = nullptr);
+                               const float* gate = nullptr, void* out_tok = nullptr,
+                               void* x_perm_out = nullptr);
 hipError_t launch_ffn_fwd_f32(const void* x_perm, const void* w_gu, const void* w_d,
                               const int32_t* offsets, const int32_t* expert_map, int E, int d,
                               int f, int64_t R, void* y_perm, void* act_save, void* ws,

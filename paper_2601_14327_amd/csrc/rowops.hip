@@ -39,6 +39,20 @@ __global__ __launch_bounds__(kRowThreads) void permute_kernel(
   }
 }
 
+// Dispatch in routed-row order: x_perm[r] = x[row_src[r] / k], one 16-byte
+// vector per thread.  The token rows are read k times each (cached loads);
+// x_perm is written once and read only by a later call (streaming stores).
+__global__ __launch_bounds__(kRowThreads) void gather_rows_kernel(
+    const u32x4_t* __restrict__ x, const int32_t* __restrict__ row_src, int k, int64_t R,
+    int vec_per_row, u32x4_t* __restrict__ x_perm) {
+  const long long i = (long long)blockIdx.x * kRowThreads + threadIdx.x;
+  if (i >= R * vec_per_row) return;
+  const long long r = i / vec_per_row;
+  const int v = (int)(i % vec_per_row);
+  const int t = row_src[r] / k;
+  st_stream(x_perm + i, x[(size_t)t * vec_per_row + v]);
+}
+
 // One 8-element row vector in its storage format: load (zero when !ok) and
 // acc[e] += g * value[e].
 template <typename T> struct RawRow;
@@ -191,6 +205,17 @@ hipError_t launch_permute(const void* x, int elem_bytes, const int32_t* dest_row
   hipLaunchKernelGGL(permute_kernel, dim3((T + tpb - 1) / tpb), dim3(kRowThreads), 0, s,
                      static_cast<const u32x4_t*>(x), dest_row, T, k, vec_per_row, tpb,
                      static_cast<u32x4_t*>(x_perm));
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const void* x, const int32_t* row_src, int k, int64_t R, int d,
+                              int elem_bytes, void* x_perm, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  const int vec_per_row = d * elem_bytes / 16;
+  const long long n = R * (long long)vec_per_row;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)((n + kRowThreads - 1) / kRowThreads)),
+                     dim3(kRowThreads), 0, s, static_cast<const u32x4_t*>(x), row_src, k, R,
+                     vec_per_row, static_cast<u32x4_t*>(x_perm));
   return hipGetLastError();
 }
 

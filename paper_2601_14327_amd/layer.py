@@ -6,13 +6,14 @@ Forward (router path):
     -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
 Forward (given routing, one device's expert shard with k = 1):
     moe_expert_counts -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
-With fused dispatch (bf16 forward-only plans, the default there),
-moe_permute + moe_grouped_ffn_fwd become one moe_grouped_ffn_fwd_gather
-call that reads the token rows through row_src; x_perm is never written.
-With one slot per token (k = 1, bf16) the combine folds in as well
+With fused dispatch (bf16, the default), moe_permute + moe_grouped_ffn_fwd
+become one moe_grouped_ffn_fwd_gather call that reads the token rows through
+row_src.  Where x_perm is kept (the backward's weight gradient reads it),
+moe_permute still writes it for k > 1; with k = 1 the FFN call writes it by a
+copy beside its products.
+With one slot per token (k = 1) the combine folds in as well
 (moe_grouped_ffn_fwd_gather_combine): the down projection writes each row,
-times its gate, to its token row; y_perm is written only for a backward pass,
-whose plans also keep moe_permute (the weight gradient reads x_perm).
+times its gate, to its token row; y_perm is written only for a backward pass.
 Backward:
     moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
       [-> moe_route_bwd, accumulating the router's dx]   (router path)
@@ -52,21 +53,23 @@ class MoELayerPlan:
         self.n_pruned = torch.empty(1, dtype=i32, device=dev)
         # pre-activations are kept when a backward pass will read them (or on request)
         save_act = backward if save_act is None else save_act
-        # the dispatch folds into the FFN's operand loads unless x_perm is needed
-        # (the weight gradient reads it) or the dtype has no fused kernel
+        # the dispatch folds into the FFN's operand loads (bf16); x_perm is still
+        # kept where the weight gradient (or a caller) reads it, written by the
+        # FFN call beside its products
         if fused_dispatch is None:
-            fused_dispatch = dtype == torch.bfloat16 and not backward and not save_act
+            fused_dispatch = dtype == torch.bfloat16
         self.fused = bool(fused_dispatch)
-        self.x_perm = (None if self.fused else
+        self.x_perm = (None if self.fused and not (backward or save_act) else
                        torch.empty((R, d_model), dtype=dtype, device=dev))
         # the dispatch order is kept when the FFN gathers through it or the
         # router backward sums dW_r over it
         self.row_src = (torch.empty(R, dtype=i32, device=dev) if self.fused or backward
                         else None)
         # one slot per token (bf16): the combine folds into the down projection's
-        # epilogue; y_perm is then written only for the backward (combine_bwd)
-        self.fused_combine = k == 1 and dtype == torch.bfloat16 and (self.fused or backward)
-        self.y_perm = (None if self.fused_combine and not backward else
+        # epilogue; y_perm is then written only for the backward (combine_bwd) or
+        # when the caller keeps the activations (save_act)
+        self.fused_combine = k == 1 and self.fused
+        self.y_perm = (None if self.fused_combine and not (backward or save_act) else
                        torch.empty((R, d_model), dtype=dtype, device=dev))
         self.act_save = (torch.empty((R, 2 * d_ff), dtype=dtype, device=dev) if save_act
                          else None)
@@ -114,15 +117,18 @@ class MoELayerPlan:
 
     def experts_and_combine(self, x, w_gate_up, w_down, expert_map=None):
         if self.fused_combine:
-            if self.x_perm is not None:   # the weight gradient reads x_perm
-                api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
             api.moe_grouped_ffn_fwd_gather_combine(
                 x, self.row_src, self.topk_gate, w_gate_up, w_down, self.offsets, rows=self.R,
                 expert_map=expert_map, ws=self.ws_ffn, out=self.out,
                 keep_y=self.y_perm is not None, y_perm=self.y_perm,
-                save_act=self.act_save is not None, act_save=self.act_save)
+                save_act=self.act_save is not None, act_save=self.act_save,
+                x_perm_out=self.x_perm)
             return self.out
         if self.fused:
+            # k > 1: x_perm (when kept) by the token-major permute, which reads each
+            # token row once; a row-order copy beside the FFN would read it k times
+            if self.x_perm is not None:
+                api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
             api.moe_grouped_ffn_fwd_gather(x, self.row_src, self.k, w_gate_up, w_down,
                                            self.offsets, rows=self.R, expert_map=expert_map,
                                            ws=self.ws_ffn, y_perm=self.y_perm,

@@ -123,29 +123,41 @@ def test_ffn_validation(L):
                                  p, 1 << 30, None) == 1
     assert "aligned" in _err(L)
     # fused dispatch: bf16 only, R <= T*k, row_src required
-    assert L.moe_grouped_ffn_fwd_gather(p, p, 10, 2, p, p, p, None, 0, 8, 128, 128, 20, p, None,
-                                        p, 1 << 30, None) == 2
-    assert L.moe_grouped_ffn_fwd_gather(p, p, 10, 2, p, p, p, None, 1, 8, 128, 128, 21, p, None,
-                                        p, 1 << 30, None) == 1
-    assert L.moe_grouped_ffn_fwd_gather(p, None, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, p, None,
-                                        p, 1 << 30, None) == 1
+    g = L.moe_grouped_ffn_fwd_gather
+    assert g(p, p, 10, 2, p, p, p, None, 0, 8, 128, 128, 20, p, None, None, p, 1 << 30,
+             None) == 2
+    assert g(p, p, 10, 2, p, p, p, None, 1, 8, 128, 128, 21, p, None, None, p, 1 << 30,
+             None) == 1
+    assert g(p, None, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, p, None, None, p, 1 << 30,
+             None) == 1
+    # the copy of the dispatched rows must not alias y_perm, and is 16-byte aligned
+    q = p + 16
+    assert g(p, p, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, q, None, q, p, 1 << 30,
+             None) == 1
+    assert "alias" in _err(L)
+    assert g(p, p, 10, 2, p, p, p, None, 1, 8, 128, 128, 20, q, None, p + 2, p, 1 << 30,
+             None) == 1
+    assert "aligned" in _err(L)
     # gather + combine: one slot per token only, R <= T, out not aliasing y_perm
     gc = L.moe_grouped_ffn_fwd_gather_combine
-    assert gc(p, p, 10, 2, p, p, p, None, p, 1, 8, 128, 128, 20, p, None, None, p, 1 << 30,
-              None) == 2
+    assert gc(p, p, 10, 2, p, p, p, None, p, 1, 8, 128, 128, 20, p, None, None, None, p,
+              1 << 30, None) == 2
     assert "one slot per token" in _err(L)
-    assert gc(p, p, 10, 1, p, p, p, None, p, 0, 8, 128, 128, 10, p, None, None, p, 1 << 30,
-              None) == 2
-    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 11, p, None, None, p, 1 << 30,
+    assert gc(p, p, 10, 1, p, p, p, None, p, 0, 8, 128, 128, 10, p, None, None, None, p,
+              1 << 30, None) == 2
+    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 11, p, None, None, None, p,
+              1 << 30, None) == 1
+    assert gc(p, p, 10, 1, p, p, p, None, None, 1, 8, 128, 128, 10, p, None, None, None, p,
+              1 << 30, None) == 1
+    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 10, p, p, None, None, p, 1 << 30,
               None) == 1
-    assert gc(p, p, 10, 1, p, p, p, None, None, 1, 8, 128, 128, 10, p, None, None, p, 1 << 30,
-              None) == 1
-    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 10, p, p, None, p, 1 << 30,
+    assert "alias" in _err(L)
+    assert gc(p, p, 10, 1, p, p, p, None, p, 1, 8, 128, 128, 10, q, None, None, q, p, 1 << 30,
               None) == 1
     assert "alias" in _err(L)
     # x addressed with 32-bit offsets: T * d_model * 2 bytes under 2 GiB
-    assert L.moe_grouped_ffn_fwd_gather(p, p, 1 << 19, 2, p, p, p, None, 1, 8, 2048, 128, 20, p,
-                                        None, p, 1 << 30, None) == 2
+    assert g(p, p, 1 << 19, 2, p, p, p, None, 1, 8, 2048, 128, 20, p, None, None, p, 1 << 30,
+             None) == 2
 
 
 def test_route_bwd_validation(L):

@@ -359,11 +359,13 @@ def test_ffn_fwd_gather_matches_permute_then_ffn(T, k, E, d, f, mapped):
     counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
     x_perm = laep.moe_permute(x, dest_row, k)
     y1, a1 = laep.moe_grouped_ffn_fwd(x_perm, wgu, wd, offsets, expert_map=emap)
+    xp_copy = torch.full_like(x_perm, 5.0)
     y2, a2 = laep.moe_grouped_ffn_fwd_gather(x, row_src, k, wgu, wd, offsets, expert_map=emap,
-                                            save_act=True)
+                                            save_act=True, x_perm_out=xp_copy)
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
     assert torch.equal(a1, a2)
+    assert torch.equal(xp_copy, x_perm)   # the dispatched rows written beside the FFN
     # and against the oracle's permute + grouped FFN
     rc, ro, rd = om.expert_counts(ids, E)
     xp = om.permute(c["x"], rd, k)
@@ -399,10 +401,14 @@ def test_ffn_fwd_gather_combine_matches_three_calls(T, E, d, f, mapped, keep_y):
     y1, a1 = laep.moe_grouped_ffn_fwd_gather(x, row_src, 1, wgu, wd, offsets, expert_map=emap,
                                             save_act=True)
     out1 = laep.moe_combine(y1, g, dest_row)
+    xp_copy = torch.empty((T, d), dtype=bf, device="cuda") if keep_y else None
     out2, y2, a2 = laep.moe_grouped_ffn_fwd_gather_combine(
-        x, row_src, g, wgu, wd, offsets, expert_map=emap, keep_y=keep_y, save_act=True)
+        x, row_src, g, wgu, wd, offsets, expert_map=emap, keep_y=keep_y, save_act=True,
+        x_perm_out=xp_copy)
     torch.cuda.synchronize()
     assert torch.equal(out1, out2)
+    if keep_y:
+        assert torch.equal(xp_copy, laep.moe_permute(x, dest_row, 1))
     assert torch.equal(a1, a2)
     if keep_y:
         assert torch.equal(y1, y2)
