@@ -257,16 +257,18 @@ class Setup:
                 p.dw_down = torch.empty(self.wd.shape, dtype=torch.float32, device=self.dev)
             out += [("combine_bwd", lambda: L.moe_combine_bwd(self.dout, p.y_perm, gate,
                                                               p.dest_row, dy_perm=p.dy_perm,
-                                                              dgate=p.dgate)),
-                    ("ffn_bwd", lambda: L.moe_grouped_ffn_bwd(
+                                                              dgate=p.dgate))]
+            if w.routed:   # the router's weight gradients on a side stream, beside the FFN's
+                out += [("route_bwd_w", lambda: p.route_backward_weights_async(x, self.wr))]
+            out += [("ffn_bwd", lambda: L.moe_grouped_ffn_bwd(
                         p.dy_perm, p.x_perm, p.act_save, self.wgu, self.wd, p.offsets,
                         h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
                         dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,
                         dx_perm=p.dx_perm)),
                     ("permute_bwd", lambda: L.moe_permute_bwd(p.dx_perm, p.dest_row, w.T, w.k,
                                                               out=p.dx))]
-            if w.routed:   # router / gate backward, accumulated onto dx
-                out += [("route_bwd", lambda: p.route_backward(x, self.wr, renorm=w.renorm))]
+            if w.routed:   # router's dx, accumulated onto dx; then wait for route_bwd_w
+                out += [("route_bwd_dx", lambda: p.route_backward_data(x, self.wr))]
         return out
 
     def algorithmic(self):

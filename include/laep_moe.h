@@ -247,6 +247,10 @@ int laep_repack_experts(const int32_t* expert_map, int E, int n_out, int dtype,
  *   dgate, topk_gate device [T, k] float32; topk_idx device [T, k] int32
  *   (as moe_route wrote them); x device [T, d_model] dtype; w_router device
  *   [E, d_model] dtype; dx device [T, d_model] dtype.
+ *   dx may be NULL (no data gradient) and dw_router may be NULL (no weight
+ *   gradients; dbias must then be NULL too), so a training step can take the
+ *   weight gradients as soon as dgate exists and dx once the expert path's dx
+ *   does (two calls, two workspaces).
  *   renorm = 1 needs offsets [E + 1] and row_src [T * k] from
  *   moe_expert_counts on the same topk_idx (dw_router is summed over each
  *   expert's routed rows in that order); logits and alive may be NULL.

@@ -80,22 +80,30 @@ def moe_route_bwd(dgate: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.
                   x: torch.Tensor, w_router: torch.Tensor, *, renorm: bool = True,
                   logits=None, alive=None, offsets=None, row_src=None, dx=None,
                   accumulate_dx: bool = False, want_dlogits: bool = False,
-                  want_dbias: bool = False, dw_router=None, dlogits=None, dbias=None, ws=None):
-    """Router/gate backward with the selection fixed.
-    Returns (dx, dw_router, dbias or None, dlogits or None)."""
+                  want_dbias: bool = False, dw_router=None, dlogits=None, dbias=None, ws=None,
+                  data: bool = True, weights: bool = True):
+    """Router/gate backward with the selection fixed.  ``data=False`` skips dx,
+    ``weights=False`` skips dw_router and dbias.
+    Returns (dx, dw_router, dbias, dlogits), None for what was not computed."""
     for t, n in ((dgate, "dgate"), (topk_idx, "topk_idx"), (topk_gate, "topk_gate"), (x, "x"),
                  (w_router, "w_router")):
         _dev(t, n)
     T, k = topk_idx.shape
     E, d = w_router.shape
     dev = x.device
-    dx = torch.zeros_like(x) if dx is None else dx
-    dw_router = (torch.empty((E, d), dtype=torch.float32, device=dev) if dw_router is None
-                 else dw_router)
+    if data:
+        dx = torch.zeros_like(x) if dx is None else dx
+    else:
+        dx = None
+    if weights:
+        dw_router = (torch.empty((E, d), dtype=torch.float32, device=dev) if dw_router is None
+                     else dw_router)
+        if want_dbias and dbias is None:
+            dbias = torch.empty(E, dtype=torch.float32, device=dev)
+    else:
+        dw_router, dbias = None, None
     if want_dlogits and dlogits is None:
         dlogits = torch.empty((T, E), dtype=torch.float32, device=dev)
-    if want_dbias and dbias is None:
-        dbias = torch.empty(E, dtype=torch.float32, device=dev)
     ws = _workspace(ws, workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d), dev)
     check(lib().moe_route_bwd(_ptr(dgate), _ptr(topk_idx), _ptr(topk_gate), _ptr(logits),
                               _ptr(alive), _ptr(x), _ptr(w_router), _ptr(offsets), _ptr(row_src),

@@ -287,13 +287,14 @@ int moe_route_bwd(const float* dgate, const int32_t* topk_idx, const float* topk
   if (rc) return rc;
   if ((rc = check_experts(E, k))) return rc;
   if ((rc = check_rows(T, k, d_model))) return rc;
-  REQUIRE(w_router && dw_router, LAEP_ERR_INVALID_ARG,
-          "moe_route_bwd: w_router and dw_router must be non-null");
+  REQUIRE(w_router, LAEP_ERR_INVALID_ARG, "moe_route_bwd: w_router must be non-null");
+  REQUIRE(dw_router || !dbias, LAEP_ERR_INVALID_ARG,
+          "moe_route_bwd: dbias needs dw_router (they are computed together)");
   REQUIRE(aligned16(w_router) && aligned16(dw_router), LAEP_ERR_INVALID_ARG,
           "moe_route_bwd: w_router and dw_router must be 16-byte aligned");
   if (T > 0) {
-    REQUIRE(dgate && topk_idx && topk_gate && x && dx && ws, LAEP_ERR_INVALID_ARG,
-            "moe_route_bwd: dgate, topk_idx, topk_gate, x, dx and ws must be non-null");
+    REQUIRE(dgate && topk_idx && topk_gate && x && ws, LAEP_ERR_INVALID_ARG,
+            "moe_route_bwd: dgate, topk_idx, topk_gate, x and ws must be non-null");
     REQUIRE(aligned16(x) && aligned16(dx), LAEP_ERR_INVALID_ARG,
             "moe_route_bwd: x and dx must be 16-byte aligned");
     if (renorm)

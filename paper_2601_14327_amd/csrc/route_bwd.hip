@@ -329,7 +329,8 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
                             hipStream_t s) {
   if (T_ == 0) {
     // no tokens: zero weight gradients (dx has no rows)
-    hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, dw_router, (size_t)E * d);
+    if (dw_router)
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(64), dim3(256), 0, s, dw_router, (size_t)E * d);
     if (dbias) hipLaunchKernelGGL(fill_zero_kernel, dim3(1), dim3(256), 0, s, dbias, (size_t)E);
     return hipGetLastError();
   }
@@ -346,36 +347,39 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
   TableWs tw = carve_table(base, m);
   float* part = reinterpret_cast<float*>(base + table_bytes(m));
   float* part_b = reinterpret_cast<float*>(base + table_bytes(m) + align_up((size_t)m * d * 4, 256));
-  if (renorm)
+  // dx (optional) and the weight gradients (optional, with dbias)
+  if (renorm && dw_router)
     hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, nullptr, E,
                        kSegRows, 0, m, tw.n_entries, tw.table);
   const dim3 gred(E, (d + 255) / 256 < 8 ? (d + 255) / 256 : 8);
   if (dtype == kDtypeBf16) {
-    hipLaunchKernelGGL(route_bwd_dx_kernel<bf16_t>, gdx, dim3(256), 0, s,
-                       static_cast<const bf16_t*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
-                       static_cast<bf16_t*>(dx));
-    if (renorm) {
+    if (dx)
+      hipLaunchKernelGGL(route_bwd_dx_kernel<bf16_t>, gdx, dim3(256), 0, s,
+                         static_cast<const bf16_t*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
+                         static_cast<bf16_t*>(dx));
+    if (dw_router && renorm) {
       hipLaunchKernelGGL((route_bwd_dw_seg_kernel<bf16_t, 1>), dim3(m), dim3(256), 0, s,
                          static_cast<const bf16_t*>(x), dl, row_src, tw.table, tw.n_entries, k, d,
                          part, part_b);
       hipLaunchKernelGGL(route_bwd_dw_reduce_kernel, gred, dim3(256), 0, s, part, part_b,
                          tw.table, tw.n_entries, E, d, dw_router, dbias);
-    } else {
+    } else if (dw_router) {
       hipLaunchKernelGGL(route_bwd_dw_kernel<bf16_t>, gdw, dim3(256), 0, s,
                          static_cast<const bf16_t*>(x), dl, T_, E, d,
                          dw_router, dbias);
     }
   } else {
-    hipLaunchKernelGGL(route_bwd_dx_kernel<float>, gdx, dim3(256), 0, s,
-                       static_cast<const float*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
-                       static_cast<float*>(dx));
-    if (renorm) {
+    if (dx)
+      hipLaunchKernelGGL(route_bwd_dx_kernel<float>, gdx, dim3(256), 0, s,
+                         static_cast<const float*>(w_router), ids, dl, T_, slots, d, accumulate_dx,
+                         static_cast<float*>(dx));
+    if (dw_router && renorm) {
       hipLaunchKernelGGL((route_bwd_dw_seg_kernel<float, 1>), dim3(m), dim3(256), 0, s,
                          static_cast<const float*>(x), dl, row_src, tw.table, tw.n_entries, k, d,
                          part, part_b);
       hipLaunchKernelGGL(route_bwd_dw_reduce_kernel, gred, dim3(256), 0, s, part, part_b,
                          tw.table, tw.n_entries, E, d, dw_router, dbias);
-    } else {
+    } else if (dw_router) {
       hipLaunchKernelGGL(route_bwd_dw_kernel<float>, gdw, dim3(256), 0, s,
                          static_cast<const float*>(x), dl, T_, E, d,
                          dw_router, dbias);

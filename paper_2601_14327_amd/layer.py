@@ -17,6 +17,9 @@ times its gate, to its token row; y_perm is written only for a backward pass.
 Backward:
     moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
       [-> moe_route_bwd, accumulating the router's dx]   (router path)
+In a training step the router's weight gradients need only the gate gradient:
+backward(router=...) runs them on a side stream beside the expert backward and
+takes the router's dx after moe_permute_bwd.
 
 All buffers are allocated once, so a pass makes no allocation and no host
 synchronisation; every step runs in the library's kernels on the current
@@ -90,9 +93,13 @@ class MoELayerPlan:
             self.dw_down = None
             self.dw_router = None
             self.dbias = None
-            self.ws_route_bwd = torch.empty(
-                max(1, api.workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d_model)), dtype=torch.uint8,
-                device=dev)
+            rb = max(1, api.workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d_model))
+            self.ws_route_bwd = torch.empty(rb, dtype=torch.uint8, device=dev)
+            # the router's weight gradients run on a side stream beside the expert
+            # backward, with a workspace of their own
+            self.ws_route_bwd_w = torch.empty(rb, dtype=torch.uint8, device=dev)
+            self._side = None
+            self._side_done = None
 
     # -- pieces --------------------------------------------------------------
     def route(self, x, w_router, bias=None, alive=None, renorm=True):
@@ -172,9 +179,43 @@ class MoELayerPlan:
                           dbias=self.dbias if want_dbias else None, ws=self.ws_route_bwd)
         return self.dx, self.dw_router
 
-    def backward(self, dout, w_gate_up, w_down, expert_map=None, accumulate=False):
+    def route_backward_weights_async(self, x, w_router, want_dbias=False):
+        """dw_router (and dbias) from self.dgate on a side stream, started now:
+        they need only the gate gradient, so they can run beside the expert
+        backward.  route_backward_data waits for them."""
+        if self.dw_router is None:
+            self.dw_router = torch.empty(w_router.shape, dtype=torch.float32, device=self.device)
+            self.dbias = torch.empty(self.E, dtype=torch.float32, device=self.device)
+        if self._side is None:
+            self._side = torch.cuda.Stream(device=self.device)   # default priority
+            self._side_done = torch.cuda.Event()
+        main = torch.cuda.current_stream(self.device)
+        self._side.wait_stream(main)
+        with torch.cuda.stream(self._side):
+            api.moe_route_bwd(self.dgate, self.topk_idx, self.topk_gate, x, w_router,
+                              renorm=True, offsets=self.offsets, row_src=self.row_src,
+                              data=False, dw_router=self.dw_router,
+                              want_dbias=want_dbias, dbias=self.dbias if want_dbias else None,
+                              ws=self.ws_route_bwd_w)
+            self._side_done.record(self._side)
+
+    def route_backward_data(self, x, w_router):
+        """The router's dx, accumulated onto self.dx; then the current stream
+        waits for route_backward_weights_async."""
+        api.moe_route_bwd(self.dgate, self.topk_idx, self.topk_gate, x, w_router, renorm=True,
+                          offsets=self.offsets, row_src=self.row_src, dx=self.dx,
+                          accumulate_dx=True, weights=False, ws=self.ws_route_bwd)
+        torch.cuda.current_stream(self.device).wait_event(self._side_done)
+        return self.dx, self.dw_router
+
+    def backward(self, dout, w_gate_up, w_down, expert_map=None, accumulate=False,
+                 router=None, want_dbias=False):
+        """Expert backward; with router=(x, w_router) (renormalised gates) also
+        the router's, its weight gradients beside the expert backward."""
         api.moe_combine_bwd(dout, self.y_perm, self.topk_gate, self.dest_row,
                             dy_perm=self.dy_perm, dgate=self.dgate)
+        if router is not None:
+            self.route_backward_weights_async(router[0], router[1], want_dbias=want_dbias)
         if self.dw_gate_up is None:
             self.dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32,
                                           device=self.device)
@@ -187,6 +228,8 @@ class MoELayerPlan:
                                 dw_down=self.dw_down, accumulate=accumulate, ws=self.ws_bwd,
                                 dx_perm=self.dx_perm)
         api.moe_permute_bwd(self.dx_perm, self.dest_row, self.T, self.k, out=self.dx)
+        if router is not None:
+            self.route_backward_data(router[0], router[1])
         return self.dx, self.dgate, self.dw_gate_up, self.dw_down
 
 

@@ -176,6 +176,10 @@ def test_route_bwd_validation(L):
     assert call(args(dtype=5)) == 2
     assert call(args(k=9)) == 1
     assert call(args(wsb=16)) == 3
+    assert call(args(dw=None, db=p)) == 1        # dbias comes with dw_router
+    assert "dbias" in _err(L)
+    assert call(args(w=None, dx=None, dw=None)) == 1
+    assert "w_router" in _err(L)
     need = L.moe_workspace_bytes(4, 16, 2, 8, 0, 0)
     assert need >= 16 * 8 * 4
     # the segment partials of the weight gradient grow with d_model

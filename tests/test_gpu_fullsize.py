@@ -279,6 +279,17 @@ def test_routed_training_step_full_size():
     assert rownorm_err(hint(plan.dw_router), rw) <= TOL_F32
     assert rownorm_err(hint(plan.dbias), rb) <= TOL_F32
     assert rownorm_err(h32(plan.dx), rx) <= TOL_BF16
+    # the training step with the router's weight gradients on a side stream,
+    # beside the expert backward: the same bits
+    dx_seq, dw_seq, db_seq = plan.dx.clone(), plan.dw_router.clone(), plan.dbias.clone()
+    dwd_seq = plan.dw_down.clone()
+    case("full-size routed training step, router weight gradients beside the expert backward")
+    plan.forward(x, wr, wgu, wd, renorm=w.renorm)
+    plan.backward(dout, wgu, wd, router=(x, wr), want_dbias=True)
+    torch.cuda.synchronize()
+    assert torch.equal(plan.dx, dx_seq)
+    assert torch.equal(plan.dw_router, dw_seq) and torch.equal(plan.dbias, db_seq)
+    assert torch.equal(plan.dw_down, dwd_seq)
 
 
 def test_pruned_compact_layer_full_size():

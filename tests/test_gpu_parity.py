@@ -655,3 +655,15 @@ def test_route_bwd_parity(T, d, E, k, dtype, renorm, bias, dead):
     assert rownorm_err(host(dw), rw) <= TOL_F32
     assert rownorm_err(host(db), rb) <= TOL_F32
     assert rownorm_err(host(dx), rx) <= (TOL_BF16 if dtype == "bf16" else TOL_F32)
+    # the two halves alone (dx only, weights only) give the same bits
+    dx2 = dev(dx_in, td)
+    d2, w2, b2, l2 = laep.moe_route_bwd(dg, idx, gate, x, wr, renorm=renorm, logits=logits,
+                                        alive=alive, offsets=offsets, row_src=row_src, dx=dx2,
+                                        accumulate_dx=True, want_dlogits=True, weights=False)
+    d3, w3, b3, _ = laep.moe_route_bwd(dg, idx, gate, x, wr, renorm=renorm, logits=logits,
+                                       alive=alive, offsets=offsets, row_src=row_src,
+                                       data=False, want_dbias=True)
+    torch.cuda.synchronize()
+    assert w2 is None and b2 is None and d3 is None
+    assert torch.equal(d2, dx) and torch.equal(l2, dl)
+    assert torch.equal(w3, dw) and torch.equal(b3, db)
