@@ -268,6 +268,11 @@ def test_routed_training_step_full_size():
                              backward=True)
     case("full-size routed training step (balanced_bwd)")
     plan.forward(x, wr, wgu, wd, renorm=w.renorm)
+    # x_perm, written on the side stream beside the gathered FFN, is the permute's
+    xp = laep.moe_permute(x, plan.dest_row, w.k, plan.R)
+    torch.cuda.synchronize()
+    assert torch.equal(plan.x_perm, xp)
+    del xp
     plan.backward(dout, wgu, wd)
     torch.cuda.synchronize()
     dx_expert = h32(plan.dx)
