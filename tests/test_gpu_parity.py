@@ -667,3 +667,52 @@ def test_route_bwd_parity(T, d, E, k, dtype, renorm, bias, dead):
     assert w2 is None and b2 is None and d3 is None
     assert torch.equal(d2, dx) and torch.equal(l2, dl)
     assert torch.equal(w3, dw) and torch.equal(b3, db)
+
+
+def test_zero_rows_everywhere():
+    """No routed rows at all: every call is a no-op on its row outputs, and the
+    weight gradients come out as the empty sums they are (zero, or unchanged
+    when accumulating)."""
+    E, d, f, k = 4, 128, 256, 2
+    bf = torch.bfloat16
+    rng = np.random.default_rng(7)
+    wgu = dev((rng.standard_normal((E, 2 * f, d)) * 0.02).astype(np.float32), bf)
+    wd = dev((rng.standard_normal((E, d, f)) * 0.02).astype(np.float32), bf)
+    wr = dev((rng.standard_normal((E, d)) * 0.02).astype(np.float32), bf)
+    offsets = torch.zeros(E + 1, dtype=torch.int32, device="cuda")
+    x0 = torch.empty((0, d), dtype=bf, device="cuda")
+    case("zero rows: grouped FFN forward / backward")
+    y, act = laep.moe_grouped_ffn_fwd(x0, wgu, wd, offsets)
+    assert y.shape == (0, d) and act.shape == (0, 2 * f)
+    dwgu = torch.full((E, 2 * f, d), 7.0, device="cuda")
+    dwd = torch.full((E, d, f), 7.0, device="cuda")
+    laep.moe_grouped_ffn_bwd(x0, x0, act, wgu, wd, offsets, dw_gate_up=dwgu, dw_down=dwd)
+    torch.cuda.synchronize()
+    assert not dwgu.any() and not dwd.any()
+    dwgu.fill_(7.0), dwd.fill_(7.0)
+    laep.moe_grouped_ffn_bwd(x0, x0, act, wgu, wd, offsets, dw_gate_up=dwgu, dw_down=dwd,
+                             accumulate=True)
+    torch.cuda.synchronize()
+    assert bool((dwgu == 7.0).all()) and bool((dwd == 7.0).all())
+    case("zero tokens: row ops and router backward")
+    idx0 = torch.empty((0, k), dtype=torch.int32, device="cuda")
+    g0 = torch.empty((0, k), dtype=torch.float32, device="cuda")
+    r0 = torch.empty(0, dtype=torch.int32, device="cuda")
+    assert laep.moe_permute(x0, r0, k, 0).shape == (0, d)
+    assert laep.moe_combine(x0, g0, r0).shape == (0, d)
+    dy, dg = laep.moe_combine_bwd(x0, x0, g0, r0)
+    assert dy.shape == (0, d) and dg.shape == (0, k)
+    assert laep.moe_permute_bwd(x0, r0, 0, k).shape == (0, d)
+    dw = torch.full((E, d), 7.0, device="cuda")
+    db = torch.full((E,), 7.0, device="cuda")
+    dx, dw, db, _ = laep.moe_route_bwd(g0, idx0, g0, x0, wr, offsets=offsets, row_src=r0,
+                                       dw_router=dw, want_dbias=True, dbias=db)
+    torch.cuda.synchronize()
+    assert dx.shape == (0, d) and not dw.any() and not db.any()
+    # weights only / data only: nothing else is touched
+    dw.fill_(7.0)
+    _, w_none, _, _ = laep.moe_route_bwd(g0, idx0, g0, x0, wr, offsets=offsets, row_src=r0,
+                                         weights=False)
+    assert w_none is None
+    torch.cuda.synchronize()
+    assert bool((dw == 7.0).all())
