@@ -257,6 +257,9 @@ int laep_repack_experts(const int32_t* expert_map, int E, int n_out, int dtype,
  *   renorm = 0 needs logits [T, E] (moe_route's float32 logits output) and
  *   the alive mask moe_route used (NULL = all alive).
  *   Workspace: moe_workspace_bytes(LAEP_CALL_ROUTE_BWD, T, k, E, d_model, 0).
+ *   Two calls in flight at once (the two halves on two streams) need two
+ *   workspaces.  T = 0: dw_router and dbias (when given) are zero-filled and
+ *   nothing else is touched; the activation pointers may then be NULL.
  */
 int moe_route_bwd(const float* dgate, const int32_t* topk_idx,
                   const float* topk_gate, const float* logits,
