@@ -25,8 +25,11 @@ FFN.  The readings used here:
 
 Rounding points (the layer dtype "bf16" or "f32"; "f64" = none):
 act_save = round(A); H = round(silu(A_g) * A_u) from the unrounded A;
-Y = round(H W_d^T); out = round(sum_j g_j Y_j).  Backward: dH = round(dY W_d)
-before the SwiGLU backward.  Gates, dgate and weight gradients are float32.
+Y = round(H W_d^T); out = round(sum_j g_j Y_j).  Backward: dY = round(g dout);
+dH = dY W_d is kept unrounded into the SwiGLU backward; dA = round(.);
+dX = round(dA W_gu).  The router backward keeps dlogits unrounded into
+dW_r, db and dx.  Gates, dgate, dlogits and weight gradients are returned
+as float32.
 """
 from __future__ import annotations
 
@@ -68,23 +71,51 @@ def topk_gating(logits, k: int, alive=None, renorm: bool = True,
     n_alive = int(alive.sum())
     kk = min(k, n_alive)
     idx = np.full((T, k), -1, dtype=np.int32)
-    gate = np.zeros((T, k), dtype=F64)
     idx[:, :kk] = order[:, :kk]
     sel = np.take_along_axis(masked, order[:, :kk], axis=1)
-    top = sel[:, :1]
-    if renorm:
-        ex = np.exp(sel - top)
-        gate[:, :kk] = ex / ex.sum(axis=1, keepdims=True)
-    else:
-        ex_all = np.where(alive[None, :], np.exp(masked - top), 0.0)
-        gate[:, :kk] = np.exp(sel - top) / ex_all.sum(axis=1, keepdims=True)
-    gate = round_f32(gate)
+    gate = selection_gates(logits, idx, alive=alive, renorm=renorm, decide_f32=False)
     if n_alive > k:
         nxt = np.take_along_axis(masked, order[:, k:k + 1], axis=1)[:, 0]
         margin = sel[:, kk - 1] - nxt
     else:
         margin = np.full(T, np.inf)
     return idx, gate, margin
+
+
+def selection_gates(logits, idx, alive=None, renorm: bool = True,
+                    decide_f32: bool = True) -> np.ndarray:
+    """Gates of a given selection idx [T, k] (slots holding -1 are empty and
+    get gate 0), whether or not it is the top-k:
+
+      renorm=True:  g_j = exp(l_j) / sum over the selected i of exp(l_i)
+      renorm=False: g_j = exp(l_j) / sum over all alive e of exp(l_e)
+
+    evaluated in float64 (shifted by the token's largest logit, which
+    cancels) from the float32-rounded logits, and returned rounded to
+    float32.  ``topk_gating`` takes its gates from here; a routing checker
+    uses it to price an alternative selection at a near-tie.
+    """
+    logits = np.asarray(logits, F64)
+    if decide_f32:
+        logits = round_f32(logits)
+    idx = np.asarray(idx)
+    T, E = logits.shape
+    alive = np.ones(E, bool) if alive is None else np.asarray(alive).astype(bool)
+    masked = np.where(alive[None, :], logits, -np.inf)
+    used = idx >= 0
+    sel = np.where(used, np.take_along_axis(masked, np.where(used, idx, 0), axis=1), -np.inf)
+    if renorm:
+        top = np.max(sel, axis=1, keepdims=True)
+        top = np.where(np.isfinite(top), top, 0.0)
+        ex = np.where(used, np.exp(sel - top), 0.0)
+        den = ex.sum(axis=1, keepdims=True)
+    else:
+        top = np.max(masked, axis=1, keepdims=True)
+        top = np.where(np.isfinite(top), top, 0.0)
+        ex = np.where(used, np.exp(sel - top), 0.0)
+        den = np.where(alive[None, :], np.exp(masked - top), 0.0).sum(axis=1, keepdims=True)
+    gate = ex / np.where(den > 0, den, 1.0)
+    return round_f32(gate)
 
 
 def route(x, w_router, k, bias=None, alive=None, renorm=True):
@@ -110,8 +141,9 @@ def route_bwd(dgate, idx, gate, x, w_router, logits=None, alive=None, renorm: bo
                    alive e; 0 for dead ones.  Needs the logits.
     dW_r = dl^T x and db = sum_t dl (float32);
     dx = round_dtype(dx_in + dl W_r)  (dx_in = 0 when not given).
-    Slots with idx = -1 carry no gradient.
-    Returns (dl rounded to float32 [T, E], dW_r [E, d], db [E], dx [T, d]).
+    Slots with idx = -1 carry no gradient.  dl enters dW_r, db and dx
+    unrounded; it is returned rounded to float32 (the dlogits output).
+    Returns (dl [T, E], dW_r [E, d], db [E], dx [T, d]).
     """
     dgate = np.asarray(dgate, F64)
     idx = np.asarray(idx)
@@ -137,13 +169,12 @@ def route_bwd(dgate, idx, gate, x, w_router, logits=None, alive=None, renorm: bo
         tt, jj = np.nonzero(ok)
         q[tt, idx[tt, jj]] = dgate[tt, jj]
         dl = np.where(alive_m[None, :], p * (q - s[:, None]), 0.0)
-    dl = round_f32(dl)
     dw = round_f32(dl.T @ x)
     db = round_f32(dl.sum(axis=0))
     dx = dl @ w
     if dx_in is not None:
         dx = dx + np.asarray(dx_in, F64)
-    return dl, dw, db, rounder(dtype)(dx)
+    return round_f32(dl), dw, db, rounder(dtype)(dx)
 
 
 # --------------------------------------------------------------------------
@@ -304,11 +335,9 @@ def grouped_ffn_dgrad(dy_perm, act_save, w_gate_up, w_down, offsets,
                       expert_map=None, dtype: str = "bf16", dA_given=None):
     """Data gradient of the grouped FFN.
 
-    Per expert: dH = round(dY W_d); (dA, H_b) = swiglu_bwd(dH, act_save);
-    dX = round(dA W_gu).  (The paper fixes no rounding points; dH is taken
-    in the layer dtype, as the first data-gradient product stores it.)
-    ``dA_given`` (teacher forcing) replaces the dA computed here as the input
-    of dX.  Returns (dx_perm, dA, H_b).
+    Per expert: dH = dY W_d (unrounded); (dA, H_b) = swiglu_bwd(dH,
+    act_save); dX = round(dA W_gu).  ``dA_given`` (teacher forcing) replaces
+    the dA computed here as the input of dX.  Returns (dx_perm, dA, H_b).
     """
     rnd = rounder(dtype)
     R, d = dy_perm.shape
@@ -322,7 +351,7 @@ def grouped_ffn_dgrad(dy_perm, act_save, w_gate_up, w_down, offsets,
         if hi == lo:
             continue
         p = _phys(expert_map, e)
-        dH = rnd(np.asarray(dy_perm[lo:hi], F64) @ np.asarray(w_down[p], F64))
+        dH = np.asarray(dy_perm[lo:hi], F64) @ np.asarray(w_down[p], F64)
         dA[lo:hi], Hb[lo:hi] = swiglu_bwd(dH, act_save[lo:hi], dtype)
         src = dA[lo:hi] if dA_given is None else np.asarray(dA_given[lo:hi], F64)
         dx[lo:hi] = rnd(src @ np.asarray(w_gate_up[p], F64))
@@ -385,7 +414,7 @@ def layer_forward(x, w_router, w_gate_up, w_down, k, bias=None, alive=None,
 
 
 __all__ = [
-    "router_logits", "topk_gating", "route", "expert_counts", "permute",
+    "router_logits", "topk_gating", "selection_gates", "route", "expert_counts", "permute",
     "expert_ffn", "grouped_ffn_fwd", "combine", "combine_bwd", "swiglu_bwd",
     "grouped_ffn_dgrad", "grouped_ffn_wgrad", "permute_bwd", "layer_forward",
     "round_bf16",

@@ -125,3 +125,38 @@ def test_counts_skip_unrouted_slots():
     counts, offsets, dest = moe.expert_counts(idx, 3)
     assert counts.tolist() == [2, 1, 0] and offsets.tolist() == [0, 2, 3, 3]
     assert dest.tolist() == [0, -1, 2, -1, 1, -1]
+
+
+def test_selection_gates_of_any_selection_against_library_softmax():
+    """Gates of an arbitrary selection (not the top-k, in any slot order,
+    with empty slots): scipy's softmax over the selected logits (renorm) or
+    over all alive logits taken at the selected experts (full softmax)."""
+    rng = np.random.default_rng(11)
+    T, E, k = 40, 9, 4
+    logits = rng.standard_normal((T, E)) * 2
+    alive = np.array([1, 0, 1, 1, 1, 1, 0, 1, 1], bool)
+    lf = round_f32(logits)
+    live = np.nonzero(alive)[0]
+    idx = np.stack([rng.permutation(live)[:k] for _ in range(T)]).astype(np.int32)
+    idx[::5, 3] = -1                            # an empty slot in some rows
+    for renorm in (True, False):
+        g = moe.selection_gates(logits, idx, alive=alive, renorm=renorm)
+        for t in range(T):
+            used = idx[t] >= 0
+            if renorm:
+                want = scipy.special.softmax(lf[t, idx[t][used]])
+            else:
+                full = np.full(E, -np.inf)
+                full[alive] = lf[t, alive]
+                want = scipy.special.softmax(full)[idx[t][used]]
+            np.testing.assert_allclose(g[t][used], want, rtol=1e-7)
+            assert np.all(g[t][~used] == 0)
+        # the gates follow the experts, not the slots
+        perm = idx[:, ::-1].copy()
+        np.testing.assert_array_equal(moe.selection_gates(logits, perm, alive=alive,
+                                                          renorm=renorm), g[:, ::-1])
+    # with the top-k selection they are topk_gating's gates
+    ti, tg, _ = moe.topk_gating(logits, k, alive=alive, renorm=True)
+    np.testing.assert_array_equal(moe.selection_gates(logits, ti, alive=alive), tg)
+    # no slot filled: all gates zero
+    assert np.all(moe.selection_gates(logits[:2], np.full((2, k), -1, np.int32)) == 0)
