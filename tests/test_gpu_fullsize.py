@@ -1,7 +1,9 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times (MoELayerPlan).  Integer outputs are checked completely;
-floating-point outputs on sampled rows the oracle computes one by one
-(rows are independent, so a row subset is exact)."""
+floating-point outputs on rows the oracle computes one by one (rows are
+independent, so a row subset is exact): one row from every 32-row block of
+every 256-row tile of every expert, and for the weight gradients whole
+256 x 256 output tiles."""
 import numpy as np
 import pytest
 import torch
@@ -24,13 +26,18 @@ def hint(t):
     return t.detach().cpu().numpy()
 
 
-def _sample_rows(offsets, per_expert=3, seed=0):
+def _block_rows(offsets, block=32, seed=0):
+    """One random row from every `block`-row block of every expert's rows
+    (blocks start at the expert's first row, as its row tiles do), plus
+    each expert's last row."""
     rng = np.random.default_rng(seed)
     rows = []
     for e in range(len(offsets) - 1):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
+        for b in range(lo, hi, block):
+            rows.append(int(rng.integers(b, min(b + block, hi))))
         if hi > lo:
-            rows += [lo, hi - 1] + rng.integers(lo, hi, size=per_expert).tolist()
+            rows.append(hi - 1)
     return np.unique(np.array(rows, np.int64))
 
 
@@ -86,7 +93,8 @@ def test_router_layer_full_size(name):
     ridx, rgate, margin, rlog = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
                                         renorm=w.renorm)
     idx = hint(plan.topk_idx)
-    n_diff, _ = check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k)
+    n_diff, _ = check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k,
+                              renorm=w.renorm, label=f"full-size {name}, first pass")
     print(f"  near-tie tokens routed differently: {n_diff} of {w.T}")
     rc, ro, rd = om.expert_counts(idx, w.E)
     np.testing.assert_array_equal(hint(plan.counts), rc)
@@ -107,7 +115,8 @@ def test_router_layer_full_size(name):
         ridx, rgate, margin, rlog = om.route(c["x"], c["w_router"], w.k, bias=c.get("bias"),
                                             alive=alive, renorm=w.renorm)
         idx = hint(plan.topk_idx)
-        check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k, alive)
+        check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k, alive,
+                      renorm=w.renorm, label=f"full-size {name}, after pruning")
         rc, ro, rd = om.expert_counts(idx, w.E)
         np.testing.assert_array_equal(hint(plan.counts), rc)
         np.testing.assert_array_equal(hint(plan.dest_row), rd)
@@ -121,9 +130,9 @@ def test_router_layer_full_size(name):
     xp = plan.x_perm.view(torch.int16).cpu().numpy()
     xs = x.view(torch.int16).cpu().numpy()
     assert np.array_equal(xp, xs[src])
-    rows = _sample_rows(ro, per_expert=2)
+    rows = _block_rows(ro)
     _check_ffn_rows(plan, c, rows, c["w_gate_up"], c["w_down"])
-    toks = np.random.default_rng(1).choice(w.T, 256, replace=False)
+    toks = np.random.default_rng(1).choice(w.T, 2048, replace=False)
     _check_combine_tokens(plan, toks)
 
 
@@ -148,9 +157,9 @@ def test_shard_forward_full_size():
     np.testing.assert_array_equal(hint(plan.counts), rc)
     np.testing.assert_array_equal(hint(plan.dest_row), rd)
     print(f"  rows per expert: {sorted(rc.tolist())}")
-    rows = _sample_rows(ro, per_expert=2, seed=3)
+    rows = _block_rows(ro, seed=3)
     _check_ffn_rows(plan, c, rows, c["w_gate_up"], c["w_down"])
-    toks = np.random.default_rng(2).choice(w.T, 256, replace=False)
+    toks = np.random.default_rng(2).choice(w.T, 2048, replace=False)
     _check_combine_tokens(plan, toks)
 
 
@@ -185,7 +194,7 @@ def test_shard_backward_full_size():
     # plan hands the backward the forward's H, so the H_b buffer keeps dH
     dA_ws, dh_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
     h_fwd = laep.ffn_fwd_h_view(plan.ws_ffn, R, f, BF)
-    srows = _sample_rows(offsets, per_expert=2, seed=6)
+    srows = _block_rows(offsets, seed=6)
     ts = torch.from_numpy(srows).cuda()
     ex = _expert_of_rows(srows, offsets)
     dy_s, act_s = h32(plan.dy_perm[ts]), h32(plan.act_save[ts])
@@ -201,13 +210,23 @@ def test_shard_backward_full_size():
         assert rownorm_err(dx_s[sel], rdx) <= TOL_BF16
         _, _, rh = om.expert_ffn(xp_s[sel], c["w_gate_up"][e], c["w_down"][e], "bf16")
         assert rownorm_err(h_s[sel], rh) <= TOL_BF16
-    # wgrad on sampled output rows, teacher-forced on the GPU's dA / forward H
+    # wgrad, teacher-forced on the GPU's dA / forward H: per expert one whole
+    # 256 x 256 output tile of dW_gu and of dW_d, and three full output rows
     case("full-size wgrad checks")
     dwgu, dwd = plan.dw_gate_up, plan.dw_down
+    TB = 256
     for e in range(w.E):
         lo, hi = int(offsets[e]), int(offsets[e + 1])
         if hi == lo:
             continue
+        i0, j0 = TB * int(rng.integers(2 * f // TB)), TB * int(rng.integers(d // TB))
+        dA_t = h32(dA_ws[lo:hi, i0:i0 + TB]).astype(np.float64)
+        x_t = h32(plan.x_perm[lo:hi, j0:j0 + TB]).astype(np.float64)
+        assert rownorm_err(h32(dwgu[e, i0:i0 + TB, j0:j0 + TB]), dA_t.T @ x_t) <= TOL_F32, e
+        i0, j0 = TB * int(rng.integers(d // TB)), TB * int(rng.integers(f // TB))
+        dy_t = h32(plan.dy_perm[lo:hi, i0:i0 + TB]).astype(np.float64)
+        h_t = h32(h_fwd[lo:hi, j0:j0 + TB]).astype(np.float64)
+        assert rownorm_err(h32(dwd[e, i0:i0 + TB, j0:j0 + TB]), dy_t.T @ h_t) <= TOL_F32, e
         tr = torch.arange(lo, hi, device="cuda")
         i_d = rng.choice(d, 3, replace=False)
         i_g = rng.choice(2 * f, 3, replace=False)
@@ -339,11 +358,12 @@ def test_pruned_compact_layer_full_size():
     ridx, rgate, _, rlog = om.route(c["x"], c["w_router"][keep], w.k, bias=c["bias"][keep],
                                     renorm=w.renorm)
     idx = hint(plan.topk_idx)
-    check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k)
+    check_routing(idx, hint(plan.topk_gate), ridx, rgate, rlog, w.k, renorm=w.renorm,
+                  label="full-size mild_pruned, compact layer")
     rc2, ro2, rd2 = om.expert_counts(idx, E2)
     np.testing.assert_array_equal(hint(plan.counts), rc2)
     np.testing.assert_array_equal(hint(plan.dest_row), rd2)
-    rows = _sample_rows(ro2, per_expert=2)
+    rows = _block_rows(ro2)
     _check_ffn_rows(plan, c, rows, c["w_gate_up"][keep], c["w_down"][keep])
-    toks = np.random.default_rng(2).choice(w.T, 256, replace=False)
+    toks = np.random.default_rng(2).choice(w.T, 2048, replace=False)
     _check_combine_tokens(plan, toks)

@@ -52,7 +52,7 @@ def test_route_parity(T, d, E, k, dtype, renorm, bias):
     c = random_case(T * 7 + E, T=T, d_model=d, E=E, k=k, d_ff=64, dtype=dtype, bias_std=bias,
                     weight_std=0.05)
     idx, gate, logits, ridx, rgate, margin, rlog = _route_case(c, k, dtype, renorm)
-    check_routing(idx, gate, ridx, rgate, rlog, k)
+    check_routing(idx, gate, ridx, rgate, rlog, k, renorm=renorm)
     assert rownorm_err(logits, rlog) <= TOL_F32
 
 
@@ -538,7 +538,7 @@ def test_tiny_layer_end_to_end():
     ref = om.layer_forward(c["x"], c["w_router"], c["w_gate_up"], c["w_down"], w.k,
                            renorm=w.renorm, dtype="f32")
     check_routing(host(plan.topk_idx), host(plan.topk_gate), ref["idx"], ref["gate"],
-                  ref["logits"], w.k)
+                  ref["logits"], w.k, renorm=w.renorm)
     ok = np.all(host(plan.topk_idx) == ref["idx"], axis=1)
     assert rownorm_err(host(out)[ok], ref["out"][ok]) <= TOL_F32
 
@@ -585,7 +585,7 @@ def test_layer_fuzz(seed):
     torch.cuda.synchronize()
     ridx, rgate, _, rlog = om.route(c["x"], c["w_router"], k, bias=bias, alive=alive,
                                    renorm=renorm)
-    check_routing(host(idx), host(gate), ridx, rgate, rlog, k, alive)
+    check_routing(host(idx), host(gate), ridx, rgate, rlog, k, alive, renorm=renorm)
     gi, gg = host(idx), host(gate)
     rc, ro, rd = om.expert_counts(gi, E)
     np.testing.assert_array_equal(host(counts), rc)
