@@ -81,6 +81,15 @@ _lock = threading.Lock()
 _lib = None
 
 
+def bind(handle):
+    """Apply the C signatures to a loaded handle of the library."""
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    return handle
+
+
 def lib():
     """The loaded library (raises if it was not built)."""
     global _lib
@@ -91,12 +100,7 @@ def lib():
                     raise RuntimeError(
                         f"{LIB_PATH} is missing: build it with `python -c 'import "
                         f"__graft_entry__ as g; g.build()'` (no fallback implementation exists)")
-                handle = ctypes.CDLL(LIB_PATH)
-                for name, (res, args) in SIGNATURES.items():
-                    fn = getattr(handle, name)
-                    fn.restype = res
-                    fn.argtypes = args
-                _lib = handle
+                _lib = bind(ctypes.CDLL(LIB_PATH))
     return _lib
 
 

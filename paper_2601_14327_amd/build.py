@@ -80,5 +80,69 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# ---------------------------------------------------------------------------
+# Host sanitizer build (CPU checking only; never loaded by the product path).
+# The host-only sources (argument validation, workspace sizing, the side
+# streams, the rearrangement utility) are compiled with clang's address and
+# undefined-behaviour sanitizers and linked with the ordinary HIP objects of
+# build(), whose device code is untouched.  tests/test_host_sanitizers.py runs
+# the C-ABI contract tests against the result with the sanitizer runtime
+# preloaded.
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+             "-fno-omit-frame-pointer", "-g", "-O1"]
+
+
+def _clangxx() -> str:
+    for cand in ("/opt/rocm/llvm/bin/clang++", shutil.which("clang++")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("clang++ not found (needed for the host sanitizer build)")
+
+
+def sanitizer_runtime() -> str:
+    """Path of clang's shared address-sanitizer runtime (to preload)."""
+    cxx = _clangxx()
+    r = subprocess.run([cxx, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                       stdout=subprocess.PIPE, text=True, check=True)
+    path = r.stdout.strip()
+    if not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("clang's shared ASan runtime was not found")
+    return path
+
+
+def build_host_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """liblaep_moe_hostsan.so in out_dir: host sources under ASan + UBSan,
+    HIP objects as build() made them (built first when missing)."""
+    cxx = _clangxx()
+    os.makedirs(out_dir, exist_ok=True)
+    hip_objs = [os.path.join(BUILD, src + ".o") for src in HIP_SOURCES]
+    if not all(os.path.exists(o) for o in hip_objs):
+        build(verbose=verbose)
+    inc = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include"]
+    jobs, san_objs = [], []
+    for src in HIP_HOST_SOURCES + CXX_SOURCES:
+        obj = os.path.join(out_dir, src + ".san.o")
+        san_objs.append(obj)
+        jobs.append([cxx, "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", *SAN_FLAGS,
+                     *inc, "-c", os.path.join(CSRC, src), "-o", obj])
+    with concurrent.futures.ThreadPoolExecutor(len(jobs)) as ex:
+        results = list(ex.map(_compile, jobs))
+    for rc, cmd, out in results:
+        if verbose or rc != 0:
+            print(cmd)
+            print(out)
+        if rc != 0:
+            raise RuntimeError("host sanitizer build: compilation failed")
+    lib_out = os.path.join(out_dir, "liblaep_moe_hostsan.so")
+    rc, cmd, out = _compile([cxx, "-shared", "-fPIC", *SAN_FLAGS, "-shared-libasan", *san_objs,
+                             *hip_objs, "-L/opt/rocm/lib", "-lamdhip64",
+                             "-Wl,-rpath,/opt/rocm/lib", "-o", lib_out])
+    if rc != 0:
+        print(cmd)
+        print(out)
+        raise RuntimeError("host sanitizer build: link failed")
+    return lib_out
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -18,6 +18,13 @@ HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.jo
 def L():
     import paper_2601_14327_amd as laep
 
+    # tests/test_host_sanitizers.py reruns this module against the host
+    # sanitizer build of the library
+    alt = os.environ.get("LAEP_ABI_TEST_LIB")
+    if alt:
+        from paper_2601_14327_amd._lib import bind
+
+        return bind(ctypes.CDLL(alt))
     if not os.path.exists(laep.LIB_PATH):
         from paper_2601_14327_amd import build
 
@@ -212,6 +219,16 @@ def test_workspace_sizes_are_monotone(L):
     assert L.moe_workspace_bytes(0, 1024, 1, 16, 256, 256) == 0
 
 
+def _rearrange(L, loads, ng):
+    loads = np.ascontiguousarray(loads, dtype=np.float64)
+    n = loads.shape[0]
+    group_of, order = np.empty(n, np.int32), np.empty(n, np.int32)
+    sums = np.empty(max(ng, 1), np.float64)
+    rc = L.laep_rearrange(loads.ctypes.data, n, ng, group_of.ctypes.data, order.ctypes.data,
+                          sums.ctypes.data)
+    return rc, dict(group_of=group_of, order=order, sums=sums[:ng])
+
+
 def test_rearrange_matches_oracle(L):
     from oracle import laep as olaep
     from paper_2601_14327_amd import laep_rearrange
@@ -221,8 +238,13 @@ def test_rearrange_matches_oracle(L):
     for _ in range(200):
         n = int(rng.integers(1, 80))
         cases.append((rng.integers(0, 1000, n).astype(float).tolist(), int(rng.integers(1, n + 1))))
-    for loads, ng in cases:
-        got = laep_rearrange(loads, ng)
+    for i, (loads, ng) in enumerate(cases):
+        rc, got = _rearrange(L, loads, ng)
+        assert rc == 0
+        if i < 3:   # the Python binding gives the same placement
+            b = laep_rearrange(loads, ng)
+            for key in got:
+                np.testing.assert_array_equal(b[key], got[key])
         want = olaep.rearrange(loads, ng)
         np.testing.assert_array_equal(got["group_of"], want["group_of"])
         np.testing.assert_array_equal(got["order"], want["order"])
@@ -234,6 +256,11 @@ def test_rearrange_errors(L):
 
     with pytest.raises(LaepError):
         laep_rearrange([1.0, 2.0], 0)
+    assert _rearrange(L, [1.0, 2.0], 0)[0] == 1
+    assert L.laep_rearrange(None, 3, 2, None, None, None) == 1
+    # no experts: valid, the group sums are zero
+    rc, got = _rearrange(L, [], 3)
+    assert rc == 0 and np.all(got["sums"] == 0)
 
 
 def test_expert_pruning_validation(L):
