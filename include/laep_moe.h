@@ -300,6 +300,9 @@ int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T,
  *   Constraints: d_model % 64 == 0, d_ff % 64 == 0, R < 2^31; bf16: one
  *   expert's w_gate_up under 2 GiB (4*d_ff*d_model bytes), since the GEMMs
  *   address it with 32-bit offsets (LAEP_ERR_UNSUPPORTED otherwise).
+ *   LAEP_BF16 runs on the bf16 matrix cores (fp32 accumulation).  LAEP_F32
+ *   is a plain fp32 FMA loop (no matrix cores), meant for small parity
+ *   layers, not for speed; its backward is not implemented.
  *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff)
  *   (holds H and the tile table; on return H [R, d_ff] (dtype) is at byte
  *   offset 0, which moe_grouped_ffn_bwd can take as h_fwd).
@@ -369,7 +372,7 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  * moe_grouped_ffn_bwd -- backward of moe_grouped_ffn_fwd (data and weight
  * gradients), evaluated at the saved pre-activations act_save (Â):
  *
- *   dH   = dY W_d[p]
+ *   dH   = dY W_d[p]          (stored in dtype between the two steps)
  *   dA_g = dH * Â_u * s * (1 + Â_g (1 - s)),  s = sigmoid(Â_g)
  *   dA_u = dH * silu(Â_g)                      dA = round([dA_g, dA_u])
  *   H_b  = round(silu(Â_g) * Â_u)
@@ -389,7 +392,7 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  *   On return the workspace holds dA [R, 2*d_ff] (dtype) at byte offset 0 and,
  *   at byte offset laep_ws_hb_offset(R, d_ff, dtype), H_b [R, d_ff] (dtype)
  *   when h_fwd is NULL, else dH.
- *   Only LAEP_BF16 is supported.
+ *   Only LAEP_BF16 is supported (LAEP_F32 -> LAEP_ERR_UNSUPPORTED).
  *   Streams: the weight gradients run on the library-owned side stream of the
  *   current device (one per device, created on the first call that uses it,
  *   default priority, kept until the process ends), forked

@@ -442,8 +442,7 @@ hipError_t launch_ffn_fwd_products(const void* x_perm, const void* w_gu, const v
   char* tables = static_cast<char*>(ws) + align_up((size_t)R * f * 2, 256);
   TableWs tgu = carve_table(tables, max_gu);
   TableWs td = carve_table(tables + table_bytes(max_gu), max_d);
-  // default: all row tiles of an expert in one group (column-block-major)
-  const int group = tile_group("LAEP_TILE_GROUP_FWD", 1 << 20);
+  const int group = kFwdTileGroup;
   TileList lgu = {nt_gu, group, max_gu, tgu.n_entries, tgu.table};
   TileList ld = {nt_d, group, max_d, td.n_entries, td.table};
   const int list_blocks = ceil_div(max_gu > max_d ? max_gu : max_d, kTableThreads);

@@ -486,7 +486,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   hipLaunchKernelGGL(build_table_kernel, dim3(1), dim3(kTableThreads), 0, s, offsets, expert_map,
                      E, kBwdBM, 1, E, te.n_entries, te.table);
 
-  const int group = tile_group("LAEP_TILE_GROUP_BWD", 8);
+  const int group = kBwdTileGroup;
   // weight gradients: dW_d[p] [d, f] = dY^T H over the expert's rows (H: the
   // forward's when given, else H_b), dW_gu[p] [2f, d] = dA^T X
   GemmParams wd = {};

@@ -5,8 +5,6 @@
 #include "internal.hpp"
 #include "tiles.hpp"
 
-#include <cstdlib>
-
 namespace laep {
 namespace {
 
@@ -42,13 +40,12 @@ struct GemmParams {
   int group;               // row tiles per rasterisation group (backward products)
 };
 
-// Row tiles per rasterisation group of the tile orders: `fallback` unless the
-// environment variable `name` holds a positive integer (a tuning override).
-inline int tile_group(const char* name, int fallback) {
-  const char* v = getenv(name);
-  const int g = v ? atoi(v) : 0;
-  return g > 0 ? g : fallback;
-}
+// Row tiles per rasterisation group of the tile orders.  Forward: all row
+// tiles of an expert in one group (column-block-major within the expert).
+// Backward: groups of 8 row tiles (a sweep of 2-32 measured 2-8 alike, 16
+// and more slower: too many weight panels of column blocks in flight).
+constexpr int kFwdTileGroup = 1 << 20;
+constexpr int kBwdTileGroup = 8;
 
 __device__ __forceinline__ void store_bf16x4(bf16_t* p, float a, float b, float c, float d) {
   u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
