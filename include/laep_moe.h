@@ -142,6 +142,36 @@ int moe_route_count(const void* x, const void* w_router, const float* bias,
                     void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * moe_route_count_noalloc -- moe_route_count for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, minus the workspace; outputs are
+ * bit-identical to moe_route_count's (the same kernels).
+ *
+ *   The counting scratch (moe_workspace_bytes(LAEP_CALL_COUNTS, T, k, E, 0, 0)
+ *   bytes) lives in a library-owned device array of
+ *   LAEP_NOALLOC_SCRATCH_BYTES bytes per GPU, held until the process ends.
+ *   The call makes no allocation of any kind (its first call on a device
+ *   only looks the array's address up).  The scratch is fully written before
+ *   it is read, so stale contents from an earlier call do not matter.
+ *   Errors: a shape whose scratch exceeds LAEP_NOALLOC_SCRATCH_BYTES ->
+ *   LAEP_ERR_WORKSPACE before anything is enqueued (8 MiB hold the counting
+ *   scratch of up to 691840 tokens at E = 64, 172928 at E = 256); otherwise
+ *   as moe_route_count.
+ *   Concurrency: every call on one GPU shares that GPU's array.  Calls that
+ *   overlap in time on one GPU (different streams, or different host
+ *   threads without ordering) race on it and give undefined results;
+ *   serialise them, e.g. on one stream.
+ */
+#define LAEP_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+int moe_route_count_noalloc(const void* x, const void* w_router,
+                            const float* bias, const uint8_t* alive, int dtype,
+                            int T, int d_model, int E, int k, int renorm,
+                            float* logits, int32_t* topk_idx, float* topk_gate,
+                            int32_t* counts, int32_t* offsets,
+                            int32_t* dest_row, int32_t* row_src,
+                            int64_t* etn_accum, void* stream);
+
+/*
  * laep_prune_mask -- the LAEP prune decision for one layer and one counted
  * batch (Section 3.2, Eqs. (1) and (2); Algorithm 1, Step 2 with ITER = 1).
  *

@@ -44,6 +44,7 @@ from .api import (  # noqa: F401
     moe_route,
     moe_route_bwd,
     moe_route_count,
+    moe_route_count_noalloc,
     workspace_bytes,
 )
 from .layer import MoELayerPlan, layer_forward  # noqa: F401

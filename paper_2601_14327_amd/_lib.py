@@ -53,6 +53,8 @@ SIGNATURES = {
     "moe_expert_counts": (_i, [_p, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "moe_route_count": (_i, [_p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _p,
                              _p, _p, _sz, _p]),
+    "moe_route_count_noalloc": (_i, [_p, _p, _p, _p, _i, _i, _i, _i, _i, _i, _p, _p, _p, _p, _p,
+                                     _p, _p, _p, _p]),
     "laep_prune_mask": (_i, [_p, _i, _i64, _d, _d, _p, _p, _p]),
     "laep_expert_pruning": (_i, [_p, _i, _i, _i, _i64, _p, _d, _p, _p, _p, _p]),
     "laep_compact_experts": (_i, [_p, _i, _i, _p, _p, _p]),

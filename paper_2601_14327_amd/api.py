@@ -164,6 +164,37 @@ def moe_route_count(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=Non
     return topk_idx, topk_gate, counts, offsets, dest_row, row_src, logits
 
 
+def moe_route_count_noalloc(x: torch.Tensor, w_router: torch.Tensor, k: int, *, bias=None,
+                            alive=None, renorm: bool = True, want_logits: bool = False,
+                            want_row_src: bool = False, etn_accum=None, topk_idx=None,
+                            topk_gate=None, counts=None, offsets=None, dest_row=None,
+                            row_src=None, logits=None):
+    """moe_route_count with the library's own scratch array (no workspace;
+    the C call allocates nothing).  Pass every output to keep this wrapper
+    allocation-free too.  Returns as moe_route_count."""
+    _dev(x, "x"), _dev(w_router, "w_router")
+    T, d = x.shape
+    E = w_router.shape[0]
+    dev = x.device
+    i32 = torch.int32
+    topk_idx = torch.empty((T, k), dtype=i32, device=dev) if topk_idx is None else topk_idx
+    topk_gate = (torch.empty((T, k), dtype=torch.float32, device=dev) if topk_gate is None
+                 else topk_gate)
+    counts = torch.empty(E, dtype=i32, device=dev) if counts is None else counts
+    offsets = torch.empty(E + 1, dtype=i32, device=dev) if offsets is None else offsets
+    dest_row = torch.empty(T * k, dtype=i32, device=dev) if dest_row is None else dest_row
+    if want_row_src and row_src is None:
+        row_src = torch.empty(T * k, dtype=i32, device=dev)
+    if want_logits and logits is None:
+        logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    check(lib().moe_route_count_noalloc(_ptr(x), _ptr(w_router), _ptr(bias), _ptr(alive),
+                                        _dtype_code(x), T, d, E, k, int(renorm), _ptr(logits),
+                                        _ptr(topk_idx), _ptr(topk_gate), _ptr(counts),
+                                        _ptr(offsets), _ptr(dest_row), _ptr(row_src),
+                                        _ptr(etn_accum), _stream(dev)))
+    return topk_idx, topk_gate, counts, offsets, dest_row, row_src, logits
+
+
 def laep_prune_mask(counts: torch.Tensor, total: int, alpha: float = math.inf,
                     beta: float = 0.0, *, alive=None, n_pruned=None):
     """LAEP prune decision.  Returns (alive [E] uint8, n_pruned [1] int32)."""

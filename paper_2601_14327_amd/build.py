@@ -18,7 +18,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblaep_moe.so")
 
 HIP_SOURCES = ["route.hip", "route_bwd.hip", "counts.hip", "prune.hip", "compact.hip", "rowops.hip",
-               "gemm_bf16.hip", "gemm_bwd.hip", "gemm_f32.hip", "calib.hip"]
+               "gemm_bf16.hip", "gemm_bwd.hip", "gemm_f32.hip", "calib.hip", "noalloc.hip"]
 HIP_HOST_SOURCES = ["api.cpp", "streams.cpp"]   # host code that calls the HIP runtime
 CXX_SOURCES = ["rearrange.cpp"]         # plain host C++
 

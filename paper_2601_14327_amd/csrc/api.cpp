@@ -160,27 +160,35 @@ int moe_expert_counts(const int32_t* topk_idx, int T, int k, int E, int32_t* cou
                     "moe_expert_counts");
 }
 
-int moe_route_count(const void* x, const void* w_router, const float* bias, const uint8_t* alive,
-                    int dtype, int T, int d_model, int E, int k, int renorm, float* logits,
-                    int32_t* topk_idx, float* topk_gate, int32_t* counts, int32_t* offsets,
-                    int32_t* dest_row, int32_t* row_src, int64_t* etn_accum, void* ws,
-                    size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// argument checks shared by moe_route_count and moe_route_count_noalloc
+int check_route_count(const char* name, const void* x, const void* w_router, int dtype, int T,
+                      int d_model, int E, int k, const int32_t* topk_idx, const float* topk_gate,
+                      const int32_t* counts, const int32_t* offsets, const int32_t* dest_row) {
   int rc = check_dtype(dtype);
   if (rc) return rc;
   if ((rc = check_experts(E, k))) return rc;
   if ((rc = check_rows(T, k, d_model))) return rc;
-  REQUIRE(counts && offsets, LAEP_ERR_INVALID_ARG,
-          "moe_route_count: counts and offsets must be non-null");
+  REQUIRE(counts && offsets, LAEP_ERR_INVALID_ARG, "%s: counts and offsets must be non-null",
+          name);
   if (T > 0) {
     REQUIRE(x && w_router && topk_idx && topk_gate && dest_row, LAEP_ERR_INVALID_ARG,
-            "moe_route_count: x, w_router, topk_idx, topk_gate and dest_row must be non-null");
+            "%s: x, w_router, topk_idx, topk_gate and dest_row must be non-null", name);
     REQUIRE(aligned16(x) && aligned16(w_router), LAEP_ERR_INVALID_ARG,
-            "moe_route_count: x and w_router must be 16-byte aligned");
+            "%s: x and w_router must be 16-byte aligned", name);
   }
-  const size_t need = laep::counts_ws_bytes(T, k, E);
-  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_route_count: workspace %zu < %zu bytes",
-          ws_bytes, need);
-  REQUIRE(need == 0 || ws, LAEP_ERR_INVALID_ARG, "moe_route_count: ws must be non-null");
+  return LAEP_OK;
+}
+
+// the launches of the fused route + count call, on a checked workspace
+int route_count_launch(const char* name, const void* x, const void* w_router, const float* bias,
+                       const uint8_t* alive, int dtype, int T, int d_model, int E, int k,
+                       int renorm, float* logits, int32_t* topk_idx, float* topk_gate,
+                       int32_t* counts, int32_t* offsets, int32_t* dest_row, int32_t* row_src,
+                       int64_t* etn_accum, void* ws, void* stream) {
   const hipStream_t s = as_stream(stream);
   hipError_t e = laep::launch_route(x, w_router, bias, alive, dtype, T, d_model, E, k,
                                     renorm != 0, logits, topk_idx, topk_gate,
@@ -188,7 +196,54 @@ int moe_route_count(const void* x, const void* w_router, const float* bias, cons
   if (e == hipSuccess)
     e = laep::launch_counts(topk_idx, T, k, E, counts, offsets, dest_row, row_src, etn_accum, ws,
                             s, /*masks_ready=*/true);
-  return hip_status(e, "moe_route_count");
+  return hip_status(e, name);
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_route_count(const void* x, const void* w_router, const float* bias, const uint8_t* alive,
+                    int dtype, int T, int d_model, int E, int k, int renorm, float* logits,
+                    int32_t* topk_idx, float* topk_gate, int32_t* counts, int32_t* offsets,
+                    int32_t* dest_row, int32_t* row_src, int64_t* etn_accum, void* ws,
+                    size_t ws_bytes, void* stream) {
+  int rc = check_route_count("moe_route_count", x, w_router, dtype, T, d_model, E, k, topk_idx,
+                             topk_gate, counts, offsets, dest_row);
+  if (rc) return rc;
+  const size_t need = laep::counts_ws_bytes(T, k, E);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE, "moe_route_count: workspace %zu < %zu bytes",
+          ws_bytes, need);
+  REQUIRE(need == 0 || ws, LAEP_ERR_INVALID_ARG, "moe_route_count: ws must be non-null");
+  return route_count_launch("moe_route_count", x, w_router, bias, alive, dtype, T, d_model, E, k,
+                            renorm, logits, topk_idx, topk_gate, counts, offsets, dest_row,
+                            row_src, etn_accum, ws, stream);
+}
+
+static_assert(laep::kNoAllocScratchBytes == LAEP_NOALLOC_SCRATCH_BYTES,
+              "the header states the scratch array's size");
+
+int moe_route_count_noalloc(const void* x, const void* w_router, const float* bias,
+                            const uint8_t* alive, int dtype, int T, int d_model, int E, int k,
+                            int renorm, float* logits, int32_t* topk_idx, float* topk_gate,
+                            int32_t* counts, int32_t* offsets, int32_t* dest_row,
+                            int32_t* row_src, int64_t* etn_accum, void* stream) {
+  int rc = check_route_count("moe_route_count_noalloc", x, w_router, dtype, T, d_model, E, k,
+                             topk_idx, topk_gate, counts, offsets, dest_row);
+  if (rc) return rc;
+  const size_t need = laep::counts_ws_bytes(T, k, E);
+  REQUIRE(need <= laep::kNoAllocScratchBytes, LAEP_ERR_WORKSPACE,
+          "moe_route_count_noalloc: T=%d, E=%d need %zu bytes of scratch, more than the "
+          "library's %zu-byte array (use moe_route_count with a workspace)",
+          T, E, need, laep::kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    const hipError_t e = laep::noalloc_scratch(&ws);
+    if (e != hipSuccess) return hip_status(e, "moe_route_count_noalloc: scratch lookup");
+  }
+  return route_count_launch("moe_route_count_noalloc", x, w_router, bias, alive, dtype, T,
+                            d_model, E, k, renorm, logits, topk_idx, topk_gate, counts, offsets,
+                            dest_row, row_src, etn_accum, ws, stream);
 }
 
 int laep_prune_mask(const int32_t* counts, int E, int64_t total, double alpha, double beta,

@@ -42,6 +42,12 @@ hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* count
 // the expert-mask area of the counting workspace (uint64 [ceil(T/64)][E])
 uint32_t* counts_masks(void* ws);
 
+// Scratch of the allocation-free route + count call: a static device array of
+// this many bytes per GPU (csrc/noalloc.hip).  noalloc_scratch() returns its
+// device address on the current device (looked up once per device).
+constexpr size_t kNoAllocScratchBytes = size_t(8) << 20;
+hipError_t noalloc_scratch(void** out);
+
 hipError_t launch_prune(const int32_t* counts, int E, int64_t total, double alpha, double beta,
                         uint8_t* alive, int32_t* n_pruned, hipStream_t s);
 constexpr int kMaxLayers = 256;

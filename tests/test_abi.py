@@ -304,3 +304,22 @@ def test_compact_and_repack_validation(L):
     assert "aligned" in _err(L)
     # nothing to copy: valid, and enqueues nothing
     assert rp(p, 8, 0, 1, 64, 64, p, None, p, p, p, None, p, p, None) == 0
+
+
+def test_route_count_noalloc_validation(L):
+    """The allocation-free route + count call: the same argument checks as
+    moe_route_count, and shapes whose counting scratch exceeds the library's
+    array are rejected before anything is enqueued."""
+    keep, p = _fake()
+    call = lambda T, E, k, x=p, dtype=1, d=64: L.moe_route_count_noalloc(
+        x, p, None, None, dtype, T, d, E, k, 1, None, p, p, p, p, p, None, None, None)
+    assert call(16, 8, 9) == 1 and "k=9" in _err(L)
+    assert call(16, 8, 2, dtype=7) == 2
+    assert call(16, 8, 2, x=None) == 1 and "moe_route_count_noalloc" in _err(L)
+    assert call(16, 8, 2, x=p + 2) == 1 and "aligned" in _err(L)
+    limit = 8 << 20
+    assert L.moe_workspace_bytes(1, 691840, 8, 64, 0, 0) <= limit
+    assert L.moe_workspace_bytes(1, 691841 + 63, 8, 64, 0, 0) > limit
+    assert call(700000, 64, 8) == 3
+    assert "scratch" in _err(L) and "moe_route_count" in _err(L)
+    assert call(200000, 256, 8) == 3
