@@ -31,6 +31,15 @@ Prints ONE JSON line:
   cpu_baseline the float64 CPU oracle timed on a bounded token sample (all BLAS
                threads, and one thread on a smaller sample)
   warm         the step with the same input set every step
+  settle       untimed steps run before the warmup until the step time is
+               steady (the GPU's clocks ramp up over the first ~1 s of load)
+  placement    expert rearrangement (Algorithm 2, laep_rearrange) of the
+               per-expert loads the last step counted, into 8 device groups:
+               group sums of the greedy and of the contiguous placement, the
+               straggler factor max/mean of each, a lower bound and, for at
+               most 16 experts, the exact optimum
+  padding      rows of the FFN's 256-row tiles beyond the routed rows
+               (sum over experts of ceil(M_e / 256) * 256 - R)
 
 Other workloads: skewed, skewed_mild (routed, pruned every step), shard (16
 experts, given Zipf routing), shard_bwd (shard forward + backward),
@@ -291,6 +300,56 @@ class Setup:
         by["route_count_masked"] = by["route_count"]
         fl = {"ffn_fwd": 6.0 * R * d * f, "ffn_bwd": 12.0 * R * d * f}
         return by, fl
+
+
+def _settle(su, min_s=1.0, max_s=6.0, batch=10, tol=0.01):
+    """Untimed steps until the step time is steady: batches of `batch` steps,
+    at least `min_s` seconds, until two consecutive batch means agree within
+    `tol` (or `max_s` seconds).  Returns (steps, seconds)."""
+    import torch
+
+    t_start = time.perf_counter()
+    prev, n = None, 0
+    while True:
+        t0 = time.perf_counter()
+        for i in range(batch):
+            for _, fn in su.calls(n + i):
+                fn()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / batch
+        n += batch
+        el = time.perf_counter() - t_start
+        if el >= max_s or (el >= min_s and prev is not None and abs(dt - prev) <= tol * prev):
+            return n, round(el, 2)
+        prev = dt
+
+
+def _placement(su, n_groups=8):
+    """Algorithm 2 on the loads the last step counted (alive experts only)."""
+    import numpy as np
+
+    counts = su.plan.counts.cpu().numpy().astype(np.float64)
+    ids = np.arange(counts.shape[0])
+    if getattr(su.plan, "alive", None) is not None and su.w.prune_beta is not None \
+            and not su.w.prune_window:
+        ids = np.nonzero(su.plan.alive.cpu().numpy().astype(bool))[0]
+    elif su.keep is not None:       # compact layer: name the survivors by their old ids
+        ids = np.asarray(su.keep)
+    loads = counts[:len(ids)] if su.keep is not None else counts[ids]
+    rep = su.laep.placement_report(loads, n_groups, expert_ids=ids)
+    rep["source"] = "per-expert routed rows counted by the last step (moe counts)"
+    return rep
+
+
+def _padding(su, bm=256):
+    import numpy as np
+
+    counts = su.plan.counts.cpu().numpy().astype(np.int64)
+    R = int(counts.sum())
+    padded = int((-(-counts // bm) * bm).sum())
+    return {"tile_rows": bm, "routed_rows": R, "padded_rows": padded,
+            "waste_rows": padded - R, "waste_frac": round((padded - R) / max(padded, 1), 4),
+            "experts_with_rows": int((counts > 0).sum())}
 
 
 def _stats(v):
@@ -554,6 +613,7 @@ def main():
     su = Setup(w, dev)
     stream = torch.cuda.current_stream(dev)
 
+    settle_steps, settle_s = _settle(su)
     for i in range(args.warmup):
         for _, fn in su.calls(i):
             fn()
@@ -601,6 +661,8 @@ def main():
     torch.cuda.synchronize()
     warm_ms = (time.perf_counter() - t1) * 1e3 / args.steps
 
+    placement = _placement(su)
+    padding = _padding(su)
     by, fl = su.algorithmic()
     breakdown = {}
     for j, n in enumerate(names):
@@ -660,6 +722,9 @@ def main():
         "warm": {"ms_per_step": warm_ms, "value": w.T / (warm_ms * 1e-3),
                  "note": "same input set every step"},
         "pruning": su.pruning,
+        "settle": {"steps": settle_steps, "seconds": settle_s},
+        "placement": placement,
+        "padding": padding,
         "supplementary": supp,
         "breakdown": breakdown,
     }

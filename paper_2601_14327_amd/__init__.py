@@ -48,4 +48,5 @@ from .api import (  # noqa: F401
     workspace_bytes,
 )
 from .layer import MoELayerPlan, layer_forward  # noqa: F401
+from .placement import placement_report  # noqa: F401
 from .pruning import ExpertPruner, compact_layer, hybrid_alpha  # noqa: F401
