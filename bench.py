@@ -9,9 +9,9 @@ dispatch folded into the FFN's operand loads) -> combine, every call a kernel
 of the C-ABI library; three input sets rotate over the steps so the
 activations are not cache-resident.  With one slot per token (shard,
 shard_bwd) the combine folds into the FFN call as well (the down projection
-writes each row, times its gate, to its token row).  Training steps keep
-x_perm, which the weight gradient reads: with k = 1 the FFN call writes it by a
-copy beside its products, for k > 1 the permute writes it.
+writes each row, times its gate, to its token row).  Training steps write no
+x_perm either: the weight gradient gathers the token rows through row_src as
+well.
 
 Prints ONE JSON line:
   value        tokens/s of the whole step (wall clock over the timed steps,
@@ -239,15 +239,13 @@ class Setup:
                                                            dest_row=p.dest_row,
                                                            row_src=p.row_src))]
             gate = self.gate
-        # training plans keep x_perm (the weight gradient reads it): with k = 1 the
-        # FFN call writes it by a copy beside its products
         if p.fused_combine:   # one slot per token: dispatch and combine folded into the FFN
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather_combine(
                 x, p.row_src, gate, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
                 out=p.out, keep_y=p.y_perm is not None, y_perm=p.y_perm,
                 save_act=p.act_save is not None, act_save=p.act_save, x_perm_out=p.x_perm))]
         elif p.fused:   # dispatch folded into the FFN's operand loads
-            if p.x_perm is not None:   # k > 1: the token-major permute reads x once
+            if p.x_perm is not None:   # kept for inspection: the token-major permute
                 out += [("permute", lambda: L.moe_permute(x, p.dest_row, w.k, R, out=p.x_perm))]
             out += [("ffn_fwd", lambda: L.moe_grouped_ffn_fwd_gather(
                 x, p.row_src, w.k, self.wgu, self.wd, p.offsets, rows=R, ws=p.ws_ffn,
@@ -269,7 +267,11 @@ class Setup:
                                                               dgate=p.dgate))]
             if w.routed:   # the router's weight gradients on a side stream, beside the FFN's
                 out += [("route_bwd_w", lambda: p.route_backward_weights_async(x, self.wr))]
-            out += [("ffn_bwd", lambda: L.moe_grouped_ffn_bwd(
+            out += [("ffn_bwd", lambda: L.moe_grouped_ffn_bwd_gather(
+                        p.dy_perm, x, p.row_src, w.k, p.act_save, self.wgu, self.wd,
+                        p.offsets, h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
+                        dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,
+                        dx_perm=p.dx_perm) if p.fused else L.moe_grouped_ffn_bwd(
                         p.dy_perm, p.x_perm, p.act_save, self.wgu, self.wd, p.offsets,
                         h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
                         dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,

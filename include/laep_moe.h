@@ -440,6 +440,30 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
                         int accumulate,
                         void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * moe_grouped_ffn_bwd_gather -- moe_grouped_ffn_bwd with the dispatch folded
+ * into the weight gradient (the backward half of the expert-parallel
+ * dispatch, Section 3.3): dW_gu = dA^T X reads routed row r of X straight
+ * from token row row_src[r] / k of x, so the dispatched rows x_perm are never
+ * needed.  Results are bit-identical to moe_permute followed by
+ * moe_grouped_ffn_bwd.
+ *
+ *   x device [T, d_model] bf16; row_src device [R] int32 (as
+ *   moe_expert_counts writes it, every entry in [0, T*k)); the other
+ *   arguments, the workspace and the streams are those of moe_grouped_ffn_bwd.
+ *   dtype must be LAEP_BF16 and x under 2 GiB (T*d_model*2 bytes: its rows
+ *   are addressed with 32-bit offsets); LAEP_ERR_UNSUPPORTED otherwise.
+ */
+int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x,
+                               const int32_t* row_src, int T, int k,
+                               const void* act_save, const void* h_fwd,
+                               const void* w_gate_up, const void* w_down,
+                               const int32_t* offsets, const int32_t* expert_map,
+                               int dtype, int E, int d_model, int d_ff, int64_t R,
+                               void* dx_perm, float* dw_gate_up, float* dw_down,
+                               int accumulate, void* ws, size_t ws_bytes,
+                               void* stream);
+
 /* Byte offset of H_b inside the moe_grouped_ffn_bwd workspace. */
 size_t laep_ws_hb_offset(int64_t R, int d_ff, int dtype);
 

@@ -36,6 +36,7 @@ from .api import (  # noqa: F401
     moe_combine_bwd,
     moe_expert_counts,
     moe_grouped_ffn_bwd,
+    moe_grouped_ffn_bwd_gather,
     moe_grouped_ffn_fwd,
     moe_grouped_ffn_fwd_gather,
     moe_grouped_ffn_fwd_gather_combine,

@@ -409,6 +409,38 @@ def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *
     return out + (ws,) if return_ws else out
 
 
+def moe_grouped_ffn_bwd_gather(dy_perm, x, row_src, k: int, act_save, w_gate_up, w_down,
+                               offsets, *, h_fwd=None, expert_map=None, dw_gate_up=None,
+                               dw_down=None, accumulate=False, ws=None, dx_perm=None,
+                               return_ws: bool = False):
+    """moe_grouped_ffn_bwd with the weight gradient reading X's routed rows
+    from the token rows x through row_src (no x_perm).  Returns as
+    moe_grouped_ffn_bwd."""
+    for t, n in ((dy_perm, "dy_perm"), (x, "x"), (row_src, "row_src"), (act_save, "act_save"),
+                 (w_gate_up, "w_gate_up"), (w_down, "w_down"), (offsets, "offsets")):
+        _dev(t, n)
+    if h_fwd is not None:
+        _dev(h_fwd, "h_fwd")
+    T, d = x.shape
+    R = dy_perm.shape[0]
+    f = w_down.shape[2]
+    E = offsets.shape[0] - 1
+    dev = x.device
+    dx_perm = torch.empty_like(dy_perm) if dx_perm is None else dx_perm
+    if dw_gate_up is None:
+        dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32, device=dev)
+    if dw_down is None:
+        dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=dev)
+    ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d, f), dev)
+    check(lib().moe_grouped_ffn_bwd_gather(
+        _ptr(dy_perm), _ptr(x), _ptr(row_src), T, k, _ptr(act_save), _ptr(h_fwd),
+        _ptr(w_gate_up), _ptr(w_down), _ptr(offsets), _ptr(expert_map), _dtype_code(x), E, d, f,
+        R, _ptr(dx_perm), _ptr(dw_gate_up), _ptr(dw_down), int(accumulate), _ptr(ws), ws.numel(),
+        _stream(dev)))
+    out = (dx_perm, dw_gate_up, dw_down)
+    return out + (ws,) if return_ws else out
+
+
 def ffn_fwd_h_view(ws: torch.Tensor, R: int, d_ff: int, dtype: torch.dtype):
     """H [R, f] as the forward leaves it in its workspace (byte offset 0)."""
     esz = torch.empty((), dtype=dtype).element_size()

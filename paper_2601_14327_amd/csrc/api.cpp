@@ -514,6 +514,40 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act
                     "moe_grouped_ffn_bwd");
 }
 
+int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x, const int32_t* row_src, int T,
+                               int k, const void* act_save, const void* h_fwd,
+                               const void* w_gate_up, const void* w_down, const int32_t* offsets,
+                               const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
+                               int64_t R, void* dx_perm, float* dw_gate_up, float* dw_down,
+                               int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_ffn_shape(dtype, E, d_model, d_ff, R);
+  if (rc) return rc;
+  REQUIRE(dtype == LAEP_BF16, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_bwd_gather: only LAEP_BF16 is supported");
+  REQUIRE(T >= 0 && k >= 1, LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd_gather: T=%d, k=%d", T, k);
+  REQUIRE(R <= (int64_t)T * k, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_bwd_gather: R=%lld exceeds T*k", (long long)R);
+  REQUIRE((int64_t)T * d_model * 2 < kMaxBufferBytes, LAEP_ERR_UNSUPPORTED,
+          "moe_grouped_ffn_bwd_gather: x (T*d_model bf16) must be under 2 GiB");
+  REQUIRE(offsets && dw_gate_up && dw_down && ws, LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_bwd_gather: offsets, dw_gate_up, dw_down and ws must be non-null");
+  REQUIRE(R == 0 || (dy_perm && x && row_src && act_save && w_gate_up && w_down && dx_perm),
+          LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_bwd_gather: activation pointers and row_src must be non-null");
+  REQUIRE(aligned16(dy_perm) && aligned16(x) && aligned16(act_save) && aligned16(h_fwd) &&
+              aligned16(w_gate_up) && aligned16(w_down) && aligned16(dx_perm) &&
+              aligned16(dw_gate_up) && aligned16(dw_down) && aligned16(ws),
+          LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd_gather: buffers must be 16-byte aligned");
+  const size_t need = laep::ffn_bwd_ws_bytes(R, E, d_model, d_ff, dtype);
+  REQUIRE(ws_bytes >= need, LAEP_ERR_WORKSPACE,
+          "moe_grouped_ffn_bwd_gather: workspace %zu < %zu bytes", ws_bytes, need);
+  return hip_status(laep::launch_ffn_bwd_bf16(dy_perm, x, act_save, h_fwd, w_gate_up, w_down,
+                                              offsets, expert_map, E, d_model, d_ff, R, dx_perm,
+                                              dw_gate_up, dw_down, accumulate != 0, ws,
+                                              as_stream(stream), row_src, k, T),
+                    "moe_grouped_ffn_bwd_gather");
+}
+
 int moe_combine(const void* y_perm, const float* topk_gate, const int32_t* dest_row, int T, int k,
                 int d_model, int dtype, void* out, void* stream) {
   int rc = check_dtype(dtype);

@@ -27,6 +27,14 @@
 // with streaming (non-temporal) stores: every output (dA, H_b, dX, the fp32
 // weight gradients) is far larger than the caches (measured 3 % faster on the
 // backward call).
+//
+// Gathered X (the dispatch folded into the weight gradient): dW_gu = dA^T X
+// can read X's routed row r straight from token row row_src[r] / k of x, so
+// x_perm is never written.  The k-rows of a k-step are then different token
+// rows at every step: each thread loads the row_src entries of its 4 k-rows
+// one k-step ahead, issued before that iteration's LDS-DMA halves, so the
+// in-order vmcnt waits of the ring still cover them.  Rows past the expert's
+// end get an offset beyond x's buffer range and read as zeros.
 #include <type_traits>
 
 #include "gemm_common.hpp"
@@ -61,9 +69,20 @@ __device__ __forceinline__ int tr_off(int r, int mf, int gh, int i) {
   return r * 512 + ((lblock ^ ((r & 7) << 1)) << 5) + ((i & 3) << 3);
 }
 
+// The transposed read through a restrict-qualified pointer, so the read
+// carries alias-scope information.  Without it the compiler cannot tell the
+// read from the LDS-DMA writes in flight and drains every outstanding load
+// (vmcnt(0)) before the first read of each k-step, which serialises the
+// ring's prefetch.  The ring's explicit vmcnt waits and barriers already
+// order a slot's DMA writes before its reads (as for the plain reads of the
+// K-contiguous fragments, which never drew that wait).
+__device__ __forceinline__ s16x4_t ds_read_tr(lds_s16x4_t* __restrict__ p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+}
+
 __device__ __forceinline__ u32x4_t read_tr_frag(const char* st, int off1, int off2) {
-  const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(st + off1));
-  const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(st + off2));
+  const s16x4_t a = ds_read_tr((lds_s16x4_t*)(st + off1));
+  const s16x4_t b = ds_read_tr((lds_s16x4_t*)(st + off2));
   const u32x2_t ua = __builtin_bit_cast(u32x2_t, a);
   const u32x2_t ub = __builtin_bit_cast(u32x2_t, b);
   u32x4_t v = {ua[0], ua[1], ub[0], ub[1]};
@@ -91,8 +110,9 @@ __device__ __forceinline__ void dma_half(char* dst, const char* base, uint32_t e
                                              16, voff[i], 0, 0, 0);
 }
 
-template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR>
+template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR, bool B_GATHER>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) {
+  static_assert(!B_GATHER || EPI == EPI_WGRAD, "only the weight gradient gathers its B rows");
   constexpr int NT = 64 * NWM * NWN;
   constexpr int WTM = BM / NWM, WTN = BN / NWN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -177,6 +197,8 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   // B is K-strided in every backward product: [K][N] rows, feature nt*BN + col
   // (clamped to the last valid column block)
   uint32_t b_voff[NH];
+  int b_kr[NH];   // gathered B: k-row of chunk i within a k-step, and its column bytes
+  uint32_t b_cb[NH];
 #pragma unroll
   for (int i = 0; i < NH; ++i) {
     const int q = i * NT + tid;
@@ -185,9 +207,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     int c = nt * BN + col;
     c = c < p.N ? c : p.N - 8;
     b_voff[i] = (uint32_t)(((long long)r * p.ldb + c) * 2);
+    b_kr[i] = r;
+    b_cb[i] = (uint32_t)(c * 2);
   }
   const char* b_tile = reinterpret_cast<const char*>(
-      (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb : p.B + (long long)te.phys * p.strideB);
+      B_GATHER ? p.B
+               : (EPI == EPI_WGRAD) ? p.B + (long long)te.row0 * p.ldb
+                                    : p.B + (long long)te.phys * p.strideB);
   const long long b_kstep = 128LL * p.ldb;
   // half h: A of k-step h/2 (h even) or B (h odd), in slot h % 5.  Past the
   // end the last k-step is loaded again (never read), so every iteration
@@ -204,6 +230,34 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     if (h & 1) dma_half<NH, NT>(dst, b_tile + b_kstep * ks, extent(ks, p.ldb), b_voff, wave);
     else dma_half<NH, NT>(dst, a_tile + a_kstep * ks, A_TR ? extent(ks, p.lda) : 0xffffffffu,
                           a_voff, wave);
+  };
+  // gathered B: the row_src entries of this thread's k-rows of step ks and a
+  // mask of the valid ones (rows past the expert, and the reloads past the
+  // last step, are not); then the DMA offsets they give (invalid rows fall
+  // outside x's buffer range).  Branch-free, and the loaded entries are only
+  // used at the next k-step, so no wait follows the loads: every load reads
+  // an entry of the expert's rows, and the validity is applied at use.
+  auto gather_idx = [&](int ks, uint32_t* raw, uint32_t& okm) {
+    okm = 0;
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const int kr = ks * 64 + b_kr[i];
+      const bool ok = ks < nk && kr < kext;
+      raw[i] = (uint32_t)p.row_src[te.row0 + (ok ? kr : 0)];
+      okm |= ok ? (1u << i) : 0u;
+    }
+  };
+  auto gather_voff = [&](const uint32_t* raw, uint32_t okm, uint32_t* v) {
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const uint32_t off = (raw[i] / (uint32_t)p.slots_k) * (uint32_t)p.ldb * 2u + b_cb[i];
+      v[i] = (okm >> i) & 1u ? off : 0x80000000u;
+    }
+  };
+  auto issue_b_gathered = [&](int h, const uint32_t* raw, uint32_t okm) {
+    uint32_t v[NH];
+    gather_voff(raw, okm, v);
+    dma_half<NH, NT>(smem + (h % kRingSlots) * kRingHalf, b_tile, p.b_extent, v, wave);
   };
 
   // ---- fragment offsets within a half, k16 sub-step 0 -------------------------------
@@ -270,8 +324,21 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     };
 
     // prologue: halves 0 .. 4 in flight, step 0 (halves 0, 1) landed
+    uint32_t idx_next[NH], ok_next = 0;  // gathered B: row_src of the next B half to issue
+    if constexpr (B_GATHER) {
+      uint32_t idx0[NH], idx1[NH], ok0, ok1;
+      gather_idx(0, idx0, ok0);
+      gather_idx(1, idx1, ok1);
+      gather_idx(2, idx_next, ok_next);
+      issue_half(0);
+      issue_b_gathered(1, idx0, ok0);
+      issue_half(2);
+      issue_b_gathered(3, idx1, ok1);
+      issue_half(4);
+    } else {
 #pragma unroll
-    for (int h = 0; h < kRingSlots; ++h) issue_half(h);
+      for (int h = 0; h < kRingSlots; ++h) issue_half(h);
+    }
     wait_vmcnt<3 * NH>();
     __builtin_amdgcn_s_barrier();
     int ia = 0, ib = 1;  // slots of the current step's A and B halves
@@ -291,7 +358,18 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       // two halves of step kt are free: they receive B of kt+2 and A of kt+3.
       wait_vmcnt_lgkm0<NH>();
       __builtin_amdgcn_s_barrier();
-      issue_half(2 * kt + 5);
+      if constexpr (B_GATHER) {
+        // the offsets of B(kt + 2) from the entries loaded last iteration; the
+        // entries of step kt + 3 are loaded before this iteration's halves,
+        // so the next boundary's wait covers them
+        uint32_t v[NH];
+        gather_voff(idx_next, ok_next, v);
+        gather_idx(kt + 3, idx_next, ok_next);
+        dma_half<NH, NT>(smem + ((2 * kt + 5) % kRingSlots) * kRingHalf, b_tile, p.b_extent, v,
+                         wave);
+      } else {
+        issue_half(2 * kt + 5);
+      }
       issue_half(2 * kt + 6);
       ia = ia + 2 >= kRingSlots ? ia + 2 - kRingSlots : ia + 2;
       ib = ib + 2 >= kRingSlots ? ib + 2 - kRingSlots : ib + 2;
@@ -447,11 +525,11 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restri
 
 constexpr int kBwdBM = 256, kBwdBN = 256;
 
-template <int EPI, bool A_TR>
+template <int EPI, bool A_TR, bool B_GATHER = false>
 hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, EPI, A_TR>), dim3(round8(grid)),
-                     dim3(512), 0, s, p);
+  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, EPI, A_TR, B_GATHER>),
+                     dim3(round8(grid)), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 
@@ -473,7 +551,8 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                                const void* h_fwd, const void* w_gu, const void* w_d,
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* dx_perm, float* dw_gu, float* dw_d,
-                               int accumulate, void* ws, hipStream_t s) {
+                               int accumulate, void* ws, hipStream_t s, const int32_t* row_src,
+                               int slots_k, int64_t x_rows) {
   char* base = static_cast<char*>(ws);
   bf16_t* dA = reinterpret_cast<bf16_t*>(base);
   bf16_t* Hb = reinterpret_cast<bf16_t*>(base + ffn_bwd_hb_offset(R, f, kDtypeBf16));
@@ -508,8 +587,11 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   GemmParams wg = wd;
   wg.A = dA;
   wg.lda = 2 * f;
-  wg.B = static_cast<const bf16_t*>(x_perm);
+  wg.B = static_cast<const bf16_t*>(x_perm);   // token rows x when gathering
   wg.ldb = d;
+  wg.row_src = row_src;
+  wg.slots_k = slots_k;
+  wg.b_extent = (uint32_t)(x_rows * d * 2);
   wg.Mw = 2 * f;
   wg.N = d;
   wg.n_tiles_n = ceil_div(d, kBwdBN);
@@ -559,7 +641,9 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   // dA (and H_b) ready: the remaining weight gradients on the side stream
   if (err == hipSuccess) err = fork();
   if (err == hipSuccess && !h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
-  if (err == hipSuccess) err = launch_bwd<EPI_WGRAD, true>(wg, E * wg.tiles_per_entry, s2);
+  if (err == hipSuccess)
+    err = row_src ? launch_bwd<EPI_WGRAD, true, true>(wg, E * wg.tiles_per_entry, s2)
+                  : launch_bwd<EPI_WGRAD, true>(wg, E * wg.tiles_per_entry, s2);
 
   // dgrad 2: dX = dA W_gu
   g.A = dA;

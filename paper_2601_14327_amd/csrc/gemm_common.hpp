@@ -38,6 +38,9 @@ struct GemmParams {
   const float* gate;
   bf16_t* out_tok;
   int group;               // row tiles per rasterisation group (backward products)
+  // weight gradient with the B operand gathered (dW_gu = dA^T X with X's
+  // routed row r read from token row row_src[r] / slots_k of B): bytes of B
+  uint32_t b_extent;
 };
 
 // Row tiles per rasterisation group of the tile orders.  Forward: all row

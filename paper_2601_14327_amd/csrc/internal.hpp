@@ -94,13 +94,16 @@ hipError_t launch_ffn_fwd_f32(const void* x_perm, const void* w_gu, const void* 
 size_t ffn_bwd_ws_bytes(int64_t R, int E, int d, int f, int dtype);
 size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype);
 // h_fwd != NULL: dW_d uses the forward's H (and starts beside data-gradient 1);
-// else H_b, recomputed at the saved pre-activations
+// else H_b, recomputed at the saved pre-activations.
+// row_src != NULL: x_perm is the token rows x [x_rows, d] and the weight
+// gradient reads routed row r from token row row_src[r] / slots_k.
 hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
                                const void* h_fwd, const void* w_gu, const void* w_d,
                                const int32_t* offsets,
                                const int32_t* expert_map, int E, int d, int f, int64_t R,
                                void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
-                               void* ws, hipStream_t s);
+                               void* ws, hipStream_t s, const int32_t* row_src = nullptr,
+                               int slots_k = 1, int64_t x_rows = 0);
 
 // Router backward.
 size_t route_bwd_ws_bytes(int T, int k, int E, int d_model);

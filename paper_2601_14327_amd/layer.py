@@ -8,14 +8,15 @@ Forward (given routing, one device's expert shard with k = 1):
     moe_expert_counts -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
 With fused dispatch (bf16, the default), moe_permute + moe_grouped_ffn_fwd
 become one moe_grouped_ffn_fwd_gather call that reads the token rows through
-row_src.  Where x_perm is kept (the backward's weight gradient reads it),
-moe_permute still writes it for k > 1; with k = 1 the FFN call writes it by a
-copy beside its products.
+row_src, and the backward's weight gradient reads them the same way
+(moe_grouped_ffn_bwd_gather), so a training step never writes x_perm.  A
+forward that keeps its activations for inspection (save_act without a
+backward) still writes x_perm.
 With one slot per token (k = 1) the combine folds in as well
 (moe_grouped_ffn_fwd_gather_combine): the down projection writes each row,
 times its gate, to its token row; y_perm is written only for a backward pass.
 Backward:
-    moe_combine_bwd -> moe_grouped_ffn_bwd -> moe_permute_bwd
+    moe_combine_bwd -> moe_grouped_ffn_bwd[_gather] -> moe_permute_bwd
       [-> moe_route_bwd, accumulating the router's dx]   (router path)
 In a training step the router's weight gradients need only the gate gradient:
 backward(router=...) runs them on a side stream beside the expert backward and
@@ -56,14 +57,15 @@ class MoELayerPlan:
         self.n_pruned = torch.empty(1, dtype=i32, device=dev)
         # pre-activations are kept when a backward pass will read them (or on request)
         save_act = backward if save_act is None else save_act
-        # the dispatch folds into the FFN's operand loads (bf16); x_perm is still
-        # kept where the weight gradient (or a caller) reads it, written by the
-        # FFN call beside its products
+        # the dispatch folds into the FFN's operand loads (bf16), forward and
+        # backward; x_perm is kept only unfused, or for a forward that keeps its
+        # activations without a backward (inspection)
         if fused_dispatch is None:
             fused_dispatch = dtype == torch.bfloat16
         self.fused = bool(fused_dispatch)
-        self.x_perm = (None if self.fused and not (backward or save_act) else
+        self.x_perm = (None if self.fused and (backward or not save_act) else
                        torch.empty((R, d_model), dtype=dtype, device=dev))
+        self.x_in = None   # the token rows of the last forward (the gathered backward reads them)
         # the dispatch order is kept when the FFN gathers through it or the
         # router backward sums dW_r over it
         self.row_src = (torch.empty(R, dtype=i32, device=dev) if self.fused or backward
@@ -123,6 +125,7 @@ class MoELayerPlan:
                             n_pruned=self.n_pruned)
 
     def experts_and_combine(self, x, w_gate_up, w_down, expert_map=None):
+        self.x_in = x
         if self.fused_combine:
             api.moe_grouped_ffn_fwd_gather_combine(
                 x, self.row_src, self.topk_gate, w_gate_up, w_down, self.offsets, rows=self.R,
@@ -132,8 +135,8 @@ class MoELayerPlan:
                 x_perm_out=self.x_perm)
             return self.out
         if self.fused:
-            # k > 1: x_perm (when kept) by the token-major permute, which reads each
-            # token row once; a row-order copy beside the FFN would read it k times
+            # x_perm (kept for inspection only) by the token-major permute, which
+            # reads each token row once
             if self.x_perm is not None:
                 api.moe_permute(x, self.dest_row, self.k, self.R, out=self.x_perm)
             api.moe_grouped_ffn_fwd_gather(x, self.row_src, self.k, w_gate_up, w_down,
@@ -222,11 +225,18 @@ class MoELayerPlan:
             self.dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=self.device)
         # dW_d from the H the forward computed (left in its workspace)
         h_fwd = api.ffn_fwd_h_view(self.ws_ffn, self.R, self.f, self.dtype)
-        api.moe_grouped_ffn_bwd(self.dy_perm, self.x_perm, self.act_save, w_gate_up, w_down,
-                                self.offsets, h_fwd=h_fwd, expert_map=expert_map,
-                                dw_gate_up=self.dw_gate_up,
-                                dw_down=self.dw_down, accumulate=accumulate, ws=self.ws_bwd,
-                                dx_perm=self.dx_perm)
+        if self.fused:   # the weight gradient gathers X from the forward's token rows
+            api.moe_grouped_ffn_bwd_gather(self.dy_perm, self.x_in, self.row_src, self.k,
+                                           self.act_save, w_gate_up, w_down, self.offsets,
+                                           h_fwd=h_fwd, expert_map=expert_map,
+                                           dw_gate_up=self.dw_gate_up, dw_down=self.dw_down,
+                                           accumulate=accumulate, ws=self.ws_bwd,
+                                           dx_perm=self.dx_perm)
+        else:
+            api.moe_grouped_ffn_bwd(self.dy_perm, self.x_perm, self.act_save, w_gate_up,
+                                    w_down, self.offsets, h_fwd=h_fwd, expert_map=expert_map,
+                                    dw_gate_up=self.dw_gate_up, dw_down=self.dw_down,
+                                    accumulate=accumulate, ws=self.ws_bwd, dx_perm=self.dx_perm)
         api.moe_permute_bwd(self.dx_perm, self.dest_row, self.T, self.k, out=self.dx)
         if router is not None:
             self.route_backward_data(router[0], router[1])

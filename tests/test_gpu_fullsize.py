@@ -194,12 +194,16 @@ def test_shard_backward_full_size():
     # plan hands the backward the forward's H, so the H_b buffer keeps dH
     dA_ws, dh_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
     h_fwd = laep.ffn_fwd_h_view(plan.ws_ffn, R, f, BF)
+    # the plan keeps no x_perm (the weight gradient gathers the token rows):
+    # the dispatched rows, for the checks, by indexing here
+    assert plan.x_perm is None
+    xg = x[(plan.row_src.long() // w.k)]
     srows = _block_rows(offsets, seed=6)
     ts = torch.from_numpy(srows).cuda()
     ex = _expert_of_rows(srows, offsets)
     dy_s, act_s = h32(plan.dy_perm[ts]), h32(plan.act_save[ts])
     dA_s, dh_s, dx_s = h32(dA_ws[ts]), h32(dh_ws[ts]), h32(plan.dx_perm[ts])
-    xp_s, h_s = h32(plan.x_perm[ts]), h32(h_fwd[ts])
+    xp_s, h_s = h32(xg[ts]), h32(h_fwd[ts])
     for e in np.unique(ex):
         sel = ex == e
         dH = dy_s[sel].astype(np.float64) @ c["w_down"][e].astype(np.float64)
@@ -221,7 +225,7 @@ def test_shard_backward_full_size():
             continue
         i0, j0 = TB * int(rng.integers(2 * f // TB)), TB * int(rng.integers(d // TB))
         dA_t = h32(dA_ws[lo:hi, i0:i0 + TB]).astype(np.float64)
-        x_t = h32(plan.x_perm[lo:hi, j0:j0 + TB]).astype(np.float64)
+        x_t = h32(xg[lo:hi, j0:j0 + TB]).astype(np.float64)
         assert rownorm_err(h32(dwgu[e, i0:i0 + TB, j0:j0 + TB]), dA_t.T @ x_t) <= TOL_F32, e
         i0, j0 = TB * int(rng.integers(d // TB)), TB * int(rng.integers(f // TB))
         dy_t = h32(plan.dy_perm[lo:hi, i0:i0 + TB]).astype(np.float64)
@@ -235,7 +239,7 @@ def test_shard_backward_full_size():
         ref_d = dy_e.T @ h_e
         assert rownorm_err(h32(dwd[e][torch.from_numpy(i_d).cuda()]), ref_d) <= TOL_F32
         dA_e = h32(dA_ws[tr][:, torch.from_numpy(i_g).cuda()]).astype(np.float64)
-        x_e = h32(plan.x_perm[tr]).astype(np.float64)
+        x_e = h32(xg[tr]).astype(np.float64)
         ref_g = dA_e.T @ x_e
         assert rownorm_err(h32(dwgu[e][torch.from_numpy(i_g).cuda()]), ref_g) <= TOL_F32
     # permute backward (k = 1: a gather back to token order)
@@ -287,14 +291,20 @@ def test_routed_training_step_full_size():
                              backward=True)
     case("full-size routed training step (balanced_bwd)")
     plan.forward(x, wr, wgu, wd, renorm=w.renorm)
-    # x_perm, written on the side stream beside the gathered FFN, is the permute's
-    xp = laep.moe_permute(x, plan.dest_row, w.k, plan.R)
-    torch.cuda.synchronize()
-    assert torch.equal(plan.x_perm, xp)
-    del xp
+    assert plan.x_perm is None      # the weight gradient gathers the token rows
     plan.backward(dout, wgu, wd)
     torch.cuda.synchronize()
     dx_expert = h32(plan.dx)
+    # the gathered backward equals the permute + unfused backward bit for bit
+    case("full-size gathered backward vs permute + unfused backward (balanced_bwd)")
+    xp = laep.moe_permute(x, plan.dest_row, w.k, plan.R)
+    h_fwd = laep.ffn_fwd_h_view(plan.ws_ffn, plan.R, w.d_ff, BF)
+    dxp, dwgu_u, dwd_u = laep.moe_grouped_ffn_bwd(plan.dy_perm, xp, plan.act_save, wgu, wd,
+                                                  plan.offsets, h_fwd=h_fwd)
+    torch.cuda.synchronize()
+    assert torch.equal(dxp, plan.dx_perm)
+    assert torch.equal(dwgu_u, plan.dw_gate_up) and torch.equal(dwd_u, plan.dw_down)
+    del xp, dxp, dwgu_u, dwd_u
     plan.route_backward(x, wr, renorm=w.renorm, want_dbias=True)
     torch.cuda.synchronize()
     rl, rw, rb, rx = om.route_bwd(hint(plan.dgate).astype(np.float64), hint(plan.topk_idx),

@@ -375,6 +375,61 @@ def test_ffn_fwd_gather_matches_permute_then_ffn(T, k, E, d, f, mapped):
     assert rownorm_err(host(a2), ract) <= TOL_BF16
 
 
+@pytest.mark.parametrize("T,k,E,d,f,mapped", [
+    (300, 4, 8, 256, 128, False),    # ragged tiles, top-4, an empty expert
+    (257, 1, 3, 128, 256, False),    # one slot per token
+    (700, 8, 12, 192, 192, True),    # expert_map with unused slots, f % 128 = 64
+    (90, 2, 5, 64, 64, False),       # experts shorter than one 64-row k-step
+    (1500, 6, 8, 128, 128, False),   # long experts: many k-steps of gathered rows
+])
+def test_ffn_bwd_gather_matches_permute_then_bwd(T, k, E, d, f, mapped):
+    """The weight gradient reading X's routed rows from the token rows through
+    row_src (moe_grouped_ffn_bwd_gather) is bit-identical to moe_permute +
+    moe_grouped_ffn_bwd, with and without the forward's H, and its weight
+    gradients match the oracle (teacher-forced on the GPU's dA and H)."""
+    rng = np.random.default_rng(3 * T + E)
+    n_phys = E + 2 if mapped else E
+    c = random_case(T + 3 * E, T=T, d_model=d, E=n_phys, k=1, d_ff=f, dtype="bf16")
+    w = np.r_[3.0, np.ones(E - 2), 0.0] if E > 2 else np.ones(E)
+    ids = np.stack([rng.choice(E, size=k, replace=False, p=w / w.sum()) for _ in range(T)])
+    bf = torch.bfloat16
+    x, wgu, wd = dev(c["x"], bf), dev(c["w_gate_up"], bf), dev(c["w_down"], bf)
+    emap_h = np.array([e + 2 for e in range(E)], np.int32) if mapped else None
+    emap = dev(emap_h, torch.int32) if mapped else None
+    idx = dev(ids.astype(np.int32), torch.int32)
+    case(f"ffn bwd gather T={T} k={k} E={E} d={d} f={f} mapped={mapped}")
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+    R = T * k
+    x_perm = laep.moe_permute(x, dest_row, k)
+    ws_f = torch.empty(laep.workspace_bytes(laep.LAEP_CALL_FFN_FWD, R, 1, E, d, f),
+                       dtype=torch.uint8, device="cuda")
+    _, act = laep.moe_grouped_ffn_fwd(x_perm, wgu, wd, offsets, expert_map=emap, ws=ws_f,
+                                      save_act=True)
+    h_f = laep.ffn_fwd_h_view(ws_f, R, f, bf)
+    dy = dev(rng.standard_normal((R, d)).astype(np.float32), bf)
+    zeros = lambda t: torch.zeros(t.shape, dtype=torch.float32, device="cuda")
+    for use_h in (False, True):
+        h = h_f if use_h else None
+        a = laep.moe_grouped_ffn_bwd(dy, x_perm, act, wgu, wd, offsets, h_fwd=h,
+                                     expert_map=emap, dw_gate_up=zeros(wgu), dw_down=zeros(wd))
+        b = laep.moe_grouped_ffn_bwd_gather(dy, x, row_src, k, act, wgu, wd, offsets, h_fwd=h,
+                                            expert_map=emap, dw_gate_up=zeros(wgu),
+                                            dw_down=zeros(wd), return_ws=True)
+        torch.cuda.synchronize()
+        for n, u, g in zip(("dx_perm", "dw_gate_up", "dw_down"), a, b[:3]):
+            assert torch.equal(u, g), f"{n} differs (use_h={use_h})"
+    # weight gradients against the oracle, on the oracle's dispatched rows
+    dA_g, _ = laep.ffn_bwd_ws_views(b[3], R, f, bf)
+    rc, ro, rdst = om.expert_counts(ids, E)
+    xp = om.permute(c["x"], rdst, k)
+    rgu, rdd = om.grouped_ffn_wgrad(host(dy), xp, host(dA_g), host(h_f), ro, n_phys,
+                                    expert_map=emap_h)
+    got_gu, got_d = host(b[1]), host(b[2])
+    for p in range(n_phys):
+        assert rownorm_err(got_gu[p], rgu[p]) <= TOL_F32, p
+        assert rownorm_err(got_d[p], rdd[p]) <= TOL_F32, p
+
+
 @pytest.mark.parametrize("T,E,d,f,mapped,keep_y", [
     (300, 8, 256, 128, False, False),   # ragged tiles, an empty expert
     (1, 3, 128, 256, False, True),      # a single token
