@@ -115,14 +115,29 @@ __device__ __forceinline__ void argmax_step(float& bv, int& be) {
   be = take ? oe : be;
 }
 
-template <int NCH>
-__device__ __forceinline__ void route_dma(char* dst, const bf16_t* const* src, int k0, int wave) {
+// fourth word of a raw buffer resource: 32-bit data format, no swizzle
+constexpr int kRouteBufferFlags = 0x00020000;
+
+// One stage of LDS-DMA loads through buffer loads with the LDS flag: chunk i
+// of this thread at byte voff[i] + soff of its operand's buffer (x or W_r,
+// chosen per chunk and wave: each wave's 64 chunks lie in the same operand).
+// The buffer form matters: with the global-segment form of the same copy the
+// compiler cannot tell the DMA's LDS writes from the stage reads and waits
+// for every load in flight (vmcnt(0)) before the reads, so no chunk's load
+// overlapped another's compute.
+template <int NCH, int XCH>
+__device__ __forceinline__ void route_dma(char* dst, __amdgpu_buffer_rsrc_t rx,
+                                          __amdgpu_buffer_rsrc_t rw, const uint32_t* voff,
+                                          int soff, int wave) {
 #pragma unroll
-  for (int i = 0; i < NCH; ++i)
-    __builtin_amdgcn_global_load_lds(src[i] + k0,
-                                     (__attribute__((address_space(3))) void*)(
-                                         dst + (i * kRouteThreads + wave * 64) * 16),
-                                     16, 0, 0);
+  for (int i = 0; i < NCH; ++i) {
+    // chunks [0, XCH) of the stage are x rows (wave-uniform test)
+    const bool is_x = i * kRouteThreads + wave * 64 < XCH;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        is_x ? rx : rw,
+        (__attribute__((address_space(3))) void*)(dst + (i * kRouteThreads + wave * 64) * 16), 16,
+        voff[i], soff, 0, 0);
+  }
 }
 
 template <int N>
@@ -139,12 +154,23 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   constexpr int EP = 32 * NB;        // experts padded to 32
   constexpr int LD = EP + 1;         // LDS row stride (floats)
   constexpr int EPL = EP / 16;       // experts owned per top-k lane
-  __shared__ float s_log[kRouteTokens * LD];
+  // One LDS array, carved by hand.  Separate __shared__ arrays get alias
+  // scopes of their own, and the stage reads then share the LDS-DMA copies'
+  // scope: the compiler would wait for every copy in flight (vmcnt(0)) before
+  // each chunk's reads and serialise the stages.  The stage loop's explicit
+  // waits and barriers order the copies and the reads.
+  constexpr int STAGE_B = (StageBytes<NB, KC>::value + 15) / 16 * 16;
+  constexpr int LOG_OFF = STAGE_B;
+  constexpr int BIAS_OFF = LOG_OFF + kRouteTokens * LD * 4;
+  constexpr int MASK_OFF = BIAS_OFF + EP * 4;
+  constexpr int ALIVE_OFF = MASK_OFF + EP * 4;
+  __shared__ __attribute__((aligned(1024))) char s_mem[ALIVE_OFF + EP];
   // LDS-staged path: the operand stages, reused for the cross-wave partial sums
-  __shared__ __attribute__((aligned(1024))) char s_stage[StageBytes<NB, KC>::value];
-  __shared__ float s_bias[EP];
-  __shared__ uint8_t s_alive[EP];
-  __shared__ uint32_t s_mask[EP];
+  char* const s_stage = s_mem;
+  float* const s_log = reinterpret_cast<float*>(s_mem + LOG_OFF);
+  float* const s_bias = reinterpret_cast<float*>(s_mem + BIAS_OFF);
+  uint32_t* const s_mask = reinterpret_cast<uint32_t*>(s_mem + MASK_OFF);
+  uint8_t* const s_alive = reinterpret_cast<uint8_t*>(s_mem + ALIVE_OFF);
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -170,21 +196,26 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     // LDS-staged: every thread fills NCH chunks of each stage; the waves
     // share the KC/16 k-steps of a stage round robin.
     using St = RouterStage<NB, KC>;
-    const bf16_t* src[St::NCH];
+    static_assert(St::CPR % 2 == 0, "a wave's 64 chunks must not straddle the x / W_r boundary");
+    // x from the workgroup's first token (32 rows: 32-bit offsets), W_r whole
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(x + (size_t)t0 * d), 0, -1, kRouteBufferFlags);
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(w), 0, -1, kRouteBufferFlags);
+    const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+    uint32_t voff[St::NCH];
 #pragma unroll
     for (int i = 0; i < St::NCH; ++i) {
       const int q = i * kRouteThreads + tid;
       const int r = q / St::CPR;
       const int lc = (q % St::CPR) ^ (r & 15);
-      const bf16_t* base;
       if (r < 32) {
-        const int t = t0 + r < n_tok ? t0 + r : n_tok - 1;
-        base = reinterpret_cast<const bf16_t*>(x) + (size_t)t * d;
+        const int t = t0 + r < n_tok ? r : n_tok - 1 - t0;
+        voff[i] = (uint32_t)(((size_t)t * d + lc * 8) * 2);
       } else {
         const int e = r - 32 < E ? r - 32 : E - 1;
-        base = reinterpret_cast<const bf16_t*>(w) + (size_t)e * d;
+        voff[i] = (uint32_t)(((size_t)e * d + lc * 8) * 2);
       }
-      src[i] = base + lc * 8;
     }
     const int n_chunks = d / KC;
     // NS stages: chunks c .. c+NS-2 in flight while chunk c computes.  Past the
@@ -197,16 +228,23 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     auto issue = [&](int c) {
       const int cl = c < n_chunks ? c : n_chunks - 1;
       const int cc = cl + rot < n_chunks ? cl + rot : cl + rot - n_chunks;
-      route_dma<St::NCH>(s_stage + (c % NS) * St::BYTES, src, cc * KC, wave);
+      route_dma<St::NCH, 32 * St::CPR>(s_stage + (c % NS) * St::BYTES, rx, rw, voff, cc * KC * 2,
+                                        wave_s);
     };
 #pragma unroll
     for (int c = 0; c < NS - 1; ++c) issue(c);
     for (int c = 0; c < n_chunks; ++c) {
       const char* st = s_stage + (c % NS) * St::BYTES;
       issue(c + NS - 1);                       // into the stage chunk c-1 used
-      route_wait_vmcnt<(NS - 1) * St::NCH>();  // chunk c has landed
-      __syncthreads();
-      for (int s = wave; s < KC / 16; s += kRouteWaves) {
+      // chunk c has landed: this thread's loads (the counter), then every
+      // thread's (a bare barrier: __syncthreads' fence would make the compiler
+      // wait for every load in flight, the later chunks' too)
+      route_wait_vmcnt<(NS - 1) * St::NCH>();
+      __builtin_amdgcn_s_barrier();
+      static_assert(KC / 16 % kRouteWaves == 0, "every wave takes the same number of k-steps");
+#pragma unroll
+      for (int u = 0; u < KC / 16 / kRouteWaves; ++u) {
+        const int s = wave + u * kRouteWaves;
         const int lc = 2 * s + kh;
         const u32x4_t a =
             *reinterpret_cast<const u32x4_t*>(st + row * St::RB + ((lc ^ (row & 15)) << 4));
@@ -218,9 +256,15 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
           RouterStep<bf16_t>::mma(acc[nb], a, bv);
         }
       }
-      __syncthreads();  // stage c % NS is refilled at the next iteration
+      // every thread's reads of stage c % NS are done: it is refilled at the
+      // next iteration
+      __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
     }
-    route_wait_vmcnt<0>();  // no LDS-DMA may still be writing when the LDS is reused
+    // no LDS-DMA may still be writing when the stage area is reused for the
+    // partial sums: this thread's copies (the counter), then every thread's
+    route_wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
   } else {
     using Step = RouterStep<T>;
     const int tok = t0 + row;
