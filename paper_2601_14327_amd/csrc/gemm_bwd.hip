@@ -150,9 +150,24 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
   int entry, mt, nt;
   if (EPI == EPI_WGRAD) {
     entry = L / p.tiles_per_entry;
+    const int within = L % p.tiles_per_entry;
+    const int MT = p.tiles_per_entry / p.n_tiles_n;   // output row blocks of the expert
     int m, n;
-    grouped_tile(L % p.tiles_per_entry, p.tiles_per_entry / p.n_tiles_n, p.n_tiles_n, p.group,
-                 m, n);
+    if (p.xcd_gm > 0) {
+      // block i runs on XCD i % 8, and tiles_per_entry % 8 == 0: XCD x takes
+      // block (x / gn, x % gn) of the expert's MT x NT tile grid, so each
+      // operand panel is fetched by gn (A) or gm (B) XCDs instead of all 8,
+      // and every XCD gets the same share of every expert
+      const int gm = p.xcd_gm, gn = 8 / gm;
+      const int x = within & 7, j = within >> 3;
+      const int bm = MT / gm, bn = p.n_tiles_n / gn;
+      int mm, nn;
+      grouped_tile(j, bm, bn, p.group, mm, nn);
+      m = (x / gn) * bm + mm;
+      n = (x % gn) * bn + nn;
+    } else {
+      grouped_tile(within, MT, p.n_tiles_n, p.group, m, n);
+    }
     mt = m;
     nt = n;
   } else {
@@ -525,6 +540,25 @@ __global__ __launch_bounds__(256) void swiglu_bwd_kernel(const u32x4_t* __restri
 
 constexpr int kBwdBM = 256, kBwdBN = 256;
 
+// The XCD blocking of a weight gradient's tile grid (MT x NT tiles per
+// expert; A has Mw features, B N): the split gm x gn = 8 with gm | MT and
+// gn | NT that fetches the fewest panel bytes (A panels gn times, B panels gm
+// times), or 0 when none divides.
+int wgrad_xcd_gm(int MT, int NT, int Mw, int N) {
+  int best = 0;
+  long long best_cost = 0;
+  for (int gm = 1; gm <= 8; gm *= 2) {
+    const int gn = 8 / gm;
+    if (MT % gm || NT % gn) continue;
+    const long long cost = (long long)gn * Mw + (long long)gm * N;
+    if (!best || cost < best_cost) {
+      best = gm;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
 template <int EPI, bool A_TR, bool B_GATHER = false>
 hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
@@ -584,6 +618,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   wd.wout = dw_d;
   wd.strideW = (long long)d * f;
   wd.accumulate = accumulate;
+  wd.xcd_gm = wgrad_xcd_gm(ceil_div(d, kBwdBM), wd.n_tiles_n, d, f);
   GemmParams wg = wd;
   wg.A = dA;
   wg.lda = 2 * f;
@@ -598,6 +633,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   wg.tiles_per_entry = ceil_div(2 * f, kBwdBM) * wg.n_tiles_n;
   wg.wout = dw_gu;
   wg.strideW = (long long)2 * f * d;
+  wg.xcd_gm = wgrad_xcd_gm(ceil_div(2 * f, kBwdBM), wg.n_tiles_n, 2 * f, d);
 
   // The weight gradients run on the side stream, concurrently with the data
   // gradients: dW_d from the start when it uses the forward's H, else after
