@@ -10,8 +10,8 @@ of the C-ABI library; three input sets rotate over the steps so the
 activations are not cache-resident.  With one slot per token (shard,
 shard_bwd) the combine folds into the FFN call as well (the down projection
 writes each row, times its gate, to its token row).  Training steps write no
-x_perm either: the weight gradient gathers the token rows through row_src as
-well.
+x_perm and no dy_perm: the weight gradient gathers the token rows through
+row_src as well, and the expert backward forms dY = g * dout on load.
 
 Prints ONE JSON line:
   value        tokens/s of the whole step (wall clock over the timed steps,
@@ -262,14 +262,15 @@ class Setup:
                 import torch
                 p.dw_gate_up = torch.empty(self.wgu.shape, dtype=torch.float32, device=self.dev)
                 p.dw_down = torch.empty(self.wd.shape, dtype=torch.float32, device=self.dev)
-            out += [("combine_bwd", lambda: L.moe_combine_bwd(self.dout, p.y_perm, gate,
-                                                              p.dest_row, dy_perm=p.dy_perm,
-                                                              dgate=p.dgate))]
+            out += [("combine_bwd", lambda: L.moe_combine_bwd(
+                self.dout, p.y_perm, gate, p.dest_row, dy_perm=p.dy_perm, dgate=p.dgate,
+                want_dy=p.dy_perm is not None))]
             if w.routed:   # the router's weight gradients on a side stream, beside the FFN's
                 out += [("route_bwd_w", lambda: p.route_backward_weights_async(x, self.wr))]
             out += [("ffn_bwd", lambda: L.moe_grouped_ffn_bwd_gather(
-                        p.dy_perm, x, p.row_src, w.k, p.act_save, self.wgu, self.wd,
-                        p.offsets, h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
+                        None, x, p.row_src, w.k, p.act_save, self.wgu, self.wd,
+                        p.offsets, dout=self.dout, topk_gate=gate,
+                        h_fwd=L.ffn_fwd_h_view(p.ws_ffn, R, w.d_ff, p.dtype),
                         dw_gate_up=p.dw_gate_up, dw_down=p.dw_down, ws=p.ws_bwd,
                         dx_perm=p.dx_perm) if p.fused else L.moe_grouped_ffn_bwd(
                         p.dy_perm, p.x_perm, p.act_save, self.wgu, self.wd, p.offsets,

@@ -441,20 +441,28 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm,
                         void* ws, size_t ws_bytes, void* stream);
 
 /*
- * moe_grouped_ffn_bwd_gather -- moe_grouped_ffn_bwd with the dispatch folded
- * into the weight gradient (the backward half of the expert-parallel
- * dispatch, Section 3.3): dW_gu = dA^T X reads routed row r of X straight
- * from token row row_src[r] / k of x, so the dispatched rows x_perm are never
- * needed.  Results are bit-identical to moe_permute followed by
+ * moe_grouped_ffn_bwd_gather -- moe_grouped_ffn_bwd with the expert-parallel
+ * dispatch and return (Section 3.3) folded into the products:
+ *   - dW_gu = dA^T X reads routed row r of X straight from token row
+ *     row_src[r] / k of x, so the dispatched rows x_perm are never needed;
+ *   - with dy_perm NULL, the first data gradient and dW_d form dY on load:
+ *     routed row r is round(topk_gate[s] * dout[s / k]) with s = row_src[r],
+ *     exactly what moe_combine_bwd writes into dy_perm (which it can then
+ *     skip: pass it dy_perm NULL).
+ * Results are bit-identical to moe_permute, moe_combine_bwd's dy_perm and
  * moe_grouped_ffn_bwd.
  *
+ *   dy_perm device [R, d_model] bf16 or NULL; dout device [T, d_model] bf16
+ *   and topk_gate device [T * k] fp32 (used when dy_perm is NULL);
  *   x device [T, d_model] bf16; row_src device [R] int32 (as
  *   moe_expert_counts writes it, every entry in [0, T*k)); the other
  *   arguments, the workspace and the streams are those of moe_grouped_ffn_bwd.
- *   dtype must be LAEP_BF16 and x under 2 GiB (T*d_model*2 bytes: its rows
- *   are addressed with 32-bit offsets); LAEP_ERR_UNSUPPORTED otherwise.
+ *   dtype must be LAEP_BF16 and x and dout under 2 GiB (T*d_model*2 bytes:
+ *   their rows are addressed with 32-bit offsets); LAEP_ERR_UNSUPPORTED
+ *   otherwise.
  */
-int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x,
+int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* dout,
+                               const float* topk_gate, const void* x,
                                const int32_t* row_src, int T, int k,
                                const void* act_save, const void* h_fwd,
                                const void* w_gate_up, const void* w_down,
@@ -483,8 +491,9 @@ int moe_combine(const void* y_perm, const float* topk_gate,
  * moe_combine_bwd -- backward of moe_combine:
  *   dgate[t, j]  = <dout[t], y_perm[row]>          (fp32 accumulation)
  *   dy_perm[row] = round(topk_gate[t, j] * dout[t]),  row = dest_row[t*k + j]
- *   dout device [T, d_model]; dy_perm device [rows, d_model]; dgate device [T, k] fp32
- *   (0 for unrouted slots).
+ *   dout device [T, d_model]; dy_perm device [rows, d_model] or NULL (then
+ *   only dgate: moe_grouped_ffn_bwd_gather can form dY itself); dgate device
+ *   [T, k] fp32 (0 for unrouted slots).
  */
 int moe_combine_bwd(const void* dout, const void* y_perm,
                     const float* topk_gate, const int32_t* dest_row, int T,

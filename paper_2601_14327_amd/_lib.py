@@ -67,8 +67,8 @@ SIGNATURES = {
                                                 _i, _i64, _p, _p, _p, _p, _p, _sz, _p]),
     "moe_grouped_ffn_bwd": (_i, [_p, _p, _p, _p, _p, _p, _p, _p, _i, _i, _i, _i, _i64, _p, _p, _p,
                                  _i, _p, _sz, _p]),
-    "moe_grouped_ffn_bwd_gather": (_i, [_p, _p, _p, _i, _i, _p, _p, _p, _p, _p, _p, _i, _i, _i,
-                                        _i, _i64, _p, _p, _p, _i, _p, _sz, _p]),
+    "moe_grouped_ffn_bwd_gather": (_i, [_p, _p, _p, _p, _p, _i, _i, _p, _p, _p, _p, _p, _p, _i,
+                                        _i, _i, _i, _i64, _p, _p, _p, _i, _p, _sz, _p]),
     "laep_ws_hb_offset": (_sz, [_i64, _i, _i]),
     "moe_combine": (_i, [_p, _p, _p, _i, _i, _i, _i, _p, _p]),
     "moe_combine_bwd": (_i, [_p, _p, _p, _p, _i, _i, _i, _i, _p, _p, _p]),

@@ -410,30 +410,38 @@ def moe_grouped_ffn_bwd(dy_perm, x_perm, act_save, w_gate_up, w_down, offsets, *
 
 
 def moe_grouped_ffn_bwd_gather(dy_perm, x, row_src, k: int, act_save, w_gate_up, w_down,
-                               offsets, *, h_fwd=None, expert_map=None, dw_gate_up=None,
-                               dw_down=None, accumulate=False, ws=None, dx_perm=None,
-                               return_ws: bool = False):
+                               offsets, *, dout=None, topk_gate=None, h_fwd=None,
+                               expert_map=None, dw_gate_up=None, dw_down=None, accumulate=False,
+                               ws=None, dx_perm=None, return_ws: bool = False):
     """moe_grouped_ffn_bwd with the weight gradient reading X's routed rows
-    from the token rows x through row_src (no x_perm).  Returns as
-    moe_grouped_ffn_bwd."""
-    for t, n in ((dy_perm, "dy_perm"), (x, "x"), (row_src, "row_src"), (act_save, "act_save"),
+    from the token rows x through row_src (no x_perm).  With dy_perm None,
+    dY is formed on load from ``dout`` [T, d] and ``topk_gate`` [T, k] (no
+    dy_perm).  Returns as moe_grouped_ffn_bwd."""
+    for t, n in ((x, "x"), (row_src, "row_src"), (act_save, "act_save"),
                  (w_gate_up, "w_gate_up"), (w_down, "w_down"), (offsets, "offsets")):
         _dev(t, n)
+    if dy_perm is None:
+        if dout is None or topk_gate is None:
+            raise ValueError("without dy_perm, dout and topk_gate are needed")
+        _dev(dout, "dout"), _dev(topk_gate, "topk_gate")
+    else:
+        _dev(dy_perm, "dy_perm")
     if h_fwd is not None:
         _dev(h_fwd, "h_fwd")
     T, d = x.shape
-    R = dy_perm.shape[0]
+    R = row_src.shape[0]
     f = w_down.shape[2]
     E = offsets.shape[0] - 1
     dev = x.device
-    dx_perm = torch.empty_like(dy_perm) if dx_perm is None else dx_perm
+    dx_perm = torch.empty((R, d), dtype=x.dtype, device=dev) if dx_perm is None else dx_perm
     if dw_gate_up is None:
         dw_gate_up = torch.empty(w_gate_up.shape, dtype=torch.float32, device=dev)
     if dw_down is None:
         dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=dev)
     ws = _workspace(ws, workspace_bytes(LAEP_CALL_FFN_BWD, R, 1, E, d, f), dev)
     check(lib().moe_grouped_ffn_bwd_gather(
-        _ptr(dy_perm), _ptr(x), _ptr(row_src), T, k, _ptr(act_save), _ptr(h_fwd),
+        _ptr(dy_perm), _ptr(dout), _ptr(topk_gate), _ptr(x), _ptr(row_src), T, k,
+        _ptr(act_save), _ptr(h_fwd),
         _ptr(w_gate_up), _ptr(w_down), _ptr(offsets), _ptr(expert_map), _dtype_code(x), E, d, f,
         R, _ptr(dx_perm), _ptr(dw_gate_up), _ptr(dw_down), int(accumulate), _ptr(ws), ws.numel(),
         _stream(dev)))
@@ -472,15 +480,19 @@ def moe_combine(y_perm: torch.Tensor, topk_gate: torch.Tensor, dest_row: torch.T
 
 
 def moe_combine_bwd(dout: torch.Tensor, y_perm: torch.Tensor, topk_gate: torch.Tensor,
-                    dest_row: torch.Tensor, *, dy_perm=None, dgate=None):
-    """Returns (dy_perm, dgate)."""
+                    dest_row: torch.Tensor, *, dy_perm=None, dgate=None, want_dy: bool = True):
+    """Returns (dy_perm, dgate); with want_dy False only dgate is computed
+    (dy_perm None: moe_grouped_ffn_bwd_gather forms dY itself)."""
     for t, n in ((dout, "dout"), (y_perm, "y_perm"), (topk_gate, "topk_gate"),
                  (dest_row, "dest_row")):
         _dev(t, n)
     T, k = topk_gate.shape
     d = dout.shape[1]
     dev = dout.device
-    dy_perm = torch.empty_like(y_perm) if dy_perm is None else dy_perm
+    if want_dy and dy_perm is None:
+        dy_perm = torch.empty_like(y_perm)
+    if not want_dy:
+        dy_perm = None
     dgate = torch.empty((T, k), dtype=torch.float32, device=dev) if dgate is None else dgate
     check(lib().moe_combine_bwd(_ptr(dout), _ptr(y_perm), _ptr(topk_gate), _ptr(dest_row), T, k,
                                 d, _dtype_code(dout), _ptr(dy_perm), _ptr(dgate), _stream(dev)))

@@ -514,7 +514,8 @@ int moe_grouped_ffn_bwd(const void* dy_perm, const void* x_perm, const void* act
                     "moe_grouped_ffn_bwd");
 }
 
-int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x, const int32_t* row_src, int T,
+int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* dout, const float* topk_gate,
+                               const void* x, const int32_t* row_src, int T,
                                int k, const void* act_save, const void* h_fwd,
                                const void* w_gate_up, const void* w_down, const int32_t* offsets,
                                const int32_t* expert_map, int dtype, int E, int d_model, int d_ff,
@@ -531,10 +532,13 @@ int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x, const int32_t
           "moe_grouped_ffn_bwd_gather: x (T*d_model bf16) must be under 2 GiB");
   REQUIRE(offsets && dw_gate_up && dw_down && ws, LAEP_ERR_INVALID_ARG,
           "moe_grouped_ffn_bwd_gather: offsets, dw_gate_up, dw_down and ws must be non-null");
-  REQUIRE(R == 0 || (dy_perm && x && row_src && act_save && w_gate_up && w_down && dx_perm),
+  REQUIRE(R == 0 || (x && row_src && act_save && w_gate_up && w_down && dx_perm),
           LAEP_ERR_INVALID_ARG,
           "moe_grouped_ffn_bwd_gather: activation pointers and row_src must be non-null");
-  REQUIRE(aligned16(dy_perm) && aligned16(x) && aligned16(act_save) && aligned16(h_fwd) &&
+  REQUIRE(R == 0 || dy_perm || (dout && topk_gate), LAEP_ERR_INVALID_ARG,
+          "moe_grouped_ffn_bwd_gather: without dy_perm, dout and topk_gate must be non-null");
+  REQUIRE(aligned16(dy_perm) && aligned16(dout) && aligned16(x) && aligned16(act_save) &&
+              aligned16(h_fwd) &&
               aligned16(w_gate_up) && aligned16(w_down) && aligned16(dx_perm) &&
               aligned16(dw_gate_up) && aligned16(dw_down) && aligned16(ws),
           LAEP_ERR_INVALID_ARG, "moe_grouped_ffn_bwd_gather: buffers must be 16-byte aligned");
@@ -544,7 +548,7 @@ int moe_grouped_ffn_bwd_gather(const void* dy_perm, const void* x, const int32_t
   return hip_status(laep::launch_ffn_bwd_bf16(dy_perm, x, act_save, h_fwd, w_gate_up, w_down,
                                               offsets, expert_map, E, d_model, d_ff, R, dx_perm,
                                               dw_gate_up, dw_down, accumulate != 0, ws,
-                                              as_stream(stream), row_src, k, T),
+                                              as_stream(stream), row_src, k, T, dout, topk_gate),
                     "moe_grouped_ffn_bwd_gather");
 }
 
@@ -572,8 +576,8 @@ int moe_combine_bwd(const void* dout, const void* y_perm, const float* topk_gate
   REQUIRE(k >= 1, LAEP_ERR_INVALID_ARG, "k=%d < 1", k);
   if ((rc = check_rows(T, k, d_model))) return rc;
   if (T == 0) return ok();
-  REQUIRE(dout && y_perm && topk_gate && dest_row && dy_perm && dgate, LAEP_ERR_INVALID_ARG,
-          "moe_combine_bwd: pointers must be non-null");
+  REQUIRE(dout && y_perm && topk_gate && dest_row && dgate, LAEP_ERR_INVALID_ARG,
+          "moe_combine_bwd: pointers other than dy_perm must be non-null");
   REQUIRE(aligned16(dout) && aligned16(y_perm) && aligned16(dy_perm), LAEP_ERR_INVALID_ARG,
           "moe_combine_bwd: dout, y_perm and dy_perm must be 16-byte aligned");
   return hip_status(laep::launch_combine_bwd(dout, y_perm, topk_gate, dest_row, T, k, d_model,

@@ -35,6 +35,17 @@
 // one k-step ahead, issued before that iteration's LDS-DMA halves, so the
 // in-order vmcnt waits of the ring still cover them.  Rows past the expert's
 // end get an offset beyond x's buffer range and read as zeros.
+//
+// dY formed on load (the gate scaling of the combine backward folded into
+// data-gradient 1 and dW_d): their A operand dY = round(g * dout) is read from
+// dout's token rows (routed row r: token row row_src[r] / k, times
+// gate[row_src[r]], one fp32 product rounded to bf16, exactly as
+// moe_combine_bwd forms dy_perm), so dy_perm is never written.  The A halves
+// are LDS-DMA'd from dout's token rows through row_src as usual (a gather, as
+// in the forward), and each thread scales its own chunks in place just before
+// the step boundary at which that half has landed: the ring's prefetch depth
+// is unchanged, and the transform's LDS round trip overlaps the last
+// sub-step's MFMAs.
 #include <type_traits>
 
 #include "gemm_common.hpp"
@@ -110,9 +121,18 @@ __device__ __forceinline__ void dma_half(char* dst, const char* base, uint32_t e
                                              16, voff[i], 0, 0, 0);
 }
 
-template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR, bool B_GATHER>
+// 8 bf16 values times g, each an fp32 product rounded to bf16
+__device__ __forceinline__ u32x4_t scale_bf16x8(const u32x4_t v, float g) {
+  u32x4_t o;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) o[w] = pack_bf16x2(g * lo_bf16(v[w]), g * hi_bf16(v[w]));
+  return o;
+}
+
+template <int BM, int BN, int NWM, int NWN, int EPI, bool A_TR, bool B_GATHER, bool A_DY>
 __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) {
   static_assert(!B_GATHER || EPI == EPI_WGRAD, "only the weight gradient gathers its B rows");
+  static_assert(!(A_DY && B_GATHER), "dY on load and gathered B are separate products");
   constexpr int NT = 64 * NWM * NWN;
   constexpr int WTM = BM / NWM, WTN = BN / NWN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -204,10 +224,16 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       const int r = q >> 3;
       const int lc = (q & 7) ^ swz8(r);
       const int rr = r < te.rows ? r : te.rows - 1;  // rows past the expert: any valid row
-      a_voff[i] = (uint32_t)(((long long)rr * p.lda + lc * 8) * 2);
+      if (A_DY) {  // dY on load: the token row of routed row te.row0 + rr in dout
+        const uint32_t s = (uint32_t)p.row_src[te.row0 + rr];
+        a_voff[i] = (s / (uint32_t)p.slots_k) * (uint32_t)p.lda * 2u + (uint32_t)(lc * 16);
+      } else {
+        a_voff[i] = (uint32_t)(((long long)rr * p.lda + lc * 8) * 2);
+      }
     }
   }
-  const char* a_tile = reinterpret_cast<const char*>(p.A + (long long)te.row0 * p.lda);
+  const char* a_tile = reinterpret_cast<const char*>(
+      A_DY ? p.A : p.A + (long long)te.row0 * p.lda);
   const long long a_kstep = A_TR ? 128LL * p.lda : 128LL;  // bytes per k-step
   // B is K-strided in every backward product: [K][N] rows, feature nt*BN + col
   // (clamped to the last valid column block)
@@ -275,6 +301,59 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
     dma_half<NH, NT>(smem + (h % kRingSlots) * kRingHalf, b_tile, p.b_extent, v, wave);
   };
 
+  // ---- dY formed on load (A_DY) ---------------------------------------------------
+  // data gradient 1: the tile's rows are fixed, so each chunk's token-row
+  // offset (a_voff, above) and its row's gate are loaded once; dW_d: the
+  // k-rows change every step, so (as for a gathered B) each thread loads the
+  // row_src entries of its k-rows one step ahead of that step's A half, and the
+  // gates with the half
+  float ady_g[NH];
+  int ady_kr[NH];
+  uint32_t ady_cb[NH];
+  if constexpr (A_DY && A_TR) {
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      int r, col;
+      tr_slot(i * NT + tid, kTrCpr, r, col);
+      int c = mt * BM + col;
+      c = c < p.Mw ? c : p.Mw - 8;
+      ady_kr[i] = r;
+      ady_cb[i] = (uint32_t)(c * 2);
+    }
+  }
+  auto ady_idx = [&](int ks, uint32_t* raw, uint32_t& okm) {
+    okm = 0;
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const int kr = ks * 64 + ady_kr[i];
+      const bool ok = ks < nk && kr < kext;
+      raw[i] = (uint32_t)p.row_src[te.row0 + (ok ? kr : 0)];
+      okm |= ok ? (1u << i) : 0u;
+    }
+  };
+  // dW_d: the gathered A half of step ks (rows marked invalid fall outside
+  // dout's buffer range and read as zeros), and the gates of its k-rows
+  auto ady_issue_tr = [&](int ks, const uint32_t* raw, uint32_t okm, float* g) {
+    uint32_t v[NH];
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const uint32_t off = (raw[i] / (uint32_t)p.slots_k) * (uint32_t)p.lda * 2u + ady_cb[i];
+      v[i] = (okm >> i) & 1u ? off : 0x80000000u;
+      g[i] = p.gate[raw[i]];
+    }
+    dma_half<NH, NT>(smem + ((2 * ks) % kRingSlots) * kRingHalf, a_tile, p.a_extent, v, wave);
+  };
+  // this thread's chunks of the A half of step ks, scaled in place (its own
+  // copies have landed; the next barrier publishes the result)
+  auto ady_scale = [&](int ks, const float* g) {
+    char* slot = smem + ((2 * ks) % kRingSlots) * kRingHalf;
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      u32x4_t* c = reinterpret_cast<u32x4_t*>(slot + (i * NT + tid) * 16);
+      *c = scale_bf16x8(*c, g[i]);
+    }
+  };
+
   // ---- fragment offsets within a half, k16 sub-step 0 -------------------------------
   const int lc0 = lane >> 5;
   const int gh = (lane >> 4) & 1;
@@ -340,7 +419,38 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
 
     // prologue: halves 0 .. 4 in flight, step 0 (halves 0, 1) landed
     uint32_t idx_next[NH], ok_next = 0;  // gathered B: row_src of the next B half to issue
-    if constexpr (B_GATHER) {
+    // dY on load: the gates of the A halves landed or in flight (dW_d: of
+    // steps kt+1 and kt+2 at step kt's boundary) and the row_src entries of the
+    // next A half to issue
+    float ady_g1[NH], ady_g2[NH];
+    uint32_t ady_src[NH], ady_ok = 0;
+    if constexpr (A_DY) {
+      float g0[NH];
+      if constexpr (A_TR) {
+        uint32_t s0[NH], s1[NH], s2[NH], ok0, ok1, ok2;
+        ady_idx(0, s0, ok0);
+        ady_idx(1, s1, ok1);
+        ady_idx(2, s2, ok2);
+        ady_idx(3, ady_src, ady_ok);
+        ady_issue_tr(0, s0, ok0, g0);
+        issue_half(1);
+        ady_issue_tr(1, s1, ok1, ady_g1);
+        issue_half(3);
+        ady_issue_tr(2, s2, ok2, ady_g2);
+      } else {
+#pragma unroll
+        for (int i = 0; i < NH; ++i) {   // data gradient 1: the chunk rows' gates, once
+          const int rr = min((i * NT + tid) >> 3, te.rows - 1);
+          ady_g[i] = p.gate[p.row_src[te.row0 + rr]];
+          g0[i] = ady_g[i];
+        }
+#pragma unroll
+        for (int h = 0; h < kRingSlots; ++h) issue_half(h);
+      }
+      wait_vmcnt<3 * NH>();
+      ady_scale(0, g0);
+      wait_lgkm0();
+    } else if constexpr (B_GATHER) {
       uint32_t idx0[NH], idx1[NH], ok0, ok1;
       gather_idx(0, idx0, ok0);
       gather_idx(1, idx1, ok1);
@@ -354,7 +464,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
 #pragma unroll
       for (int h = 0; h < kRingSlots; ++h) issue_half(h);
     }
-    wait_vmcnt<3 * NH>();
+    if constexpr (!A_DY) wait_vmcnt<3 * NH>();
     __builtin_amdgcn_s_barrier();
     int ia = 0, ib = 1;  // slots of the current step's A and B halves
     read_frags(smem, smem + kRingHalf, 0, fa0, fb0);
@@ -365,6 +475,16 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       mma_step(fa0, fb0);
       read_frags(sa, sb, 2, fa0, fb0);
       mma_step(fa1, fb1);
+      if constexpr (A_DY) {
+        // dY on load: this thread's copies of the A half of step kt+1 have
+        // landed once only the halves issued after it may be in flight (two
+        // iterations' worth: 2 or, for dW_d with its row_src and gate loads, 4
+        // groups of NH); scale them here, beside the MFMAs, so the LDS round
+        // trip stays off the step boundary (the boundary's lgkmcnt(0) and
+        // barrier publish them)
+        wait_vmcnt<(A_TR ? 8 : 4) * NH>();
+        ady_scale(kt + 1, A_TR ? ady_g1 : ady_g);
+      }
       read_frags(sa, sb, 3, fa1, fb1);
       mma_step(fa0, fb0);
       // step boundary: this thread's reads of step kt are in registers and its
@@ -373,7 +493,20 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       // two halves of step kt are free: they receive B of kt+2 and A of kt+3.
       wait_vmcnt_lgkm0<NH>();
       __builtin_amdgcn_s_barrier();
-      if constexpr (B_GATHER) {
+      if constexpr (A_DY && A_TR) {
+        // dW_d: the gates move down a step; the A half of kt+3 (row_src loaded
+        // last iteration) with its gates; the row_src entries of kt+4 first,
+        // so the next boundary's wait covers them
+#pragma unroll
+        for (int i = 0; i < NH; ++i) ady_g1[i] = ady_g2[i];
+        uint32_t src3[NH];
+#pragma unroll
+        for (int i = 0; i < NH; ++i) src3[i] = ady_src[i];
+        const uint32_t ok3 = ady_ok;
+        ady_idx(kt + 4, ady_src, ady_ok);
+        issue_half(2 * kt + 5);
+        ady_issue_tr(kt + 3, src3, ok3, ady_g2);
+      } else if constexpr (B_GATHER) {
         // the offsets of B(kt + 2) from the entries loaded last iteration; the
         // entries of step kt + 3 are loaded before this iteration's halves,
         // so the next boundary's wait covers them
@@ -385,7 +518,7 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_bwd_kernel(GemmParams p) 
       } else {
         issue_half(2 * kt + 5);
       }
-      issue_half(2 * kt + 6);
+      if constexpr (!(A_DY && A_TR)) issue_half(2 * kt + 6);
       ia = ia + 2 >= kRingSlots ? ia + 2 - kRingSlots : ia + 2;
       ib = ib + 2 >= kRingSlots ? ib + 2 - kRingSlots : ib + 2;
       read_frags(smem + ia * kRingHalf, smem + ib * kRingHalf, 0, fa0, fb0);
@@ -559,10 +692,10 @@ int wgrad_xcd_gm(int MT, int NT, int Mw, int N) {
   return best;
 }
 
-template <int EPI, bool A_TR, bool B_GATHER = false>
+template <int EPI, bool A_TR, bool B_GATHER = false, bool A_DY = false>
 hipError_t launch_bwd(const GemmParams& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, EPI, A_TR, B_GATHER>),
+  hipLaunchKernelGGL((gemm_bwd_kernel<kBwdBM, kBwdBN, 2, 4, EPI, A_TR, B_GATHER, A_DY>),
                      dim3(round8(grid)), dim3(512), 0, s, p);
   return hipGetLastError();
 }
@@ -586,7 +719,10 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
                                const int32_t* offsets, const int32_t* expert_map, int E, int d,
                                int f, int64_t R, void* dx_perm, float* dw_gu, float* dw_d,
                                int accumulate, void* ws, hipStream_t s, const int32_t* row_src,
-                               int slots_k, int64_t x_rows) {
+                               int slots_k, int64_t x_rows, const void* dout,
+                               const float* gate) {
+  // dy == NULL: data gradient 1 and dW_d form dY on load from dout and the gates
+  const bool dy_on_load = dy == nullptr;
   char* base = static_cast<char*>(ws);
   bf16_t* dA = reinterpret_cast<bf16_t*>(base);
   bf16_t* Hb = reinterpret_cast<bf16_t*>(base + ffn_bwd_hb_offset(R, f, kDtypeBf16));
@@ -607,8 +743,12 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   wd.table = te.table;
   wd.n_entries = te.n_entries;
   wd.f = f;
-  wd.A = static_cast<const bf16_t*>(dy);
+  wd.A = static_cast<const bf16_t*>(dy_on_load ? dout : dy);
   wd.lda = d;
+  wd.row_src = row_src;
+  wd.slots_k = slots_k;
+  wd.gate = gate;
+  wd.a_extent = (uint32_t)(x_rows * d * 2);
   wd.B = h_fwd ? static_cast<const bf16_t*>(h_fwd) : Hb;
   wd.ldb = f;
   wd.Mw = d;
@@ -646,7 +786,11 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   const hipStream_t s2 = side->stream;
   auto fork = [&]() { return side_stream_fork(*side, s); };
   if ((err = fork()) != hipSuccess) return err;
-  if (h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
+  auto launch_dw_d = [&]() {
+    return dy_on_load ? launch_bwd<EPI_WGRAD, true, false, true>(wd, E * wd.tiles_per_entry, s2)
+                      : launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
+  };
+  if (h_fwd) err = launch_dw_d();
 
   // dgrad 1: dH = dY W_d (bf16, into the H_b buffer), then the SwiGLU backward -> dA (, H_b)
   GemmParams g = {};
@@ -654,8 +798,12 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.table = tr.table;
   g.n_entries = tr.n_entries;
   g.f = f;
-  g.A = static_cast<const bf16_t*>(dy);
+  g.A = static_cast<const bf16_t*>(dy_on_load ? dout : dy);
   g.lda = d;
+  g.row_src = row_src;
+  g.slots_k = slots_k;
+  g.gate = gate;
+  g.a_extent = (uint32_t)(x_rows * d * 2);
   g.B = static_cast<const bf16_t*>(w_d);
   g.ldb = f;
   g.strideB = (long long)d * f;
@@ -665,7 +813,9 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   g.tiles_per_entry = g.n_tiles_n;
   g.out = Hb;
   g.ldo = f;
-  if (err == hipSuccess) err = launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
+  if (err == hipSuccess)
+    err = dy_on_load ? launch_bwd<EPI_STORE, false, false, true>(g, max_ragged * g.n_tiles_n, s)
+                     : launch_bwd<EPI_STORE, false>(g, max_ragged * g.n_tiles_n, s);
   if (err == hipSuccess && R > 0) {
     const long long n_vec = R * (long long)(f / 8);
     hipLaunchKernelGGL(swiglu_bwd_kernel, dim3((unsigned)((n_vec + 255) / 256)), dim3(256), 0, s,
@@ -676,7 +826,7 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   }
   // dA (and H_b) ready: the remaining weight gradients on the side stream
   if (err == hipSuccess) err = fork();
-  if (err == hipSuccess && !h_fwd) err = launch_bwd<EPI_WGRAD, true>(wd, E * wd.tiles_per_entry, s2);
+  if (err == hipSuccess && !h_fwd) err = launch_dw_d();
   if (err == hipSuccess)
     err = row_src ? launch_bwd<EPI_WGRAD, true, true>(wg, E * wg.tiles_per_entry, s2)
                   : launch_bwd<EPI_WGRAD, true>(wg, E * wg.tiles_per_entry, s2);

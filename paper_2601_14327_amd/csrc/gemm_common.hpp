@@ -41,6 +41,7 @@ struct GemmParams {
   // weight gradient with the B operand gathered (dW_gu = dA^T X with X's
   // routed row r read from token row row_src[r] / slots_k of B): bytes of B
   uint32_t b_extent;
+  uint32_t a_extent;       // bytes of dout when data-gradient 1 / dW_d form dY on load
   // weight gradient: each XCD takes one block of an expert's output tiles, the
   // tile grid cut into xcd_gm x xcd_gn blocks (xcd_gm * xcd_gn = 8; 0 = tiles
   // dealt round robin)

@@ -97,13 +97,16 @@ size_t ffn_bwd_hb_offset(int64_t R, int f, int dtype);
 // else H_b, recomputed at the saved pre-activations.
 // row_src != NULL: x_perm is the token rows x [x_rows, d] and the weight
 // gradient reads routed row r from token row row_src[r] / slots_k.
+// dy == NULL (with row_src): dY is formed on load from dout [x_rows, d] and the
+// flat gates [x_rows * slots_k], as round(gate[s] * dout[s / slots_k]).
 hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* act_save,
                                const void* h_fwd, const void* w_gu, const void* w_d,
                                const int32_t* offsets,
                                const int32_t* expert_map, int E, int d, int f, int64_t R,
                                void* dx_perm, float* dw_gu, float* dw_d, int accumulate,
                                void* ws, hipStream_t s, const int32_t* row_src = nullptr,
-                               int slots_k = 1, int64_t x_rows = 0);
+                               int slots_k = 1, int64_t x_rows = 0, const void* dout = nullptr,
+                               const float* gate = nullptr);
 
 // Router backward.
 size_t route_bwd_ws_bytes(int T, int k, int E, int d_model);

@@ -181,7 +181,7 @@ __global__ __launch_bounds__(kRowThreads) void combine_bwd_kernel(
         part += dv[q] * yv[q];
         o[q] = g * dv[q];
       }
-      Elem<T>::store8(dy + (size_t)r * d + (size_t)v * 8, o);
+      if (dy != nullptr) Elem<T>::store8(dy + (size_t)r * d + (size_t)v * 8, o);
     }
     part = wave_sum(part);
     if (lane == 0) s_red[wave] = part;

@@ -8,10 +8,12 @@ Forward (given routing, one device's expert shard with k = 1):
     moe_expert_counts -> moe_permute -> moe_grouped_ffn_fwd -> moe_combine
 With fused dispatch (bf16, the default), moe_permute + moe_grouped_ffn_fwd
 become one moe_grouped_ffn_fwd_gather call that reads the token rows through
-row_src, and the backward's weight gradient reads them the same way
-(moe_grouped_ffn_bwd_gather), so a training step never writes x_perm.  A
-forward that keeps its activations for inspection (save_act without a
-backward) still writes x_perm.
+row_src, and the backward reads them the same way
+(moe_grouped_ffn_bwd_gather), so a training step never writes x_perm; that
+call also forms dY = g * dout on load, so moe_combine_bwd writes only the
+gate gradient and a training step never writes dy_perm either.  A forward
+that keeps its activations for inspection (save_act without a backward)
+still writes x_perm.
 With one slot per token (k = 1) the combine folds in as well
 (moe_grouped_ffn_fwd_gather_combine): the down projection writes each row,
 times its gate, to its token row; y_perm is written only for a backward pass.
@@ -84,7 +86,9 @@ class MoELayerPlan:
         self.ws_ffn = torch.empty(api.workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff),
                                   dtype=torch.uint8, device=dev)
         if backward:
-            self.dy_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
+            # fused plans form dY on load in the expert backward (no dy_perm)
+            self.dy_perm = (None if self.fused else
+                            torch.empty((R, d_model), dtype=dtype, device=dev))
             self.dx_perm = torch.empty((R, d_model), dtype=dtype, device=dev)
             self.dgate = torch.empty((T, k), dtype=torch.float32, device=dev)
             self.dx = torch.empty((T, d_model), dtype=dtype, device=dev)
@@ -216,7 +220,8 @@ class MoELayerPlan:
         """Expert backward; with router=(x, w_router) (renormalised gates) also
         the router's, its weight gradients beside the expert backward."""
         api.moe_combine_bwd(dout, self.y_perm, self.topk_gate, self.dest_row,
-                            dy_perm=self.dy_perm, dgate=self.dgate)
+                            dy_perm=self.dy_perm, dgate=self.dgate,
+                            want_dy=self.dy_perm is not None)
         if router is not None:
             self.route_backward_weights_async(router[0], router[1], want_dbias=want_dbias)
         if self.dw_gate_up is None:
@@ -225,9 +230,10 @@ class MoELayerPlan:
             self.dw_down = torch.empty(w_down.shape, dtype=torch.float32, device=self.device)
         # dW_d from the H the forward computed (left in its workspace)
         h_fwd = api.ffn_fwd_h_view(self.ws_ffn, self.R, self.f, self.dtype)
-        if self.fused:   # the weight gradient gathers X from the forward's token rows
-            api.moe_grouped_ffn_bwd_gather(self.dy_perm, self.x_in, self.row_src, self.k,
+        if self.fused:   # X gathered from the forward's token rows, dY formed on load
+            api.moe_grouped_ffn_bwd_gather(None, self.x_in, self.row_src, self.k,
                                            self.act_save, w_gate_up, w_down, self.offsets,
+                                           dout=dout, topk_gate=self.topk_gate,
                                            h_fwd=h_fwd, expert_map=expert_map,
                                            dw_gate_up=self.dw_gate_up, dw_down=self.dw_down,
                                            accumulate=accumulate, ws=self.ws_bwd,

@@ -323,3 +323,26 @@ def test_route_count_noalloc_validation(L):
     assert call(700000, 64, 8) == 3
     assert "scratch" in _err(L) and "moe_route_count" in _err(L)
     assert call(200000, 256, 8) == 3
+
+
+def test_ffn_bwd_gather_validation(L):
+    """The fused backward: without dy_perm it needs dout and the gates; bf16
+    only; R <= T*k; x and dout under 2 GiB."""
+    keep, p = _fake()
+    g = L.moe_grouped_ffn_bwd_gather
+    # (dy, dout, gate, x, row_src, T, k, act, h, wgu, wd, off, emap, dtype, E, d, f, R,
+    #  dx, dwgu, dwd, acc, ws, wsb, stream)
+    ok = lambda **kw: dict(dict(dy=p, dout=None, gate=None, x=p, rs=p, T=10, k=2, dtype=1, R=20,
+                                h=None), **kw)
+    call = lambda a: g(a["dy"], a["dout"], a["gate"], a["x"], a["rs"], a["T"], a["k"], p,
+                       a["h"], p, p, p, None, a["dtype"], 8, 128, 128, a["R"], p, p, p, 0, p,
+                       1 << 30, None)
+    assert call(ok(dy=None)) == 1 and "dout" in _err(L)
+    assert call(ok(dy=None, dout=p)) == 1 and "topk_gate" in _err(L)
+    assert call(ok(dtype=0)) == 2
+    assert call(ok(R=21)) == 1
+    assert call(ok(rs=None)) == 1
+    assert call(ok(dy=None, dout=p + 2, gate=p)) == 1 and "aligned" in _err(L)
+    big = g(None, p, p, p, p, 1 << 20, 1, p, None, p, p, p, None, 1, 8, 1024, 128, 20, p, p, p,
+            0, p, 1 << 40, None)
+    assert big == 2 and "2 GiB" in _err(L)

@@ -189,7 +189,11 @@ def test_shard_backward_full_size():
     cond = np.abs(dq * y).sum(1)
     assert np.all(np.abs(hint(plan.dgate)[toks, 0] - ref_dg) <= TOL_F32 * cond)
     from oracle.numerics import round_bf16
-    assert rownorm_err(h32(plan.dy_perm[tr]), round_bf16(g[toks, None] * dq)) <= TOL_BF16
+    # the plan keeps no dy_perm (the expert backward forms dY on load): the
+    # combine backward's dY, for the checks, from a separate call
+    assert plan.dy_perm is None
+    dyp, _ = laep.moe_combine_bwd(dout, plan.y_perm, plan.topk_gate, plan.dest_row)
+    assert rownorm_err(h32(dyp[tr]), round_bf16(g[toks, None] * dq)) <= TOL_BF16
     # dgrad on sampled rows, teacher-forced on the GPU's act_save / dY / dA; the
     # plan hands the backward the forward's H, so the H_b buffer keeps dH
     dA_ws, dh_ws = laep.ffn_bwd_ws_views(plan.ws_bwd, R, f, BF)
@@ -201,7 +205,7 @@ def test_shard_backward_full_size():
     srows = _block_rows(offsets, seed=6)
     ts = torch.from_numpy(srows).cuda()
     ex = _expert_of_rows(srows, offsets)
-    dy_s, act_s = h32(plan.dy_perm[ts]), h32(plan.act_save[ts])
+    dy_s, act_s = h32(dyp[ts]), h32(plan.act_save[ts])
     dA_s, dh_s, dx_s = h32(dA_ws[ts]), h32(dh_ws[ts]), h32(plan.dx_perm[ts])
     xp_s, h_s = h32(xg[ts]), h32(h_fwd[ts])
     for e in np.unique(ex):
@@ -228,13 +232,13 @@ def test_shard_backward_full_size():
         x_t = h32(xg[lo:hi, j0:j0 + TB]).astype(np.float64)
         assert rownorm_err(h32(dwgu[e, i0:i0 + TB, j0:j0 + TB]), dA_t.T @ x_t) <= TOL_F32, e
         i0, j0 = TB * int(rng.integers(d // TB)), TB * int(rng.integers(f // TB))
-        dy_t = h32(plan.dy_perm[lo:hi, i0:i0 + TB]).astype(np.float64)
+        dy_t = h32(dyp[lo:hi, i0:i0 + TB]).astype(np.float64)
         h_t = h32(h_fwd[lo:hi, j0:j0 + TB]).astype(np.float64)
         assert rownorm_err(h32(dwd[e, i0:i0 + TB, j0:j0 + TB]), dy_t.T @ h_t) <= TOL_F32, e
         tr = torch.arange(lo, hi, device="cuda")
         i_d = rng.choice(d, 3, replace=False)
         i_g = rng.choice(2 * f, 3, replace=False)
-        dy_e = h32(plan.dy_perm[tr][:, torch.from_numpy(i_d).cuda()]).astype(np.float64)
+        dy_e = h32(dyp[tr][:, torch.from_numpy(i_d).cuda()]).astype(np.float64)
         h_e = h32(h_fwd[tr]).astype(np.float64)
         ref_d = dy_e.T @ h_e
         assert rownorm_err(h32(dwd[e][torch.from_numpy(i_d).cuda()]), ref_d) <= TOL_F32
@@ -245,6 +249,13 @@ def test_shard_backward_full_size():
     # permute backward (k = 1: a gather back to token order)
     dx_tok = h32(plan.dx[torch.from_numpy(toks).cuda()])
     assert np.array_equal(dx_tok, h32(plan.dx_perm[torch.from_numpy(rows).cuda()]))
+    # the fused backward (gathered X, dY on load) equals the unfused chain bit for bit
+    case("full-size fused backward vs the unfused chain (shard_bwd)")
+    dxp_u, dwgu_u, dwd_u = laep.moe_grouped_ffn_bwd(dyp, xg, plan.act_save, wgu, wd,
+                                                    plan.offsets, h_fwd=h_fwd)
+    torch.cuda.synchronize()
+    assert torch.equal(dxp_u, plan.dx_perm)
+    assert torch.equal(dwgu_u, plan.dw_gate_up) and torch.equal(dwd_u, plan.dw_down)
 
 
 @pytest.mark.parametrize("name", ["balanced", "shard"])
@@ -296,15 +307,17 @@ def test_routed_training_step_full_size():
     torch.cuda.synchronize()
     dx_expert = h32(plan.dx)
     # the gathered backward equals the permute + unfused backward bit for bit
-    case("full-size gathered backward vs permute + unfused backward (balanced_bwd)")
+    case("full-size fused backward (gathered X, dY on load) vs permute + combine_bwd's dY + "
+         "unfused backward (balanced_bwd)")
     xp = laep.moe_permute(x, plan.dest_row, w.k, plan.R)
     h_fwd = laep.ffn_fwd_h_view(plan.ws_ffn, plan.R, w.d_ff, BF)
-    dxp, dwgu_u, dwd_u = laep.moe_grouped_ffn_bwd(plan.dy_perm, xp, plan.act_save, wgu, wd,
+    dyp, _ = laep.moe_combine_bwd(dout, plan.y_perm, plan.topk_gate, plan.dest_row)
+    dxp, dwgu_u, dwd_u = laep.moe_grouped_ffn_bwd(dyp, xp, plan.act_save, wgu, wd,
                                                   plan.offsets, h_fwd=h_fwd)
     torch.cuda.synchronize()
     assert torch.equal(dxp, plan.dx_perm)
     assert torch.equal(dwgu_u, plan.dw_gate_up) and torch.equal(dwd_u, plan.dw_down)
-    del xp, dxp, dwgu_u, dwd_u
+    del xp, dyp, dxp, dwgu_u, dwd_u
     plan.route_backward(x, wr, renorm=w.renorm, want_dbias=True)
     torch.cuda.synchronize()
     rl, rw, rb, rx = om.route_bwd(hint(plan.dgate).astype(np.float64), hint(plan.topk_idx),

@@ -385,8 +385,10 @@ def test_ffn_fwd_gather_matches_permute_then_ffn(T, k, E, d, f, mapped):
 def test_ffn_bwd_gather_matches_permute_then_bwd(T, k, E, d, f, mapped):
     """The weight gradient reading X's routed rows from the token rows through
     row_src (moe_grouped_ffn_bwd_gather) is bit-identical to moe_permute +
-    moe_grouped_ffn_bwd, with and without the forward's H, and its weight
-    gradients match the oracle (teacher-forced on the GPU's dA and H)."""
+    moe_grouped_ffn_bwd, with and without the forward's H, and so is the
+    variant that forms dY = g * dout on load (against moe_combine_bwd's
+    dy_perm); its weight gradients match the oracle (teacher-forced on the
+    GPU's dA and H)."""
     rng = np.random.default_rng(3 * T + E)
     n_phys = E + 2 if mapped else E
     c = random_case(T + 3 * E, T=T, d_model=d, E=n_phys, k=1, d_ff=f, dtype="bf16")
@@ -418,6 +420,25 @@ def test_ffn_bwd_gather_matches_permute_then_bwd(T, k, E, d, f, mapped):
         torch.cuda.synchronize()
         for n, u, g in zip(("dx_perm", "dw_gate_up", "dw_down"), a, b[:3]):
             assert torch.equal(u, g), f"{n} differs (use_h={use_h})"
+    # dY formed on load: the same bits as combine_bwd's dy_perm + unfused backward
+    y_any = torch.randn((R, d), device="cuda").to(bf)
+    dout = dev(rng.standard_normal((T, d)).astype(np.float32), bf)
+    gates = dev(rng.uniform(0.05, 1.0, size=(T, k)).astype(np.float32), torch.float32)
+    dy_c, dg_c = laep.moe_combine_bwd(dout, y_any, gates, dest_row)
+    _, dg_only = laep.moe_combine_bwd(dout, y_any, gates, dest_row, want_dy=False)
+    for use_h in (False, True):
+        h = h_f if use_h else None
+        a = laep.moe_grouped_ffn_bwd(dy_c, x_perm, act, wgu, wd, offsets, h_fwd=h,
+                                     expert_map=emap, dw_gate_up=zeros(wgu), dw_down=zeros(wd))
+        case(f"ffn bwd gather, dY on load, use_h={use_h}")
+        c2 = laep.moe_grouped_ffn_bwd_gather(None, x, row_src, k, act, wgu, wd, offsets,
+                                             dout=dout, topk_gate=gates, h_fwd=h,
+                                             expert_map=emap, dw_gate_up=zeros(wgu),
+                                             dw_down=zeros(wd))
+        torch.cuda.synchronize()
+        for n, u, g in zip(("dx_perm", "dw_gate_up", "dw_down"), a, c2):
+            assert torch.equal(u, g), f"{n} differs with dY on load (use_h={use_h})"
+    assert torch.equal(dg_c, dg_only)
     # weight gradients against the oracle, on the oracle's dispatched rows
     dA_g, _ = laep.ffn_bwd_ws_views(b[3], R, f, bf)
     rc, ro, rdst = om.expert_counts(ids, E)
