@@ -9,9 +9,13 @@
 //  3. scatter: dest_row[t*k + j] = base[w][e] + popc(masks[w][e] & lanes < t),
 //     i.e. rows grouped by expert, ordered by token inside a group.
 // The router can write the masks itself (moe_route_count); the counting pass
-// then starts at the scan.  Beyond 512 wave tiles the scan runs in two
-// levels: partial sums per block of 64 tiles, one workgroup over the blocks,
-// then each block's tile bases.
+// then starts at the scan.  Up to 32768 masks (e.g. 8192 tokens over 64
+// experts) the scan and the scatter are one kernel: every workgroup sums the
+// masks itself (L2-resident, at most 256 KB) into the expert totals, their
+// exclusive scan and its own first base, so no single-workgroup scan and no
+// launch sits between them.  Beyond that, and beyond 512 wave tiles, the scan
+// runs in two levels: partial sums per block of 64 tiles, one workgroup over
+// the blocks, then each block's tile bases.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -98,6 +102,120 @@ __global__ __launch_bounds__(kScanThreads) void count_scan_kernel(
       run += __popcll(masks[(size_t)w * E + e]);
     }
   }
+}
+
+// ---- small T·E: scan and scatter in one kernel ----------------------------------
+constexpr int kFusedMasks = 32768;
+constexpr int kCountWT = kCountThreads / 64;  // wave tiles per workgroup
+constexpr int kPreSlots = 8;                  // routing slots per token loaded up front
+
+// Workgroup b takes wave tiles 4b .. 4b+3 (wave i, tile 4b+i, lane = token).
+//  1. thread (c, e) sums popc(masks[w][e]) over chunk c of all tiles, and over
+//     the tiles before 4b; it keeps the masks of the workgroup's own tiles;
+//  2. expert totals, their exclusive scan (wave prefix sums + wave totals),
+//     and base[4b][e] = offset[e] + the slots of e in earlier tiles;
+//  3. the bases of the four tiles, then the scatter as in count_scatter_kernel.
+// Workgroup 0 also writes counts, offsets and the expert-token accumulator.
+__global__ __launch_bounds__(kCountThreads) void count_scan_scatter_kernel(
+    const int32_t* __restrict__ idx, int n_tok, int k, int E, int E_pad, int n_wt,
+    const uint64_t* __restrict__ masks, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int64_t* __restrict__ etn, int32_t* __restrict__ dest_row,
+    int32_t* __restrict__ row_src) {
+  __shared__ int s_tot[kCountThreads];
+  __shared__ int s_pre[kCountThreads];
+  __shared__ int s_wsum[kCountWT];
+  __shared__ int s_base[kCountWT][256];
+  __shared__ uint64_t s_mask[kCountWT][256];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int w0 = blockIdx.x * kCountWT;
+
+  // the scatter's expert ids, loaded first so they arrive during the counting
+  const int wt = w0 + wave;
+  const int t = wt * 64 + lane;
+  const bool tok_ok = wt < n_wt && t < n_tok;
+  int e_pre[kPreSlots];
+#pragma unroll
+  for (int j = 0; j < kPreSlots; ++j)
+    e_pre[j] = (tok_ok && j < k) ? idx[(size_t)t * k + j] : -1;
+
+  // 1.
+  const int nc = kCountThreads / E_pad;
+  const int c = tid / E_pad, e = tid % E_pad;
+  const int per = (n_wt + nc - 1) / nc;
+  const int lo = min(c * per, n_wt), hi = min(lo + per, n_wt);
+  int tot = 0, pre = 0;
+  if (e < E) {
+    // batches of 32 loads in flight (one batch at 8192 tokens over 64 experts)
+    for (int w = lo; w < hi; w += 32) {
+      uint64_t m[32];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) m[u] = w + u < hi ? masks[(size_t)(w + u) * E + e] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 32; ++u) {
+        const int n = __popcll(m[u]);
+        const int wu = w + u;
+        tot += n;
+        pre += wu < w0 ? n : 0;
+        if (wu < hi && wu >= w0 && wu < w0 + kCountWT) s_mask[wu - w0][e] = m[u];
+      }
+    }
+  }
+  s_tot[tid] = tot;
+  s_pre[tid] = pre;
+  __syncthreads();
+
+  // 2.
+  int te = 0, pe = 0;
+  if (tid < E) {
+    for (int cc = 0; cc < nc; ++cc) {
+      te += s_tot[cc * E_pad + tid];
+      pe += s_pre[cc * E_pad + tid];
+    }
+  }
+  int inc = te;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(inc, o);
+    inc += lane >= o ? v : 0;
+  }
+  if (lane == 63) s_wsum[wave] = inc;
+  __syncthreads();
+  int before = 0;
+  for (int wv = 0; wv < wave; ++wv) before += s_wsum[wv];
+  const int off = before + inc - te;  // exclusive scan of the expert totals
+  if (tid < E) {
+    if (blockIdx.x == 0) {
+      counts[tid] = te;
+      offsets[tid] = off;
+      if (etn != nullptr) etn[tid] += te;
+      if (tid == E - 1) offsets[E] = off + te;
+    }
+    // 3.
+    int run = off + pe;
+#pragma unroll
+    for (int i = 0; i < kCountWT; ++i) {
+      s_base[i][tid] = run;
+      run += w0 + i < n_wt ? __popcll(s_mask[i][tid]) : 0;
+    }
+  }
+  __syncthreads();
+
+  if (!tok_ok) return;
+  const uint64_t lt = lanemask_lt();
+  auto place = [&](int j, int raw) {
+    const size_t s = (size_t)t * k + j;
+    const int ev = valid_expert(raw, E);
+    int dst = -1;
+    if (ev >= 0) {
+      dst = s_base[wave][ev] + __popcll(s_mask[wave][ev] & lt);
+      if (row_src != nullptr) row_src[dst] = (int32_t)s;
+    }
+    dest_row[s] = dst;
+  };
+#pragma unroll
+  for (int j = 0; j < kPreSlots; ++j)
+    if (j < k) place(j, e_pre[j]);
+  for (int j = kPreSlots; j < k; ++j) place(j, idx[(size_t)t * k + j]);
 }
 
 // ---- large T: the scan in two levels -------------------------------------------
@@ -258,6 +376,12 @@ hipError_t launch_counts(const int32_t* idx, int T, int k, int E, int32_t* count
   if (n_wt > 0 && !masks_ready)
     hipLaunchKernelGGL(count_masks_kernel, dim3(blocks), dim3(kCountThreads), 0, s, idx, T, k, E,
                        n_wt, masks);
+  if (n_wt <= kLargeTiles && (int64_t)n_wt * E <= kFusedMasks) {
+    const int gb = n_wt > 0 ? blocks : 1;  // one workgroup still writes counts and offsets
+    hipLaunchKernelGGL(count_scan_scatter_kernel, dim3(gb), dim3(kCountThreads), 0, s, idx, T, k,
+                       E, E_pad, n_wt, masks, counts, offsets, etn, dest_row, row_src);
+    return hipGetLastError();
+  }
   if (n_wt > kLargeTiles) {
     const int n_blk = (n_wt + kTilesPerBlk - 1) / kTilesPerBlk;
     int32_t* partial = reinterpret_cast<int32_t*>(

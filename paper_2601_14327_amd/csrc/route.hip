@@ -8,10 +8,11 @@
 //     eight blocks staged, each thread summing its elements over the waves)
 //     where the stage buffers hold them, else as a tree.
 //     bf16 with up to 128 experts: x and W_r go through LDS in chunks of 256
-//     (or 128) columns by LDS-DMA, 3-4 stages deep, so every global request
-//     is a whole 128-byte line (in the MFMA operand layout a direct load
-//     touches 32 bytes of each of 32 rows, four requests per line).  Other
-//     cases load the operands directly, U k-steps per chunk in flight.
+//     (or 128) columns by LDS-DMA, in two rings (x 5-8 stages deep, W_r two),
+//     so every global request is a whole 128-byte line (in the MFMA operand
+//     layout a direct load touches 32 bytes of each of 32 rows, four requests
+//     per line) and several chunks of x are in flight.  Other cases load the
+//     operands directly, U k-steps per chunk in flight.
 //  2. top-k: 16 lanes (one DPP row) per token, lane g owning experts
 //     e = 16q + g.  k passes of a (value desc, index asc) arg-max across the
 //     16 lanes, exchanged by DPP lane permutations.  The slot order is
@@ -64,27 +65,33 @@ __device__ __forceinline__ u32x4_t load16_or_zero(const T* p, bool ok) {
 }
 
 // x and W_r chunks of KC columns staged through LDS by LDS-DMA (whole 128-byte
-// lines per request), for bf16 and d % KC == 0.  Rows of the stage: 32 tokens,
-// then EP experts; 16-byte chunk c of row r sits at c ^ (r & 15).
+// lines per request), for bf16 and d % KC == 0, in two rings: NSX stages of
+// x (32 token rows) and two of W_r (EP expert rows).  16-byte chunk c of
+// row r of a stage sits at c ^ (r & 15).
 template <int NB, int KC>
 struct RouterStage {
   static constexpr int EP = 32 * NB;
-  static constexpr int ROWS = 32 + EP;
   static constexpr int RB = KC * 2;          // bytes per staged row
   static constexpr int CPR = RB / 16;        // chunks per row
-  static constexpr int BYTES = ROWS * RB;
-  static constexpr int NCH = ROWS * CPR / kRouteThreads;  // DMA chunks per thread
-  static_assert((ROWS * CPR) % kRouteThreads == 0, "stage chunks must divide over the threads");
-  // stages in flight: as many as fit next to the logits tile, at most 4
+  static constexpr int XS = 32 * RB;         // x stage bytes
+  static constexpr int WS = EP * RB;         // W_r stage bytes
+  static constexpr int NCHX = 32 * CPR / kRouteThreads;  // DMA chunks per thread and stage
+  static constexpr int NCHW = EP * CPR / kRouteThreads;
+  static_assert(NCHX * kRouteThreads == 32 * CPR && NCHW * kRouteThreads == EP * CPR,
+                "stage chunks must divide over the threads");
+  static constexpr int NSW = 2;
+  // x stages: as many as fit beside the two W_r stages and the logits tile,
+  // at most 8
   static constexpr int LOGITS = 32 * (EP + 1) * 4;
-  static constexpr int FIT = (156 * 1024 - LOGITS) / BYTES;
-  static constexpr int NS = FIT > 4 ? 4 : FIT;
-  static_assert(NS >= 2, "at least two stages");
+  static constexpr int FITX = (156 * 1024 - LOGITS - NSW * WS) / XS;
+  static constexpr int NSX = FITX > 8 ? 8 : FITX;
+  static_assert(NSX >= 2, "at least two x stages");
+  static constexpr int BYTES = NSX * XS + NSW * WS;
 };
 
 template <int NB, int KC>
 struct StageBytes {
-  static constexpr int value = RouterStage<NB, KC>::NS * RouterStage<NB, KC>::BYTES;
+  static constexpr int value = RouterStage<NB, KC>::BYTES;
 };
 template <int NB>
 struct StageBytes<NB, 0> {
@@ -140,6 +147,15 @@ __device__ __forceinline__ void route_dma(char* dst, __amdgpu_buffer_rsrc_t rx,
   }
 }
 
+// A workgroup barrier ordering LDS accesses only: unlike __syncthreads it does
+// not wait for this wave's global stores to be acknowledged (which costs a
+// memory round trip right after the top-k writes its slots).
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int N>
 __device__ __forceinline__ void route_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
@@ -177,10 +193,16 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   const int lane = tid & 63;
   const int t0 = blockIdx.x * kRouteTokens;
 
-  for (int e = tid; e < EP; e += kRouteThreads) {
-    s_bias[e] = (bias != nullptr && e < E) ? bias[e] : 0.0f;
-    s_alive[e] = (e < E) ? (alive == nullptr ? 1 : (alive[e] != 0)) : 0;
-    s_mask[e] = 0u;
+  // expert e = tid (EP <= 256 < the thread count): its bias and alive flag are
+  // loaded now and stored to LDS after the GEMM, so the operand loads are
+  // not queued behind a round trip for them
+  static_assert(EP <= kRouteThreads, "one expert per thread");
+  // (the raw byte is kept: testing it here would wait for the load)
+  float bias_e = 0.0f;
+  uint32_t alive_raw = 1;
+  if (tid < E) {
+    if (bias != nullptr) bias_e = bias[tid];
+    if (alive != nullptr) alive_raw = alive[tid];
   }
 
   // ---- 1. router GEMM -----------------------------------------------------
@@ -193,71 +215,90 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   const int row = lane & 31;
   const int kh = lane >> 5;
   if constexpr (KC > 0) {
-    // LDS-staged: every thread fills NCH chunks of each stage; the waves
-    // share the KC/16 k-steps of a stage round robin.
+    // LDS-staged: every thread fills NCHX chunks of each x stage and NCHW of
+    // each W_r stage; the waves share the KC/16 k-steps of a chunk round robin.
     using St = RouterStage<NB, KC>;
-    static_assert(St::CPR % 2 == 0, "a wave's 64 chunks must not straddle the x / W_r boundary");
     // x from the workgroup's first token (32 rows: 32-bit offsets), W_r whole
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<T*>(x + (size_t)t0 * d), 0, -1, kRouteBufferFlags);
     const __amdgpu_buffer_rsrc_t rw =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(w), 0, -1, kRouteBufferFlags);
     const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-    uint32_t voff[St::NCH];
+    uint32_t voffx[St::NCHX], voffw[St::NCHW];
 #pragma unroll
-    for (int i = 0; i < St::NCH; ++i) {
+    for (int i = 0; i < St::NCHX; ++i) {
       const int q = i * kRouteThreads + tid;
       const int r = q / St::CPR;
       const int lc = (q % St::CPR) ^ (r & 15);
-      if (r < 32) {
-        const int t = t0 + r < n_tok ? r : n_tok - 1 - t0;
-        voff[i] = (uint32_t)(((size_t)t * d + lc * 8) * 2);
-      } else {
-        const int e = r - 32 < E ? r - 32 : E - 1;
-        voff[i] = (uint32_t)(((size_t)e * d + lc * 8) * 2);
-      }
+      const int t = t0 + r < n_tok ? r : n_tok - 1 - t0;
+      voffx[i] = (uint32_t)(((size_t)t * d + lc * 8) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < St::NCHW; ++i) {
+      const int q = i * kRouteThreads + tid;
+      const int r = q / St::CPR;
+      const int lc = (q % St::CPR) ^ (r & 15);
+      const int e = r < E ? r : E - 1;
+      voffw[i] = (uint32_t)(((size_t)e * d + lc * 8) * 2);
     }
     const int n_chunks = d / KC;
-    // NS stages: chunks c .. c+NS-2 in flight while chunk c computes.  Past the
-    // end the last chunk is loaded again into the free stage (never read), so
-    // one constant vmcnt serves every wait.
-    constexpr int NS = St::NS;
+    // Two rings.  x streams from HBM, NSX-1 chunks ahead; W_r (L2-resident)
+    // one chunk ahead.  The load counter completes in issue order, so a
+    // W_r chunk issued behind x's lands only after them; with x and W_r in
+    // one stage (as before) that held x to the stage depth (2 chunks of x in
+    // flight, 8 MB over the chip, well short of what HBM latency needs).
+    // Iteration c issues x(c+NSX-1), then W(c+1), and waits for W(c): 
+    // everything issued before it, x(c) .. x(c+NSX-2) included, has landed.
+    // Past the end the last chunk is loaded again into the free stage (never
+    // read), so one constant vmcnt serves every wait.
+    constexpr int NSX = St::NSX;
+    char* const s_x = s_stage;
+    char* const s_w = s_stage + NSX * St::XS;
     // Workgroups on one XCD (block i runs on XCD i % 8) start at different
     // chunks, so they do not all request the same W_r lines at once.
     const int rot = (int)((blockIdx.x >> 3) % n_chunks);
-    auto issue = [&](int c) {
+    auto rotated = [&](int c) {
       const int cl = c < n_chunks ? c : n_chunks - 1;
-      const int cc = cl + rot < n_chunks ? cl + rot : cl + rot - n_chunks;
-      route_dma<St::NCH, 32 * St::CPR>(s_stage + (c % NS) * St::BYTES, rx, rw, voff, cc * KC * 2,
-                                        wave_s);
+      return cl + rot < n_chunks ? cl + rot : cl + rot - n_chunks;
     };
+    auto issue_x = [&](int c) {
+      route_dma<St::NCHX, St::NCHX * kRouteThreads>(s_x + (c % NSX) * St::XS, rx, rw, voffx,
+                                                     rotated(c) * KC * 2, wave_s);
+    };
+    auto issue_w = [&](int c) {
+      route_dma<St::NCHW, 0>(s_w + (c & 1) * St::WS, rx, rw, voffw, rotated(c) * KC * 2, wave_s);
+    };
+    static_assert(KC / 16 % kRouteWaves == 0, "every wave takes the same number of k-steps");
+    constexpr int U = KC / 16 / kRouteWaves;  // k-steps per wave and chunk
 #pragma unroll
-    for (int c = 0; c < NS - 1; ++c) issue(c);
+    for (int c = 0; c < NSX - 1; ++c) issue_x(c);
+    issue_w(0);
     for (int c = 0; c < n_chunks; ++c) {
-      const char* st = s_stage + (c % NS) * St::BYTES;
-      issue(c + NS - 1);                       // into the stage chunk c-1 used
+      issue_x(c + NSX - 1);                   // into the x stage chunk c-1 used
+      issue_w(c + 1);                         // into the W_r stage chunk c-1 used
       // chunk c has landed: this thread's loads (the counter), then every
       // thread's (a bare barrier: __syncthreads' fence would make the compiler
       // wait for every load in flight, the later chunks' too)
-      route_wait_vmcnt<(NS - 1) * St::NCH>();
+      route_wait_vmcnt<St::NCHX + St::NCHW>();
       __builtin_amdgcn_s_barrier();
-      static_assert(KC / 16 % kRouteWaves == 0, "every wave takes the same number of k-steps");
+      const char* sx = s_x + (c % NSX) * St::XS;
+      const char* sw = s_w + (c & 1) * St::WS;
 #pragma unroll
-      for (int u = 0; u < KC / 16 / kRouteWaves; ++u) {
+      for (int u = 0; u < U; ++u) {
         const int s = wave + u * kRouteWaves;
         const int lc = 2 * s + kh;
         const u32x4_t a =
-            *reinterpret_cast<const u32x4_t*>(st + row * St::RB + ((lc ^ (row & 15)) << 4));
+            *reinterpret_cast<const u32x4_t*>(sx + row * St::RB + ((lc ^ (row & 15)) << 4));
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const int r = 32 + nb * 32 + row;
+          const int r = nb * 32 + row;
           const u32x4_t bv =
-              *reinterpret_cast<const u32x4_t*>(st + r * St::RB + ((lc ^ (r & 15)) << 4));
+              *reinterpret_cast<const u32x4_t*>(sw + r * St::RB + ((lc ^ (r & 15)) << 4));
           RouterStep<bf16_t>::mma(acc[nb], a, bv);
         }
       }
-      // every thread's reads of stage c % NS are done: it is refilled at the
-      // next iteration
+      // every thread's reads of chunk c's stages are done: they are refilled
+      // at the next iteration
       __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));  // lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
     }
@@ -295,34 +336,51 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     }
   }
 
+  // opaque to the compiler until here, so the test of the byte is not hoisted
+  // next to its load (with a wait for it in front of the operand loads)
+  asm volatile("" : "+v"(alive_raw));
+  if (tid < EP) {  // published by the first barrier of the cross-wave sum
+    s_bias[tid] = bias_e;
+    s_alive[tid] = tid < E && alive_raw != 0;
+    s_mask[tid] = 0u;
+  }
+
   // ---- cross-wave sum, deterministic ----------------------------------------------
   // acc[nb][r]: token (r/4)*8 + kh*4 + r%4, expert nb*32 + row.
   auto tile_at = [&](int nb, int r, int& t, int& e) {
     t = (r >> 2) * 8 + kh * 4 + (r & 3);
     e = nb * 32 + row;
   };
-  constexpr bool kOneRound = KC > 0 && kRouteWaves * 32 * EP * 4 <= StageBytes<NB, KC>::value;
+  // one-round partial blocks: [wave][expert][token], rows padded to 36 floats
+  // so the 16-byte writes of 8 lanes (8 experts) fall in distinct banks
+  constexpr int kPartTP = 36;
+  constexpr bool kOneRound =
+      KC > 0 && kRouteWaves * EP * kPartTP * 4 <= StageBytes<NB, KC>::value;
   if constexpr (kOneRound) {
-    // every wave's partial block to the idle stage buffers, then each thread
-    // sums its elements over the waves in wave order and adds the bias
+    // every wave's partial block to the idle stage buffers (acc[nb][4g..4g+3]
+    // are tokens 8g + 4kh .. +3 of one expert: one 16-byte write), then each
+    // thread sums 4 tokens of one expert over the waves in wave order and adds
+    // the bias
     float* part = reinterpret_cast<float*>(s_stage);
-    constexpr int SL = 32 * EP;
+    constexpr int SL = EP * kPartTP;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        int t, e;
-        tile_at(nb, r, t, e);
-        part[wave * SL + t * EP + e] = acc[nb][r];
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const f32x4_t v4 = {acc[nb][4 * g4], acc[nb][4 * g4 + 1], acc[nb][4 * g4 + 2],
+                            acc[nb][4 * g4 + 3]};
+        *reinterpret_cast<f32x4_t*>(part + wave * SL + (nb * 32 + row) * kPartTP + g4 * 8 +
+                                    kh * 4) = v4;
       }
-    __syncthreads();
-    for (int i = tid * 4; i < SL; i += kRouteThreads * 4) {
-      f32x4_t sum = *reinterpret_cast<const f32x4_t*>(part + i);
+    lds_sync();
+    for (int i = tid; i < EP * 8; i += kRouteThreads) {
+      const int e = i >> 3, t = (i & 7) * 4;
+      f32x4_t sum = *reinterpret_cast<const f32x4_t*>(part + e * kPartTP + t);
 #pragma unroll
-      for (int wv = 1; wv < kRouteWaves; ++wv) sum += *reinterpret_cast<const f32x4_t*>(part + wv * SL + i);
-      const int t = i / EP, e = i % EP;
+      for (int wv = 1; wv < kRouteWaves; ++wv)
+        sum += *reinterpret_cast<const f32x4_t*>(part + wv * SL + e * kPartTP + t);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s_log[t * LD + e + q] = sum[q] + s_bias[e + q];
+      for (int q = 0; q < 4; ++q) s_log[(t + q) * LD + e] = sum[q] + s_bias[e];
     }
   } else if constexpr (KC > 0) {
     // a tree over the waves (8 -> 4 -> 2 -> 1) through the idle stage buffers
@@ -389,7 +447,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
       s_log[t * LD + e] += s_bias[e];
     }
   }
-  __syncthreads();
+  lds_sync();
 
   if (logits_out != nullptr) {
     for (int i = tid; i < kRouteTokens * E; i += kRouteThreads) {
@@ -408,7 +466,7 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
     const int e = q * 16 + g;
     v[q] = s_alive[e] ? s_log[ti * LD + e] : -INFINITY;
   }
-  __syncthreads();  // s_log is reused below for the gate numerators
+  lds_sync();  // s_log is reused below for the gate numerators
 
   // row maximum and (renorm == 0) the softmax denominator over alive experts
   float vmax = -INFINITY;
@@ -434,33 +492,82 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   const int t_glob = t0 + ti;
   const bool write_ok = t_glob < n_tok;
   float s_sel = 0.0f;
-  for (int j = 0; j < k; ++j) {
-    float bv = -INFINITY;
-    int be = 0x7FFFFFFF;
+  // Up to 16 slots: pass j's result stays in lane j of the token's row.  Each
+  // pass takes the largest value across the row, then the lowest expert index
+  // holding it (the order of a (value desc, index asc) arg-max), on integer
+  // keys that order like the floats: -0 is first made +0 and NaN -inf, so
+  // equal keys are exactly equal values, and each step is one DPP max or min.
+  // Taken slots get INT_MIN, below the key of -inf (a dead expert, never
+  // taken: the pass then finds nothing).
+  const bool by_lane = k <= 16;
+  int my_e = -1;
+  float my_ex = 0.0f;
+  if (by_lane) {
+    constexpr int kKeyNegInf = (int)(0xFF800000u ^ 0x7FFFFFFFu);
+    int key[EPL];
 #pragma unroll
     for (int q = 0; q < EPL; ++q) {
-      const int e = q * 16 + g;
-      if (v[q] > bv) { bv = v[q]; be = e; }  // ascending e: strict keeps the lower index
+      const float f = v[q] != v[q] ? -INFINITY : v[q] + 0.0f;
+      const int b = __float_as_int(f);
+      key[q] = b >= 0 ? b : b ^ 0x7FFFFFFF;
     }
-    argmax_step<kDppXor1>(bv, be);
-    argmax_step<kDppXor2>(bv, be);
-    argmax_step<kDppHalfMirror>(bv, be);
-    argmax_step<kDppMirror>(bv, be);
-    const bool found = (bv != -INFINITY);
-    if (found && (be & 15) == g) {
+    for (int j = 0; j < k; ++j) {
+      int m = key[0];
 #pragma unroll
-      for (int q = 0; q < EPL; ++q)
-        if (q * 16 + g == be) v[q] = -INFINITY;
+      for (int q = 1; q < EPL; ++q) m = max(m, key[q]);
+      m = max(m, dpp_i<kDppXor1>(m));
+      m = max(m, dpp_i<kDppXor2>(m));
+      m = max(m, dpp_i<kDppHalfMirror>(m));
+      m = max(m, dpp_i<kDppMirror>(m));
+      int ce = 0x7FFFFFFF;
+#pragma unroll
+      for (int q = EPL - 1; q >= 0; --q) ce = key[q] == m ? q * 16 + g : ce;
+      ce = min(ce, dpp_i<kDppXor1>(ce));
+      ce = min(ce, dpp_i<kDppXor2>(ce));
+      ce = min(ce, dpp_i<kDppHalfMirror>(ce));
+      ce = min(ce, dpp_i<kDppMirror>(ce));
+      const bool found = m > kKeyNegInf;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) key[q] = q * 16 + g == ce ? (int)0x80000000 : key[q];
+      const float mv = __int_as_float(m >= 0 ? m : m ^ 0x7FFFFFFF);
+      const float ex = found ? __expf(mv - vmax) : 0.0f;
+      s_sel += ex;
+      my_e = g == j ? (found ? ce : -1) : my_e;
+      my_ex = g == j ? ex : my_ex;
     }
-    const float ex = found ? __expf(bv - vmax) : 0.0f;
-    s_sel += ex;
-    if (g == 0) {
-      s_ex[ti * k + j] = ex;
-      if (write_ok) idx_out[(size_t)t_glob * k + j] = found ? be : -1;
-      if (masks32 != nullptr && write_ok && found) atomicOr(&s_mask[be], 1u << ti);
+    if (write_ok && g < k) {
+      idx_out[(size_t)t_glob * k + g] = my_e;
+      if (masks32 != nullptr && my_e >= 0) atomicOr(&s_mask[my_e], 1u << ti);
+    }
+  } else {
+    for (int j = 0; j < k; ++j) {
+      float bv = -INFINITY;
+      int be = 0x7FFFFFFF;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const int e = q * 16 + g;
+        if (v[q] > bv) { bv = v[q]; be = e; }  // ascending e: strict keeps the lower index
+      }
+      argmax_step<kDppXor1>(bv, be);
+      argmax_step<kDppXor2>(bv, be);
+      argmax_step<kDppHalfMirror>(bv, be);
+      argmax_step<kDppMirror>(bv, be);
+      const bool found = (bv != -INFINITY);
+      if (found && (be & 15) == g) {
+#pragma unroll
+        for (int q = 0; q < EPL; ++q)
+          if (q * 16 + g == be) v[q] = -INFINITY;
+      }
+      const float ex = found ? __expf(bv - vmax) : 0.0f;
+      s_sel += ex;
+      if (g == 0) {
+        s_ex[ti * k + j] = ex;
+        if (write_ok) idx_out[(size_t)t_glob * k + j] = found ? be : -1;
+        if (masks32 != nullptr && write_ok && found) atomicOr(&s_mask[be], 1u << ti);
+      }
     }
   }
-  __syncthreads();
+  lds_sync();  // the expert masks are complete (the slots' global stores need not be)
   if (masks32 != nullptr) {
     // mask word of (wave tile blockIdx/2, expert e): tokens 0-31 of the tile
     // in the low word, 32-63 in the high word; a last even workgroup also
@@ -475,10 +582,13 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   }
   const float denom = renorm ? s_sel : s_all;
   const float inv_ok = (denom > 0.0f) ? 1.0f : 0.0f;
+  const float den = denom > 0.0f ? denom : 1.0f;
   if (write_ok) {
-    for (int j = g; j < k; j += 16) {
-      const float ex = s_ex[ti * k + j];
-      gate_out[(size_t)t_glob * k + j] = inv_ok * (ex / (denom > 0.0f ? denom : 1.0f));
+    if (by_lane) {
+      if (g < k) gate_out[(size_t)t_glob * k + g] = inv_ok * (my_ex / den);
+    } else {
+      for (int j = g; j < k; j += 16)
+        gate_out[(size_t)t_glob * k + j] = inv_ok * (s_ex[ti * k + j] / den);
     }
   }
 }
