@@ -53,6 +53,9 @@ Profiling helpers (used by the commands recorded under profiles/):
   --summarize-pmc DIR         turn FETCH_SIZE / WRITE_SIZE counter CSVs into the
                               traffic summary (--out FILE)
   --summarize-trace DIR       turn a --kernel-trace --stats run into a summary
+  --summarize-counters DIR    turn --pmc runs of SQ / GRBM counters on one call
+                              into a per-kernel summary (MFMA busy, LDS, waits,
+                              clock)
 """
 from __future__ import annotations
 
@@ -558,6 +561,75 @@ def summarize_pmc(args):
     print(text)
 
 
+def summarize_counters(args):
+    """Per-kernel averages per dispatch of every counter in the --pmc runs under
+    DIR (one subdirectory per pass, each of the call PROFILE_CALLS times after
+    the marker dispatch), and the ratios derived from them:
+      clock        GRBM_GUI_ACTIVE / dispatch duration (the GPU clock while busy)
+      mfma_busy    SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES): share of
+                   the CUs' busy cycles in which a SIMD's matrix core was busy
+      mfma_cycles  SQ_VALU_MFMA_BUSY_CYCLES / SQ_INSTS_MFMA (cycles per MFMA)
+      lds_conflict SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE
+      wait_any, wait_inst, wait_lds  SQ_WAIT_ANY, SQ_WAIT_INST_ANY,
+                   SQ_WAIT_INST_LDS over SQ_WAVE_CYCLES (shares of wave time)"""
+    import csv
+    d = args.summarize_counters
+    per = {}      # kernel -> counter -> [values]
+    dur = {}      # kernel -> [ns]
+    for sub_dir in sorted(glob.glob(os.path.join(d, "*"))):
+        rows = []
+        for f in glob.glob(os.path.join(sub_dir, "**", "*counter_collection.csv"), recursive=True):
+            rows += list(csv.DictReader(open(f)))
+        if not rows:
+            continue
+        mark = max(int(r["Dispatch_Id"]) for r in rows if "mfma_loop_kernel" in r["Kernel_Name"])
+        seen = set()
+        for r in rows:
+            did = int(r["Dispatch_Id"])
+            if did <= mark:
+                continue
+            k = re.sub(r"\(.*", "", r["Kernel_Name"].replace("(anonymous namespace)::", ""))
+            per.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if (sub_dir, did) not in seen:
+                seen.add((sub_dir, did))
+                dur.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    rec = {"call": args.profile_call, "workload": args.workload, "kernels": {}}
+    lines = [f"# Counters of `{args.profile_call}` on workload `{args.workload}`\n",
+             "rocprofv3 --pmc passes (at most 8 SQ and 2 GRBM counters each), averaged per "
+             "dispatch over the call's dispatches. Ratios: clock = GRBM_GUI_ACTIVE / duration; "
+             "mfma_busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 x SQ_BUSY_CU_CYCLES); mfma_cycles = "
+             "SQ_VALU_MFMA_BUSY_CYCLES / SQ_INSTS_MFMA; lds_conflict = SQ_LDS_BANK_CONFLICT / "
+             "SQ_LDS_IDX_ACTIVE; wait_* = SQ_WAIT_ANY, SQ_WAIT_INST_ANY, SQ_WAIT_INST_LDS over "
+             "SQ_WAVE_CYCLES. Durations are those of the counter runs.\n",
+             "Commands:\n", f"```\n{args.command_note or ''}\n```\n"]
+    for k, cs in per.items():
+        avg = {c: sum(v) / len(v) for c, v in cs.items()}
+        dns = sum(dur[k]) / len(dur[k])
+        g = lambda c: avg.get(c)
+        ratio = lambda a, b, f=1.0: (g(a) / (f * g(b))) if g(a) is not None and g(b) else None
+        der = {"duration_us": dns / 1e3,
+               "clock_ghz": (g("GRBM_GUI_ACTIVE") / dns) if g("GRBM_GUI_ACTIVE") else None,
+               "mfma_busy": ratio("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", 4.0),
+               "mfma_cycles": ratio("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_MFMA"),
+               "lds_conflict": ratio("SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE"),
+               "wait_any": ratio("SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
+               "wait_inst": ratio("SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES"),
+               "wait_lds": ratio("SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES")}
+        rec["kernels"][k] = {"counters": avg, "derived": der}
+        lines.append(f"## `{k[:110]}`\n")
+        lines.append("| derived | value |\n|---|---:|")
+        for n, v in der.items():
+            lines.append(f"| {n} | {'' if v is None else f'{v:.4g}'} |")
+        lines.append("\n| counter | per dispatch |\n|---|---:|")
+        for c in sorted(avg):
+            lines.append(f"| {c} | {avg[c]:.6g} |")
+        lines.append("")
+    text = "\n".join(lines) + f"\n```json\n{json.dumps(rec, indent=1)}\n```\n"
+    with open(args.out, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
 def summarize_trace(args):
     import csv
     f = glob.glob(os.path.join(args.summarize_trace, "**", "*kernel_stats.csv"), recursive=True)[0]
@@ -591,6 +663,7 @@ def main():
                                                  "permute", "combine", "counts"])
     ap.add_argument("--summarize-pmc")
     ap.add_argument("--summarize-trace")
+    ap.add_argument("--summarize-counters")
     ap.add_argument("--profile-call", default="ffn_fwd")
     ap.add_argument("--command-note")
     ap.add_argument("--out")
@@ -599,6 +672,8 @@ def main():
         return summarize_pmc(args)
     if args.summarize_trace:
         return summarize_trace(args)
+    if args.summarize_counters:
+        return summarize_counters(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the library has no "
               f"multi-GPU expert-parallel path.", file=sys.stderr)
