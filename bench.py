@@ -6,8 +6,9 @@ top-8 renormalised softmax gating, SwiGLU d_ff=1024, bf16 with fp32
 accumulation.  One step = one forward pass of the whole layer:
 route + expert counts (one call) -> dispatch + grouped SwiGLU FFN (one call, the
 dispatch folded into the FFN's operand loads) -> combine, every call a kernel
-of the C-ABI library; three input sets rotate over the steps so the
-activations are not cache-resident.  With one slot per token (shard,
+of the C-ABI library; input sets rotate over the steps (at least three, and
+together more than twice the 256 MB MALL) so the activations are not
+cache-resident.  With one slot per token (shard,
 shard_bwd) the combine folds into the FFN call as well (the down projection
 writes each row, times its gate, to its token row).  Training steps write no
 x_perm and no dy_perm: the weight gradient gathers the token rows through
@@ -78,6 +79,7 @@ CSRC = os.path.join(ROOT, "paper_2601_14327_amd", "csrc")
 FFN_FWD_SOURCES = ["gemm_bf16.hip", "gemm_common.hpp", "tiles.hpp", "common.hpp"]
 FFN_BWD_SOURCES = ["gemm_bwd.hip", "gemm_common.hpp", "tiles.hpp", "common.hpp"]
 COPY_CALIB_BYTES = 1 << 32
+MALL_BYTES = 256 << 20   # MI355X last-level (Infinity) cache
 PROFILE_CALLS = 5
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -106,18 +108,30 @@ def _cpu_baseline(w, c, budget_s: float, keep=None):
 
     def run(n):
         t0 = time.perf_counter()
+        sel = slice(None) if keep is None else keep
+        wgu, wd = c["w_gate_up"][sel], c["w_down"][sel]
         if w.routed:
-            sel = slice(None) if keep is None else keep
             bias = c.get("bias")
-            om.layer_forward(c["x"][:n], c["w_router"][sel], c["w_gate_up"][sel],
-                             c["w_down"][sel], w.k, bias=None if bias is None else bias[sel],
-                             renorm=w.renorm, dtype="bf16")
+            f = om.layer_forward(c["x"][:n], c["w_router"][sel], wgu, wd, w.k,
+                                 bias=None if bias is None else bias[sel], renorm=w.renorm,
+                                 dtype="bf16")
         else:
             idx = c["topk_idx"][:n]
             counts, offsets, dest = om.expert_counts(idx, w.E)
             xp = om.permute(c["x"][:n], dest, 1)
-            y, act = om.grouped_ffn_fwd(xp, c["w_gate_up"], c["w_down"], offsets, dtype="bf16")
-            om.combine(y, c["topk_gate"][:n], dest, 1, dtype="bf16")
+            y, act = om.grouped_ffn_fwd(xp, wgu, wd, offsets, dtype="bf16")
+            gate = c["topk_gate"][:n]
+            om.combine(y, gate, dest, 1, dtype="bf16")
+            f = dict(idx=idx, gate=gate, offsets=offsets, dest_row=dest, x_perm=xp, y_perm=y,
+                     act_save=act)
+        if w.backward:   # the training step's backward, the same chain the GPU step runs
+            dy, dgate = om.combine_bwd(c["dout"][:n], f["y_perm"], f["gate"], f["dest_row"], w.k)
+            dxp, dA, hb = om.grouped_ffn_dgrad(dy, f["act_save"], wgu, wd, f["offsets"])
+            om.grouped_ffn_wgrad(dy, f["x_perm"], dA, hb, f["offsets"], wgu.shape[0])
+            dx = om.permute_bwd(dxp, f["dest_row"], w.k)
+            if w.routed:
+                om.route_bwd(dgate, f["idx"], f["gate"], c["x"][:n], c["w_router"][sel],
+                             logits=f["logits"], renorm=w.renorm, dx_in=dx)
         return time.perf_counter() - t0
 
     # grow the sample until one run costs about half the budget (or is whole)
@@ -140,7 +154,8 @@ def _cpu_baseline(w, c, budget_s: float, keep=None):
     unit = "tokens/s" if w.routed else "rows/s"
     return {"value": n / dt, "unit": unit, "cores": threads, "kind": "oracle",
             "sample": f"{n} of {w.T} {'tokens' if w.routed else 'rows'} of the same workload, "
-                      f"layer forward in float64 NumPy ({dt:.1f} s)",
+                      f"layer {'forward + backward' if w.backward else 'forward'} in float64 "
+                      f"NumPy ({dt:.1f} s)",
             "one_thread": one}
 
 
@@ -161,7 +176,10 @@ class Setup:
         bf = torch.bfloat16
         to = lambda a, dt=bf: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dt)
         rng = np.random.default_rng(0)
-        self.n_sets = 3
+        # enough x sets that together they exceed twice the 256 MB MALL, so
+        # no set is still cached when its turn comes again
+        x_bytes = w.T * w.d_model * 2
+        self.n_sets = max(3, -(-2 * MALL_BYTES // x_bytes))
         self.xs = [to(c["x"])] + [to(c["x"][rng.permutation(w.T)]) for _ in range(self.n_sets - 1)]
         self.wgu, self.wd = to(c["w_gate_up"]), to(c["w_down"])
         self.plan = laep.MoELayerPlan(w.T, w.d_model, w.E, w.k, w.d_ff, dtype=bf, device=dev,
@@ -297,7 +315,11 @@ class Setup:
             "counts": T * k * 4 + 2 * (E + 1) * 4 + R * 4,
             "permute": T * d * e + R * d * e + R * 4,
             "combine": R * d * e + T * d * e + 2 * R * 4,
-            "combine_bwd": T * d * e + 2 * R * d * e + 3 * R * 4,
+            # dout and y_perm read, gates and dest rows read, dgate written; dy_perm
+            # written only when the plan keeps it (the fused backward forms dY
+            # on load instead)
+            "combine_bwd": T * d * e + R * d * e + 3 * R * 4
+            + (R * d * e if self.plan.dy_perm is not None else 0),
             "permute_bwd": R * d * e + T * d * e + R * 4,
             # dx read + written, W_r once, x once (summed into dW_r), dgate/gates/ids, dW_r
             "route_bwd": 2 * T * d * e + E * d * e + T * d * e + 3 * T * k * 4 + E * d * 4,

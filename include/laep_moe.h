@@ -423,9 +423,10 @@ int moe_grouped_ffn_fwd_gather_combine(const void* x, const int32_t* row_src,
  *   at byte offset laep_ws_hb_offset(R, d_ff, dtype), H_b [R, d_ff] (dtype)
  *   when h_fwd is NULL, else dH.
  *   Only LAEP_BF16 is supported (LAEP_F32 -> LAEP_ERR_UNSUPPORTED).
- *   Streams: the weight gradients run on the library-owned side stream of the
- *   current device (one per device, created on the first call that uses it,
- *   default priority, kept until the process ends), forked
+ *   Streams: the weight gradients run on a library-owned side stream of the
+ *   current device (a pool of four per device, handed out round robin,
+ *   created on first use, default priority, kept until the process ends; so
+ *   calls on different caller streams overlap on the GPU), forked
  *   from `stream` (dW_d at the start when h_fwd is given, so it overlaps the
  *   first data gradient; otherwise after the SwiGLU backward) and joined back
  *   with events, so the call is ordered on `stream` as a whole and may be

@@ -504,8 +504,7 @@ hipError_t launch_ffn_fwd_bf16(const void* x_perm, const void* w_gu, const void*
   std::unique_lock<std::mutex> lock;
   SideStream* side = nullptr;
   if (x_perm_out && row_src) {
-    lock = side_stream_lock();
-    hipError_t e = side_stream_get(side);
+    hipError_t e = side_stream_acquire(side, lock);
     if (e == hipSuccess) e = side_stream_fork(*side, s);
     if (e == hipSuccess) e = launch_gather_rows(x_perm, row_src, slots_k, R, d, 2, x_perm_out,
                                                 side->stream);

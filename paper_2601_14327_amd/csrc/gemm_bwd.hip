@@ -779,9 +779,9 @@ hipError_t launch_ffn_bwd_bf16(const void* dy, const void* x_perm, const void* a
   // gradients: dW_d from the start when it uses the forward's H, else after
   // the SwiGLU backward like dW_gu; joined back (also after an error) before
   // the call returns.
-  auto lock = side_stream_lock();
+  std::unique_lock<std::mutex> lock;
   SideStream* side = nullptr;
-  hipError_t err = side_stream_get(side);
+  hipError_t err = side_stream_acquire(side, lock);
   if (err != hipSuccess) return err;
   const hipStream_t s2 = side->stream;
   auto fork = [&]() { return side_stream_fork(*side, s); };

@@ -16,15 +16,19 @@ constexpr int kDtypeBf16 = 1;
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
-// Library-owned side stream of the current device (default priority) and its
-// fork / join events, for work a call runs beside the caller's stream.  Hold
-// side_stream_lock() from side_stream_get() through the call's join.
+// Library-owned side streams of the current device (a pool of kSidePool,
+// default priority) with their fork / join events, for work a call runs
+// beside the caller's stream.  side_stream_acquire hands out the next pool
+// entry round robin, locked: keep `lock` from acquisition through the call's
+// join (the entry's events are reused by the next call that takes it).
+// Concurrent calls from different caller streams take different entries, so
+// their side work runs concurrently on the GPU.
+constexpr int kSidePool = 4;
 struct SideStream {
   hipStream_t stream = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
 };
-std::unique_lock<std::mutex> side_stream_lock();
-hipError_t side_stream_get(SideStream*& out);
+hipError_t side_stream_acquire(SideStream*& out, std::unique_lock<std::mutex>& lock);
 // the side stream waits for the work enqueued on s so far
 hipError_t side_stream_fork(const SideStream& ss, hipStream_t s);
 // s waits for the work enqueued on the side stream so far

@@ -1,26 +1,35 @@
-// Library-owned side streams: one per device, default priority, created on
-// first use and kept for the life of the process, with a fork and a join event.
-// A call that runs part of its work beside the caller's stream holds the lock
-// from its fork to its join, since the events are shared.
+// Library-owned side streams: a pool of kSidePool per device, default
+// priority, created on first use and kept for the life of the process, each
+// with a fork and a join event and a lock of its own.  A call that runs part
+// of its work beside the caller's stream takes the next entry round robin and
+// holds its lock from its fork to its join, since the entry's events are
+// shared with the next call that takes it; calls holding different entries
+// proceed (and run on the GPU) concurrently.
+#include <atomic>
+
 #include "internal.hpp"
 
 namespace laep {
 namespace {
 
 constexpr int kMaxDevices = 64;
-std::mutex g_side_mu;
-SideStream g_side[kMaxDevices];
+struct SideSlot {
+  std::mutex mu;
+  SideStream ss;
+};
+SideSlot g_side[kMaxDevices][kSidePool];
+std::atomic<unsigned> g_next[kMaxDevices];
 
 }  // namespace
 
-std::unique_lock<std::mutex> side_stream_lock() { return std::unique_lock<std::mutex>(g_side_mu); }
-
-hipError_t side_stream_get(SideStream*& out) {
+hipError_t side_stream_acquire(SideStream*& out, std::unique_lock<std::mutex>& lock) {
   int dev = 0;
   hipError_t err = hipGetDevice(&dev);
   if (err != hipSuccess) return err;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  SideStream& ss = g_side[dev];
+  SideSlot& slot = g_side[dev][g_next[dev].fetch_add(1, std::memory_order_relaxed) % kSidePool];
+  lock = std::unique_lock<std::mutex>(slot.mu);
+  SideStream& ss = slot.ss;
   if (!ss.stream) {
     if ((err = hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking)) != hipSuccess) return err;
     if ((err = hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming)) != hipSuccess) return err;

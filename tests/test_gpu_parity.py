@@ -451,6 +451,46 @@ def test_ffn_bwd_gather_matches_permute_then_bwd(T, k, E, d, f, mapped):
         assert rownorm_err(got_d[p], rdd[p]) <= TOL_F32, p
 
 
+def test_ffn_bwd_concurrent_calls_on_two_streams():
+    """Two backward calls issued back to back on two caller streams take
+    different library side streams (their weight gradients overlap on the GPU)
+    and give the same bits as the same calls made one after the other."""
+    rng = np.random.default_rng(41)
+    T, k, E, d, f = 700, 4, 8, 256, 128
+    c = random_case(77, T=T, d_model=d, E=E, k=k, d_ff=f, dtype="bf16")
+    bf = torch.bfloat16
+    x, wgu, wd = dev(c["x"], bf), dev(c["w_gate_up"], bf), dev(c["w_down"], bf)
+    ids = np.stack([rng.choice(E, size=k, replace=False) for _ in range(T)]).astype(np.int32)
+    idx = dev(ids, torch.int32)
+    case(f"ffn bwd, two concurrent calls T={T} k={k} E={E} d={d} f={f}")
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+    R = T * k
+    x_perm = laep.moe_permute(x, dest_row, k)
+    _, act = laep.moe_grouped_ffn_fwd(x_perm, wgu, wd, offsets, save_act=True)
+    dys = [dev(rng.standard_normal((R, d)).astype(np.float32), bf) for _ in range(2)]
+    zeros = lambda t: torch.zeros(t.shape, dtype=torch.float32, device="cuda")
+
+    def call(dy):
+        return laep.moe_grouped_ffn_bwd_gather(dy, x, row_src, k, act, wgu, wd, offsets,
+                                               dw_gate_up=zeros(wgu), dw_down=zeros(wd))
+
+    ref = [call(dy) for dy in dys]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    for rep in range(3):
+        outs = [None, None]
+        for i, st in enumerate(streams):
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                outs[i] = call(dys[i])
+        for st in streams:
+            torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        for i in range(2):
+            for n, u, g in zip(("dx_perm", "dw_gate_up", "dw_down"), ref[i], outs[i]):
+                assert torch.equal(u, g), f"{n} differs (call {i}, repetition {rep})"
+
+
 @pytest.mark.parametrize("T,E,d,f,mapped,keep_y", [
     (300, 8, 256, 128, False, False),   # ragged tiles, an empty expert
     (1, 3, 128, 256, False, True),      # a single token
