@@ -319,7 +319,7 @@ class Setup:
             # written only when the plan keeps it (the fused backward forms dY
             # on load instead)
             "combine_bwd": T * d * e + R * d * e + 3 * R * 4
-            + (R * d * e if self.plan.dy_perm is not None else 0),
+            + (R * d * e if getattr(self.plan, "dy_perm", None) is not None else 0),
             "permute_bwd": R * d * e + T * d * e + R * 4,
             # dx read + written, W_r once, x once (summed into dW_r), dgate/gates/ids, dW_r
             "route_bwd": 2 * T * d * e + E * d * e + T * d * e + 3 * T * k * 4 + E * d * 4,

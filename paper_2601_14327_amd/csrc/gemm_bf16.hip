@@ -401,13 +401,427 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_ring_kernel(GemmParams
 }
 
 // ---------------------------------------------------------------------------
+// Persistent variant: one workgroup per CU walks its XCD's contiguous tile
+// range, taking tiles from a per-XCD counter (so uneven tiles balance as the
+// hardware dispatcher would, without a workgroup launch per tile).  When a
+// tile's k-loop ends, the first three halves of the next tile (k-step 0 and
+// the A half of k-step 1) go by LDS-DMA into ring slots 0-2 while the
+// epilogue stages the finished tile through slots 3-4 (64 KB, one wave row
+// of 128 rows per pass); slots 3-4 receive the next tile's halves 3 and 4
+// once the epilogue has read them back.  So the next tile's operand latency
+// runs under the epilogue instead of after it.
+// ---------------------------------------------------------------------------
+// Epilogue staged through 64 KB at `stage` (forward only: no act_save).  The
+// down product's 256-column Y takes one wave row of 128 rows per pass as
+// 512-byte rows; the gate/up product's 128-column H takes all 256 rows in one
+// pass as 256-byte rows.  The 16-byte chunks of a staged row are
+// XOR-swizzled by row, which spreads a wave's 32 rows over the banks without
+// padding.  mid() runs once, after the last staging is published and before
+// its flush, when no accumulator is live any more (the caller issues the next
+// tile's first copies there).
+template <int BM, int BN, int NWM, int NWN, int EPI, typename Mid>
+__device__ __forceinline__ void fwd_epilogue_split(const GemmParams& p, const TileEntry& te,
+                                                   int nt,
+                                                   f32x16_t (&acc)[BM / NWM / 32][BN / NWN / 32],
+                                                   char* stage, Mid&& mid) {
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int WTM = BM / NWM, WTN = BN / NWN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  static_assert(BM == 256 && BN == 256 && NWM == 2, "one wave row of 128 rows per pass");
+  constexpr int PROWS = WTM;  // rows per wide pass
+  static_assert(PROWS * 512 <= 65536 && BM * 256 <= 65536, "stagings fit the 64 KB");
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / NWN, wn = wave % NWN;
+  const int lrow = lane & 31;
+  const int lcol = (lane >> 5) * 4;
+  auto st_wide = [&](int r, int col, float a, float b, float c, float d) {
+    u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
+    *reinterpret_cast<u32x2_t*>(stage + r * 512 + (((col >> 3) ^ (r & 31)) << 4) + (col & 7) * 2) =
+        w;
+  };
+  auto ld_wide = [&](int r, int cc) {
+    return *reinterpret_cast<const u32x4_t*>(stage + r * 512 + ((cc ^ (r & 31)) << 4));
+  };
+  auto st_h = [&](int r, int col, float a, float b, float c, float d) {
+    u32x2_t w = {pack_bf16x2(a, b), pack_bf16x2(c, d)};
+    *reinterpret_cast<u32x2_t*>(stage + r * 256 + (((col >> 3) ^ (r & 15)) << 4) + (col & 7) * 2) =
+        w;
+  };
+  auto ld_h = [&](int r, int cc) {
+    return *reinterpret_cast<const u32x4_t*>(stage + r * 256 + ((cc ^ (r & 15)) << 4));
+  };
+  // staged rows [0, ROWS) (global rows row_base + r of the tile), chunks
+  // cc0 .. cc0 + CPR - 1 of each, to dst + (te.row0 + row_base + r) * ldd
+  // (rows < te.rows, columns < ncols); LDS reads in batches of 4 per wait
+  auto flush = [&](auto rows_tag, auto cpr_tag, auto ld, int row_base, bf16_t* dst, long long ldd,
+                   int ncols, int cc0) {
+    constexpr int ROWS = decltype(rows_tag)::value;
+    constexpr int CPR = decltype(cpr_tag)::value;
+    constexpr int ITERS = ROWS * CPR / NT;
+    constexpr int B = ITERS < 4 ? ITERS : 4;
+    static_assert(ROWS * CPR % NT == 0 && ITERS % B == 0, "flush chunks must divide over the threads");
+#pragma unroll
+    for (int b0 = 0; b0 < ITERS; b0 += B) {
+      u32x4_t v[B];
+#pragma unroll
+      for (int it = 0; it < B; ++it) {
+        const int c = (b0 + it) * NT + tid;
+        v[it] = ld(c / CPR, cc0 + c % CPR);
+      }
+#pragma unroll
+      for (int it = 0; it < B; ++it) {
+        const int c = (b0 + it) * NT + tid;
+        const int r = row_base + c / CPR, cc = c % CPR;
+        if (r < te.rows && cc * 8 < ncols)
+          *reinterpret_cast<u32x4_t*>(dst + (te.row0 + r) * ldd + cc * 8) = v[it];
+      }
+    }
+  };
+  auto sync = [&]() {
+    wait_lgkm0();
+    __builtin_amdgcn_s_barrier();
+  };
+  // the last staging published: every accumulator is in LDS
+  auto publish_last = [&]() {
+    sync();
+    mid();
+  };
+  using R128 = std::integral_constant<int, PROWS>;
+  if (EPI == EPI_GU) {
+    const int f = p.f;
+    const int fbase = nt * (BN / 2);
+    const int fcols = min(BN / 2, f - fbase);
+    auto stage_h = [&](int row_off) {  // H = silu(gate) * up of this wave's rows
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = row_off + i * 32 + lrow;
+#pragma unroll
+        for (int pp = 0; pp < TN / 2; ++pp) {
+          const int grp = (wn * WTN) / 64 + pp;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float h[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              h[c] = fast_silu(acc[i][2 * pp][q * 4 + c]) * acc[i][2 * pp + 1][q * 4 + c];
+            st_h(r, grp * 32 + q * 8 + lcol, h[0], h[1], h[2], h[3]);
+          }
+        }
+      }
+    };
+    // forward only (act_save takes the ring kernel): all of H in one pass
+    stage_h(wm * WTM);
+    publish_last();
+    flush(std::integral_constant<int, BM>{}, std::integral_constant<int, BN / 16>{}, ld_h, 0,
+          p.out + fbase, f, fcols, 0);
+    sync();
+  } else {
+    const int ncols = min(BN, p.N - nt * BN);
+    for (int pass = 0; pass < NWM; ++pass) {
+      if (wm == pass) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = i * 32 + lrow;
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              st_wide(r, wn * WTN + j * 32 + q * 8 + lcol, acc[i][j][q * 4], acc[i][j][q * 4 + 1],
+                      acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
+        }
+      }
+      if (pass == NWM - 1) publish_last();
+      else sync();
+      if (!p.out_tok) {
+        flush(R128{}, std::integral_constant<int, BN / 8>{}, ld_wide, pass * PROWS,
+              p.out + nt * BN, p.ldo, ncols, 0);
+      } else {
+        // scatter: routed row r also goes to its token's row of out_tok, times
+        // its gate, with the combine's arithmetic (fp32 0 + g * y, one rounding)
+        constexpr int CPR = BN / 8, ITERS = PROWS * CPR / NT;
+        u32x4_t v[ITERS];
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          v[it] = ld_wide(c / CPR, c % CPR);
+        }
+#pragma unroll
+        for (int it = 0; it < ITERS; ++it) {
+          const int c = it * NT + tid;
+          const int r = pass * PROWS + c / CPR, cc = c % CPR;
+          if (r < te.rows && cc * 8 < ncols) {
+            const long long row = (long long)te.row0 + r;
+            if (p.out)
+              *reinterpret_cast<u32x4_t*>(p.out + row * p.ldo + nt * BN + cc * 8) = v[it];
+            const int src = p.row_src[row];
+            const float g = p.gate[src];
+            u32x4_t o;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              float lo = 0.0f, hi = 0.0f;
+              lo += g * lo_bf16(v[it][w]);
+              hi += g * hi_bf16(v[it][w]);
+              o[w] = pack_bf16x2(lo, hi);
+            }
+            *reinterpret_cast<u32x4_t*>(p.out_tok + (long long)(src / p.slots_k) * p.ldo +
+                                        nt * BN + cc * 8) = o;
+          }
+        }
+      }
+      sync();
+    }
+  }
+}
+
+template <int NWM, int NWN, int EPI, bool GU_ROWS, bool GATHER>
+__global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_persist_kernel(GemmParams p) {
+  constexpr int BM = 256, BN = 256;
+  constexpr int NT = 64 * NWM * NWN;
+  constexpr int WTM = BM / NWM, WTN = BN / NWN;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int ROWB = 128;                 // bytes per LDS row (64 k)
+  constexpr int HALF = BM * ROWB;           // one operand's k-step, 32 KB
+  constexpr int NSLOT = 5;
+  constexpr int NH = BM * 8 / NT;           // 16-byte chunks per thread per half
+  constexpr int SMEM = NSLOT * HALF;
+  constexpr int NPRE = 3;                   // halves of the next tile issued before the epilogue
+  static_assert(BM == BN, "ring slots hold either operand");
+  static_assert(EPI != EPI_GU || (TN % 2 == 0), "SwiGLU epilogue pairs gate/up blocks");
+  static_assert(TM == 4, "the ragged-tile dispatch below covers 0..4 row blocks");
+  static_assert((NSLOT - NPRE) * HALF >= 65536, "the epilogue stages through the free slots");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / NWN, wn = wave % NWN;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  // thread 0's value to every thread through the first LDS word, while no copy
+  // is in flight; the second barrier keeps it until every thread has read it.
+  // The result is made wave-uniform (readfirstlane), so the tile's table
+  // entry is a scalar load and its buffer descriptors stay in SGPRs (a
+  // per-lane descriptor would put every LDS-DMA in a waterfall loop).
+  auto bcast = [&](int v) {
+    if (tid == 0) *reinterpret_cast<volatile int*>(smem) = v;
+    __syncthreads();
+    const int r = *reinterpret_cast<volatile int*>(smem);
+    __syncthreads();
+    return __builtin_amdgcn_readfirstlane(r);
+  };
+
+  // this XCD's contiguous range of the tile list (block i runs on XCD i % 8)
+  const int n_valid = *p.n_entries;  // one tile per entry
+  const int per = (n_valid + 7) >> 3;
+  const int xcd = blockIdx.x & 7;
+  const int t_lo = xcd * per, t_hi = min(t_lo + per, n_valid);
+  int* const ctr = p.tile_ctr + xcd;
+  // the first tile and the one after it
+  const int L = t_lo + bcast(tid == 0 ? atomicAdd(ctr, 1) : 0);
+  if (L >= t_hi) return;  // (uniform)
+
+  // per-tile operand addressing, in two steps: the tile's rows (through
+  // row_src for gathered A rows; rows past the expert: any valid row), then,
+  // once they have arrived, the copies' offsets and descriptors
+  TileEntry te;
+  uint32_t a_voff[NH], b_voff[NH];
+  __amdgpu_buffer_rsrc_t a_rsrc, b_rsrc;
+  auto load_rows = [&](const TileEntry& t, uint32_t* raw) {
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const int r = (i * NT + tid) >> 3;
+      const int rr = r < t.rows ? r : t.rows - 1;
+      raw[i] = GATHER ? (uint32_t)p.row_src[t.row0 + rr] : (uint32_t)rr;
+    }
+  };
+  auto finish_tile = [&](const uint32_t* raw) {
+    const char* a_base = GATHER ? reinterpret_cast<const char*>(p.A)
+                                : reinterpret_cast<const char*>(p.A + (long long)te.row0 * p.lda);
+    const char* b_base = reinterpret_cast<const char*>(p.B + (long long)te.phys * p.strideB);
+#pragma unroll
+    for (int i = 0; i < NH; ++i) {
+      const int q = i * NT + tid;
+      const int r = q >> 3;
+      const int lc = (q & 7) ^ swz8(r);
+      const long long arow = GATHER ? (long long)(raw[i] / (uint32_t)p.slots_k) : (long long)raw[i];
+      a_voff[i] = (uint32_t)((arow * p.lda + lc * 8) * 2);
+      b_voff[i] = (uint32_t)(((long long)weight_row<BN, GU_ROWS>(p, te.nt, r) * p.ldb + lc * 8) * 2);
+    }
+    a_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a_base), 0, -1, kBufferFlags);
+    b_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(b_base), 0, -1, kBufferFlags);
+  };
+  const int nk = p.K / 64;
+  // half h of the current tile: A of k-step h/2 (h even) or B (h odd), in
+  // slot h % 5.  Past the end the last k-step is loaded again (never read),
+  // so every iteration issues the same number of loads and one constant
+  // vmcnt serves every wait.
+  auto issue_half = [&](int h) {
+    const int ks = min(h >> 1, nk - 1);
+    char* dst = smem + (h % NSLOT) * HALF;
+    if (h & 1) dma_chunks<NH, NT>(dst, b_rsrc, b_voff, ks * 128, wave_s);
+    else dma_chunks<NH, NT>(dst, a_rsrc, a_voff, ks * 128, wave_s);
+  };
+
+  int a_off[TM], b_off[TN];
+  const int lc0 = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int r = wm * WTM + i * 32 + (lane & 31);
+    a_off[i] = r * ROWB + ((lc0 ^ swz8(r)) << 4);
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int r = wn * WTN + j * 32 + (lane & 31);
+    b_off[j] = r * ROWB + ((lc0 ^ swz8(r)) << 4);
+  }
+  f32x16_t acc[TM][TN];
+
+  // The k-loop of one tile, its halves 0 .. 4 already issued, for a wave
+  // whose first TMV 32-row blocks hold rows of the expert.  Thread 0 takes
+  // the next tile from the counter at its start (the reply is read after the
+  // loop; the loop's in-order waits only grow stricter for an older load).
+  int next_raw = 0;
+  auto main_loop = [&](auto tmv_tag) {
+    constexpr int TMV = decltype(tmv_tag)::value;
+    constexpr int NRD = TMV > 0 ? TMV + TN : 0;
+    constexpr int NMM = TMV * TN;
+    u32x4_t fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+    auto read_frags = [&](const char* sa, const char* sb, int s, u32x4_t* fa, u32x4_t* fb) {
+      if (TMV == 0) return;
+#pragma unroll
+      for (int i = 0; i < (TMV > TN ? TMV : TN); ++i) {
+        if (i < TN) fb[i] = *reinterpret_cast<const u32x4_t*>(sb + (b_off[i] ^ (s << 5)));
+        if (i < TMV) fa[i] = *reinterpret_cast<const u32x4_t*>(sa + (a_off[i] ^ (s << 5)));
+      }
+    };
+    auto mma_step = [&](const u32x4_t* fa, const u32x4_t* fb) {
+#pragma unroll
+      for (int i = 0; i < TMV; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, fb[j]), __builtin_bit_cast(bf16x8_t, fa[i]), acc[i][j],
+              0, 0, 0);
+    };
+    auto interleave = [&]() {
+      constexpr int NP = NRD < NMM ? NRD : NMM;
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+      }
+      if (NMM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NMM - NP, 0);
+      if (NRD > NP) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NP, 0);
+    };
+    // the fragment offsets are made opaque here, so the offsets each
+    // instantiation derives from them are not hoisted out of the tile loop
+    // (five instantiations' worth would stay live across every tile)
+#pragma unroll
+    for (int i = 0; i < TM; ++i) asm volatile("" : "+v"(a_off[i]));
+#pragma unroll
+    for (int j = 0; j < TN; ++j) asm volatile("" : "+v"(b_off[j]));
+    // halves 0 and 1 (step 0) landed: all but the last three halves issued
+    wait_vmcnt<3 * NH>();
+    __builtin_amdgcn_s_barrier();
+    if (tid == 0) next_raw = atomicAdd(ctr, 1);
+    int ia = 0, ib = 1;
+    read_frags(smem, smem + HALF, 0, fa0, fb0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const char* sa = smem + ia * HALF;
+      const char* sb = smem + ib * HALF;
+      read_frags(sa, sb, 1, fa1, fb1);
+      mma_step(fa0, fb0);
+      interleave();
+      read_frags(sa, sb, 2, fa0, fb0);
+      mma_step(fa1, fb1);
+      interleave();
+      read_frags(sa, sb, 3, fa1, fb1);
+      mma_step(fa0, fb0);
+      interleave();
+      wait_vmcnt_lgkm0<NH>();
+      __builtin_amdgcn_s_barrier();
+      issue_half(2 * kt + 5);
+      issue_half(2 * kt + 6);
+      ia = ia + 2 >= NSLOT ? ia + 2 - NSLOT : ia + 2;
+      ib = ib + 2 >= NSLOT ? ib + 2 - NSLOT : ib + 2;
+      read_frags(smem + ia * HALF, smem + ib * HALF, 0, fa0, fb0);
+      mma_step(fa1, fb1);
+      interleave();
+    }
+  };
+
+  // Tiles are taken two ahead: while tile i computes, the entry and row ids of
+  // tile i+1 (known since tile i-1) are loaded and thread 0 asks the counter
+  // for tile i+2, so when tile i's k-loop ends the next tile's first copies
+  // can go out at once, before this tile's epilogue.
+  uint32_t raw[NH];
+  te = p.table[L];
+  load_rows(te, raw);
+  finish_tile(raw);
+
+#pragma unroll
+  for (int h = 0; h < NSLOT; ++h) issue_half(h);
+  while (true) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    const int tmv = min(TM, max(0, (te.rows - wm * WTM + 31) >> 5));
+    if (tmv >= TM) main_loop(std::integral_constant<int, TM>{});
+    else if (tmv == 3) main_loop(std::integral_constant<int, 3>{});
+    else if (tmv == 2) main_loop(std::integral_constant<int, 2>{});
+    else if (tmv == 1) main_loop(std::integral_constant<int, 1>{});
+    else main_loop(std::integral_constant<int, 0>{});
+    // every copy into the ring has landed and every fragment read is done:
+    // publish the tile after next, start the next tile's first three halves,
+    // then stage and write this one
+    wait_vmcnt<0>();
+    wait_lgkm0();
+    const TileEntry cur = te;
+    const int next = t_lo + bcast(next_raw);
+    const bool more = next < t_hi;
+    if (more) {
+      te = p.table[next];
+      load_rows(te, raw);
+    }
+    fwd_epilogue_split<BM, BN, NWM, NWN, EPI>(p, cur, cur.nt, acc, smem + NPRE * HALF, [&]() {
+      if (!more) return;
+      finish_tile(raw);
+#pragma unroll
+      for (int h = 0; h < NPRE; ++h) issue_half(h);
+    });
+    if (!more) break;
+#pragma unroll
+    for (int h = NPRE; h < NSLOT; ++h) issue_half(h);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 // ---------------------------------------------------------------------------
+// The products run persistent (one workgroup per CU, a multiple of 8 so
+// every XCD gets the same number, each walking its XCD's tile range through
+// p.tile_ctr), except the gate/up product that also writes act_save for the
+// backward: its wider epilogue does not fit beside the next tile's first
+// copies without spilling, so it keeps one workgroup per tile (ring kernel).
 template <int EPI, bool GU, bool GATHER = false>
-hipError_t launch_fwd(const GemmParams& p, int grid, hipStream_t s) {
-  if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU, GATHER>), dim3(round8(grid)), dim3(512), 0,
-                     s, p);
+hipError_t launch_fwd(const GemmParams& p, int max_tiles, hipStream_t s) {
+  if (max_tiles <= 0) return hipSuccess;
+  if constexpr (EPI == EPI_GU) {
+    if (p.out2) {
+      hipLaunchKernelGGL((gemm_nt_ring_kernel<2, 4, EPI, GU, GATHER>), dim3(round8(max_tiles)),
+                         dim3(512), 0, s, p);
+      return hipGetLastError();
+    }
+  }
+  int dev = 0, cus = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (err != hipSuccess) return err;
+  const int grid = max(8, cus / 8 * 8);
+  hipLaunchKernelGGL((gemm_nt_persist_kernel<2, 4, EPI, GU, GATHER>), dim3(grid), dim3(512), 0, s,
+                     p);
   return hipGetLastError();
 }
 
@@ -451,6 +865,7 @@ hipError_t launch_ffn_fwd_products(const void* x_perm, const void* w_gu, const v
   GemmParams g = {};
   g.table = tgu.table;
   g.n_entries = tgu.n_entries;
+  g.tile_ctr = tgu.n_entries + kTileCtrOffset;
   g.f = f;
   // gate/up + SwiGLU: B rows interleaved gate/up per 32, BN/2 f-columns per tile
   g.A = static_cast<const bf16_t*>(x_perm);
@@ -473,6 +888,7 @@ hipError_t launch_ffn_fwd_products(const void* x_perm, const void* w_gu, const v
   // down projection
   g.table = td.table;
   g.n_entries = td.n_entries;
+  g.tile_ctr = td.n_entries + kTileCtrOffset;
   g.A = H;
   g.lda = f;
   g.B = static_cast<const bf16_t*>(w_d);

@@ -46,6 +46,8 @@ struct GemmParams {
   // tile grid cut into xcd_gm x xcd_gn blocks (xcd_gm * xcd_gn = 8; 0 = tiles
   // dealt round robin)
   int xcd_gm;
+  // persistent forward products: eight per-XCD tile counters, zero at launch
+  int* tile_ctr;
 };
 
 // Row tiles per rasterisation group of the tile orders.  Forward: all row

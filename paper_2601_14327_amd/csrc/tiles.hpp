@@ -20,6 +20,10 @@ struct TileEntry {
 // Tile tables
 // ---------------------------------------------------------------------------
 constexpr int kTableThreads = 256;
+// ints into a table's 256-byte header (n_entries at 0): eight per-XCD tile
+// counters of the persistent forward products
+constexpr int kTileCtrOffset = 16;
+
 
 __device__ __forceinline__ int block_excl_scan_256(int v, int* s_tmp) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -154,6 +158,9 @@ __global__ __launch_bounds__(kTableThreads) void build_tile_lists_kernel(
     __syncthreads();
     const int total = s_start[kTableThreads];
     if (blockIdx.x == 0 && e == 0) *L.n_entries = min(total, L.max_entries);
+    // the persistent products' per-XCD tile counters (kTileCtrOffset ints into
+    // the table header), zeroed for the launch that follows on the stream
+    if (blockIdx.x == 0 && e < 8) L.n_entries[kTileCtrOffset + e] = 0;
     const int i = blockIdx.x * kTableThreads + e;
     if (i < total && i < L.max_entries) {
       int lo = 0, hi = kTableThreads - 1;  // last expert with start <= i
