@@ -18,7 +18,9 @@
  *  - Pointers marked "device" are HIP device (HBM) addresses; "host" ones are
  *    ordinary CPU memory.  The caller owns and allocates every buffer; the
  *    library allocates no device memory.  Scratch memory comes in through
- *    `ws` / `ws_bytes`, sized by moe_workspace_bytes().
+ *    `ws` / `ws_bytes`, sized by moe_workspace_bytes(); its contents need no
+ *    initialisation, and calls that may run concurrently (on different
+ *    streams) need workspaces of their own.
  *  - `stream` is a hipStream_t passed as void*; NULL is the null stream.
  *    Every device call only enqueues work on `stream`: no host/device copy,
  *    no synchronisation.  Inputs must stay valid until that work completes.
@@ -334,7 +336,8 @@ int moe_permute(const void* x, int dtype, const int32_t* dest_row, int T,
  *   is a plain fp32 FMA loop (no matrix cores), meant for small parity
  *   layers, not for speed; its backward is not implemented.
  *   Workspace: moe_workspace_bytes(LAEP_CALL_FFN_FWD, R, 1, E, d_model, d_ff)
- *   (holds H and the tile table; on return H [R, d_ff] (dtype) is at byte
+ *   (holds H, the tile tables and the products' tile counters, which the
+ *   call's first kernel resets; on return H [R, d_ff] (dtype) is at byte
  *   offset 0, which moe_grouped_ffn_bwd can take as h_fwd).
  */
 int moe_grouped_ffn_fwd(const void* x_perm, const void* w_gate_up,
