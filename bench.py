@@ -50,7 +50,9 @@ timed steps, pruned experts removed; the steps run the compact layer, and
 `pruning` reports the parameter reduction and the one-time repack).
 
 Profiling helpers (used by the commands recorded under profiles/):
-  --profile-target ffn|copy   run only that call a few times (for --pmc runs)
+  --profile-target ffn|copy   run only that call a few times (for --pmc runs);
+                              route_feed: moe_route_count beside a blocked read of
+                              the same x bytes in the router's launch shape
   --summarize-pmc DIR         turn FETCH_SIZE / WRITE_SIZE counter CSVs into the
                               traffic summary (--out FILE)
   --summarize-trace DIR       turn a --kernel-trace --stats run into a summary
@@ -511,6 +513,22 @@ def profile_target(args):
     # marker dispatch: the counters of every dispatch after it belong to the target
     marker = torch.empty(512, dtype=torch.float32, device=dev)
     laep.laep_calib_mfma(1, 1, marker)
+    if args.profile_target == "route_feed":
+        # the router's feed bound: moe_route_count beside a blocked read of the
+        # same x bytes in the router's launch shape (32 token rows per
+        # 512-thread workgroup), both over the rotating x sets, after a settle
+        w = su.w
+        block = 32 * w.d_model * 2
+        out = torch.empty(w.T // 32 * 512, dtype=torch.float32, device=dev)
+        _settle(su)
+        n = su.n_sets
+        for i in range(200):
+            dict(su.calls(i))["route_count"]()
+            laep.laep_calib_read(su.xs[(i + n // 2) % n], block, out)
+        torch.cuda.synchronize()
+        print(f"profile target: route_count and laep_calib_read ({block} B blocks) x 200 on "
+              f"{args.workload}", flush=True)
+        return
     for _ in range(PROFILE_CALLS):
         calls[args.profile_target]()
     torch.cuda.synchronize()
@@ -665,10 +683,57 @@ def summarize_trace(args):
         lines.append(f"| `{name[:110]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['Percentage']):.2f}% |")
+    lines += _feed_loop_lines(args)
     text = "\n".join(lines) + "\n"
     with open(args.out, "w") as fh:
         fh.write(text)
     print(text)
+
+
+def _feed_loop_lines(args):
+    """For a route_feed trace: each blocked read beside the router launch and
+    the counting launch issued just before it, and the read's rate on x."""
+    import csv
+    import statistics
+    f = glob.glob(os.path.join(args.summarize_trace, "**", "*kernel_trace.csv"), recursive=True)
+    if not f:
+        return []
+    rows = sorted(csv.DictReader(open(f[0])), key=lambda r: int(r["Start_Timestamp"]))
+    reads = [i for i, r in enumerate(rows) if "read_kernel" in r["Kernel_Name"]]
+    if not reads:
+        return []
+    from workloads import WORKLOADS
+    w = WORKLOADS[args.workload]
+    x_bytes = w.T * w.d_model * 2
+
+    def dur(r):
+        return (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    def before(i, key):
+        for j in range(i - 1, max(-1, i - 4), -1):
+            if key in rows[j]["Kernel_Name"]:
+                return dur(rows[j])
+        raise ValueError(f"no {key} dispatch before read dispatch {i}")
+
+    series = [("`read_kernel` (x bytes only)", [dur(rows[i]) for i in reads]),
+              ("`route_kernel`", [before(i, "route_kernel") for i in reads]),
+              ("`count_scan_scatter_kernel`", [before(i, "count_scan_scatter") for i in reads])]
+    g = rows[reads[0]]
+    rd = statistics.mean(series[0][1])
+    ro = statistics.mean(series[1][1])
+    out = ["", "## Feed loop",
+           f"Each of the {len(reads)} iterations: `moe_route_count` on one x set, then "
+           f"`laep_calib_read` on another ({int(g['Grid_Size_X']) // int(g['Workgroup_Size_X'])} "
+           f"workgroups of {g['Workgroup_Size_X']} threads, 32 token rows each: the router's "
+           f"launch shape), x {x_bytes / 1e6:.1f} MB.\n",
+           "| dispatch | calls | average (us) | median (us) | min (us) | max (us) |",
+           "|---|---:|---:|---:|---:|---:|"]
+    for name, v in series:
+        out.append(f"| {name} | {len(v)} | {statistics.mean(v):.2f} | {statistics.median(v):.2f} "
+                   f"| {min(v):.2f} | {max(v):.2f} |")
+    out += ["", f"Read rate on x: {x_bytes / rd / 1e3:.0f} GB/s. The router takes "
+                f"{ro / rd:.2f}x the read ({ro - rd:.2f} us above its feed bound)."]
+    return out
 
 
 # ---------------------------------------------------------------------------------------
@@ -682,7 +747,7 @@ def main():
     ap.add_argument("--no-attainable", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--profile-target", choices=["ffn_fwd", "ffn_bwd", "copy", "route_count",
-                                                 "permute", "combine", "counts"])
+                                                 "permute", "combine", "counts", "route_feed"])
     ap.add_argument("--summarize-pmc")
     ap.add_argument("--summarize-trace")
     ap.add_argument("--summarize-counters")

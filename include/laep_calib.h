@@ -1,9 +1,9 @@
 /*
  * laep_calib.h -- measurement kernels of the LAEP MoE library (gfx950).
  *
- * Not part of the MoE layer: these two calls measure what the chip attains
- * on the two resources the layer's kernels are bound by, so that achieved
- * rates can be read against attained as well as published peaks.
+ * Not part of the MoE layer: these calls measure what the chip attains on the
+ * resources the layer's kernels are bound by, so that achieved rates can be
+ * read against attained as well as published peaks.
  * Conventions (device pointers, void* streams, return codes, no allocation,
  * asynchronous enqueue, laep_last_error) are those of laep_moe.h.
  */
@@ -27,6 +27,21 @@ extern "C" {
  *         LAEP_ERR_HIP.
  */
 int laep_calib_copy(const void* src, void* dst, size_t bytes, void* stream);
+
+/*
+ * laep_calib_read -- bytes / block_bytes workgroups of 512 threads; each reads
+ * its contiguous block of block_bytes (thread t its 16-byte chunks t, t + 512,
+ * ..., all in flight at once) and writes the XOR of what it read to
+ * out[workgroup * 512 + t].  With block_bytes = 32 rows of a router input,
+ * one workgroup per CU streams the router's x exactly as the router's launch
+ * does, without its other work: the router's feed bound.
+ *   src : device, 16-byte aligned, bytes readable
+ *   out : device float[(bytes / block_bytes) * 512]
+ * Errors: LAEP_ERR_INVALID_ARG (null or misaligned pointer; block_bytes not a
+ *         multiple of 8192 in [8192, 131072], or not dividing bytes),
+ *         LAEP_ERR_HIP.
+ */
+int laep_calib_read(const void* src, size_t bytes, int block_bytes, float* out, void* stream);
 
 /*
  * laep_calib_mfma -- n_workgroups workgroups of 8 waves; every wave issues

@@ -18,7 +18,8 @@ Expert Pruning acts on), each a call into hand-written gfx950 HIP kernels:
     moe_combine_bwd, moe_grouped_ffn_bwd, moe_permute_bwd   backward
     moe_route_bwd        router / gate backward (softmax Jacobian, dW_r, dx)
     laep_rearrange       host utility: balanced expert placement
-    laep_calib_copy, laep_calib_mfma   measurement kernels (attained peaks)
+    laep_calib_copy, laep_calib_read,  measurement kernels (attained peaks,
+    laep_calib_mfma                    the router's feed bound)
 """
 from ._lib import (  # noqa: F401
     LAEP_BF16, LAEP_CALL_FFN_BWD, LAEP_CALL_FFN_FWD, LAEP_F32, LaepError, LIB_PATH, lib)
@@ -27,6 +28,7 @@ from .api import (  # noqa: F401
     ffn_fwd_h_view,
     laep_calib_copy,
     laep_calib_mfma,
+    laep_calib_read,
     laep_compact_experts,
     laep_expert_pruning,
     laep_prune_mask,

@@ -79,6 +79,7 @@ SIGNATURES = {
     # measurement kernels (laep_calib.h)
     "laep_calib_copy": (_i, [_p, _p, _sz, _p]),
     "laep_calib_mfma": (_i, [_i, _i, _p, _p]),
+    "laep_calib_read": (_i, [_p, _sz, _i, _p, _p]),
 }
 
 _lock = threading.Lock()

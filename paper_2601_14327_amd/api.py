@@ -534,6 +534,19 @@ def laep_calib_copy(src: torch.Tensor, dst: torch.Tensor):
     check(lib().laep_calib_copy(_ptr(src), _ptr(dst), nbytes, _stream(src.device)))
 
 
+def laep_calib_read(src: torch.Tensor, block_bytes: int, out: torch.Tensor):
+    """Blocked streaming read of src (laep_calib_read): one 512-thread
+    workgroup per block_bytes, out float32 [n_blocks * 512]."""
+    _dev(src, "src")
+    _dev(out, "out")
+    nbytes = src.numel() * src.element_size()
+    if block_bytes <= 0 or out.dtype != torch.float32 or \
+            out.numel() < (nbytes // block_bytes) * 512:
+        raise ValueError("out must be float32 with (src bytes / block_bytes) * 512 elements")
+    check(lib().laep_calib_read(_ptr(src), nbytes, int(block_bytes), _ptr(out),
+                                _stream(src.device)))
+
+
 def laep_calib_mfma(n_workgroups: int, iters: int, out: torch.Tensor):
     """bf16 MFMA loop: n_workgroups x 8 waves x iters x 8 MFMA 32x32x16."""
     _dev(out, "out")

@@ -608,6 +608,18 @@ int laep_calib_copy(const void* src, void* dst, size_t bytes, void* stream) {
   return hip_status(laep::launch_calib_copy(src, dst, bytes, as_stream(stream)), "laep_calib_copy");
 }
 
+int laep_calib_read(const void* src, size_t bytes, int block_bytes, float* out, void* stream) {
+  REQUIRE(src && out && aligned16(src), LAEP_ERR_INVALID_ARG,
+          "laep_calib_read: null or misaligned pointer");
+  REQUIRE(block_bytes >= 8192 && block_bytes <= 131072 && block_bytes % 8192 == 0 &&
+              bytes % (size_t)block_bytes == 0 && bytes / (size_t)block_bytes <= 0x7FFFFFFFu,
+          LAEP_ERR_INVALID_ARG,
+          "laep_calib_read: block_bytes must be a multiple of 8192 in [8192, 131072] that divides "
+          "bytes");
+  return hip_status(laep::launch_calib_read(src, bytes, block_bytes, out, as_stream(stream)),
+                    "laep_calib_read");
+}
+
 int laep_calib_mfma(int n_workgroups, int iters, float* out, void* stream) {
   REQUIRE(out && n_workgroups >= 1 && iters >= 1, LAEP_ERR_INVALID_ARG,
           "laep_calib_mfma: null out, n_workgroups < 1 or iters < 1");

@@ -1,4 +1,5 @@
-// Measurement kernels (laep_calib.h): a streaming copy and a bf16 MFMA loop.
+// Measurement kernels (laep_calib.h): a streaming copy, a blocked read and a
+// bf16 MFMA loop.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -27,6 +28,25 @@ __global__ __launch_bounds__(256) void copy_kernel(const u32x4_t* __restrict__ s
       if (i < n) st_stream(dst + i, v[j]);
     }
   }
+}
+
+// Each workgroup reads its contiguous block: thread t its 16-byte chunks
+// t, t + 512, ... (every load coalesced), all of them in flight at once, then
+// writes the XOR of what it read (so the loads are not removed).
+constexpr int kReadThreads = 512;
+constexpr int kReadMaxChunks = 16;  // chunks per thread: blocks of up to 128 KB
+__global__ __launch_bounds__(kReadThreads) void read_kernel(const u32x4_t* __restrict__ src,
+                                                            int chunks, float* __restrict__ out) {
+  const u32x4_t* p = src + (size_t)blockIdx.x * chunks * kReadThreads + threadIdx.x;
+  u32x4_t v[kReadMaxChunks];
+#pragma unroll
+  for (int u = 0; u < kReadMaxChunks; ++u)
+    if (u < chunks) v[u] = p[(size_t)u * kReadThreads];
+  uint32_t x = 0;
+#pragma unroll
+  for (int u = 0; u < kReadMaxChunks; ++u)
+    if (u < chunks) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+  out[(size_t)blockIdx.x * kReadThreads + threadIdx.x] = __uint_as_float(x);
 }
 
 __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __restrict__ out) {
@@ -63,6 +83,15 @@ hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream
   const size_t blocks = (n + per_block - 1) / per_block;
   hipLaunchKernelGGL(copy_kernel, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0,
                      s, static_cast<const u32x4_t*>(src), static_cast<u32x4_t*>(dst), n);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_read(const void* src, size_t bytes, int block_bytes, float* out,
+                             hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  const int chunks = block_bytes / (16 * kReadThreads);
+  hipLaunchKernelGGL(read_kernel, dim3((unsigned)(bytes / block_bytes)), dim3(kReadThreads), 0, s,
+                     static_cast<const u32x4_t*>(src), chunks, out);
   return hipGetLastError();
 }
 

@@ -124,5 +124,7 @@ hipError_t launch_route_bwd(const float* dgate, const int32_t* idx, const float*
 // Measurement kernels (laep_calib.h).
 hipError_t launch_calib_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_calib_mfma(int n_workgroups, int iters, float* out, hipStream_t s);
+hipError_t launch_calib_read(const void* src, size_t bytes, int block_bytes, float* out,
+                             hipStream_t s);
 
 }  // namespace laep

@@ -201,6 +201,15 @@ def test_calib_validation(L):
     assert L.laep_calib_mfma(0, 10, p, None) == 1
     assert L.laep_calib_mfma(8, 0, p, None) == 1
     assert L.laep_calib_mfma(8, 10, None, None) == 1
+    # blocked read: block sizes outside [8 KiB, 128 KiB], not a multiple of
+    # 8 KiB or not dividing the byte count; null or misaligned pointers
+    assert L.laep_calib_read(p, 1 << 20, 4096, p, None) == 1
+    assert L.laep_calib_read(p, 1 << 20, 262144, p, None) == 1
+    assert L.laep_calib_read(p, 1 << 20, 12288, p, None) == 1
+    assert L.laep_calib_read(p, 100000, 8192, p, None) == 1
+    assert L.laep_calib_read(None, 1 << 20, 8192, p, None) == 1
+    assert L.laep_calib_read(p, 1 << 20, 8192, None, None) == 1
+    assert L.laep_calib_read(p + 2, 1 << 20, 8192, p, None) == 1
 
 
 def test_rowop_validation(L):

@@ -832,3 +832,26 @@ def test_zero_rows_everywhere():
     assert w_none is None
     torch.cuda.synchronize()
     assert bool((dw == 7.0).all())
+
+
+def test_calib_kernels():
+    """The measurement kernels do the work they are timed on: the copy copies,
+    the blocked read XORs each thread's 16-byte chunks, the MFMA loop writes
+    one value per lane."""
+    rng = np.random.default_rng(5)
+    case("calibration kernels")
+    src = torch.from_numpy(rng.integers(0, 2**31, size=3 * 65536 // 4, dtype=np.int64)
+                           .astype(np.uint32).view(np.int32)).cuda()
+    dst = torch.empty_like(src)
+    laep.laep_calib_copy(src, dst)
+    block = 65536                      # 8 chunks of 16 bytes per thread
+    out = torch.empty(src.numel() * 4 // block * 512, dtype=torch.float32, device="cuda")
+    laep.laep_calib_read(src, block, out)
+    mout = torch.empty(8 * 512, dtype=torch.float32, device="cuda")
+    laep.laep_calib_mfma(8, 4, mout)
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
+    words = src.cpu().numpy().view(np.uint32).reshape(-1, block // 16 // 512, 512, 4)  # [wg, u, t, 4]
+    want = np.bitwise_xor.reduce(np.bitwise_xor.reduce(words, axis=3), axis=1).reshape(-1)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), want)
+    assert torch.isfinite(mout).all()
