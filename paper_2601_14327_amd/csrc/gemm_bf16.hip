@@ -749,10 +749,13 @@ __global__ __launch_bounds__(64 * NWM * NWN) void gemm_nt_persist_kernel(GemmPar
     }
   };
 
-  // Tiles are taken two ahead: while tile i computes, the entry and row ids of
-  // tile i+1 (known since tile i-1) are loaded and thread 0 asks the counter
-  // for tile i+2, so when tile i's k-loop ends the next tile's first copies
-  // can go out at once, before this tile's epilogue.
+  // One tile ahead: thread 0 asks the counter for the next tile at the start
+  // of each k-loop; after the loop its index reaches every thread, its entry
+  // and row ids load while this tile's accumulators are staged, and its first
+  // three halves go out once the last staging is published (no accumulator
+  // live).  Loading the entry and rows during the k-loop instead (vector loads
+  // at the first two step boundaries) measured no faster: the chain already
+  // overlaps the staging.
   uint32_t raw[NH];
   te = p.table[L];
   load_rows(te, raw);

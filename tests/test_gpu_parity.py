@@ -309,6 +309,10 @@ def _ffn_inputs(seed, counts, d, f, dtype, E_phys=None):
     ("bf16", [300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),       # ragged, f % 128 = 64
     ("bf16", [0, 0, 0, 513], 320, 128),                           # one expert takes all
     ("bf16", [64] * 16, 512, 512),
+    # 512 tiles per product: several per persistent workgroup, with a
+    # one-step k-loop in the gate/up (K = d = 64) or the down product (K = f = 64)
+    ("bf16", [1024] * 31 + [1000], 64, 512),
+    ("bf16", [1000] + [1024] * 31, 1024, 64),
 ])
 def test_ffn_fwd_parity(dtype, counts, d, f):
     x, wgu, wd, offsets = _ffn_inputs(len(counts) * 31 + d, counts, d, f, dtype)
