@@ -53,9 +53,13 @@ Profiling helpers (used by the commands recorded under profiles/):
   --profile-target ffn|copy   run only that call a few times (for --pmc runs);
                               route_feed: moe_route_count beside a blocked read of
                               the same x bytes in the router's launch shape
+  --library-ref               the grouped FFN on 64 equal experts of 1024 rows
+                              beside torch.matmul (hipBLASLt) on the same two
+                              products as dense matrices (context, not the metric)
   --summarize-pmc DIR         turn FETCH_SIZE / WRITE_SIZE counter CSVs into the
                               traffic summary (--out FILE)
   --summarize-trace DIR       turn a --kernel-trace --stats run into a summary
+                              (--append-log FILE adds the run's JSON result line)
   --summarize-counters DIR    turn --pmc runs of SQ / GRBM counters on one call
                               into a per-kernel summary (MFMA busy, LDS, waits,
                               clock)
@@ -422,6 +426,66 @@ def _attainable(dev):
             "mfma_frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 3)}
 
 
+def library_ref(args):
+    """The grouped FFN on 64 equal experts of 1024 rows (no ragged tiles, the
+    `balanced` layer's d and f), beside the platform BLAS (hipBLASLt, through
+    torch.matmul) on the same two products as dense matrices of the same
+    flops: [R, d] x [d, 2f] and [R, f] x [f, d].  Context for the GEMM core,
+    not the metric: the library's products gather rows and fuse SwiGLU, the
+    dense ones do neither."""
+    import torch
+
+    import paper_2601_14327_amd as laep
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    E, rows, d, f = 64, 1024, 2048, 1024
+    R = E * rows
+    g = torch.Generator(device=dev).manual_seed(7)
+    bf = torch.bfloat16
+    x = torch.randn(R, d, device=dev, generator=g).to(bf)
+    wgu = (torch.randn(E, 2 * f, d, device=dev, generator=g) * d ** -0.5).to(bf)
+    wd = (torch.randn(E, d, f, device=dev, generator=g) * f ** -0.5).to(bf)
+    offsets = torch.arange(0, R + 1, rows, dtype=torch.int32, device=dev)
+    y = torch.empty(R, d, dtype=bf, device=dev)
+    # dense operands, [K, N] contiguous (no transposed views)
+    b1 = wgu[0].t().contiguous()
+    h = torch.randn(R, f, device=dev, generator=g).to(bf)
+    b2 = wd[0].t().contiguous()
+    c1 = torch.empty(R, 2 * f, dtype=bf, device=dev)
+    c2 = torch.empty(R, d, dtype=bf, device=dev)
+    calls = {
+        "laep_grouped_ffn_fwd": lambda: laep.moe_grouped_ffn_fwd(x, wgu, wd, offsets,
+                                                                 save_act=False, y_perm=y),
+        "torch_matmul_gate_up": lambda: torch.matmul(x, b1, out=c1),
+        "torch_matmul_down": lambda: torch.matmul(h, b2, out=c2),
+    }
+    flops = {"laep_grouped_ffn_fwd": 6.0 * R * d * f, "torch_matmul_gate_up": 4.0 * R * d * f,
+             "torch_matmul_down": 2.0 * R * d * f}
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 3.0:   # clocks up
+        for fn in calls.values():
+            fn()
+        torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {}
+    for name, fn in calls.items():
+        ts = []
+        for _ in range(args.steps):
+            s.record()
+            fn()
+            e.record()
+            torch.cuda.synchronize()
+            ts.append(s.elapsed_time(e) * 1e3)
+        med = sorted(ts)[len(ts) // 2]
+        out[name] = {"median_us": round(med, 1),
+                     "TFLOPs": round(flops[name] / (med * 1e-6) / 1e12, 1)}
+    dense_us = out["torch_matmul_gate_up"]["median_us"] + out["torch_matmul_down"]["median_us"]
+    out["torch_matmul_both"] = {"median_us": round(dense_us, 1),
+                                "TFLOPs": round(6.0 * R * d * f / (dense_us * 1e-6) / 1e12, 1)}
+    print(json.dumps({"library_ref": out, "shape": {"experts": E, "rows_per_expert": rows,
+                                                    "d_model": d, "d_ff": f}}), flush=True)
+
+
 def _supplementary(w, su, dev, reps=20):
     """Latency-bound calls at other sizes: moe_expert_counts over T x {1, 8, 64}
     (random distinct expert ids, the workload's E and k), and route followed
@@ -684,6 +748,10 @@ def summarize_trace(args):
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['Percentage']):.2f}% |")
     lines += _feed_loop_lines(args)
+    if args.append_log:   # the run's own result line
+        last = [ln for ln in open(args.append_log).read().splitlines() if ln.startswith("{")][-1]
+        lines += ["", "## Result line of the same command (HIP events, medians)", "",
+                  "```json", json.dumps(json.loads(last), indent=1), "```"]
     text = "\n".join(lines) + "\n"
     with open(args.out, "w") as fh:
         fh.write(text)
@@ -748,11 +816,13 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--profile-target", choices=["ffn_fwd", "ffn_bwd", "copy", "route_count",
                                                  "permute", "combine", "counts", "route_feed"])
+    ap.add_argument("--library-ref", action="store_true")
     ap.add_argument("--summarize-pmc")
     ap.add_argument("--summarize-trace")
     ap.add_argument("--summarize-counters")
     ap.add_argument("--profile-call", default="ffn_fwd")
     ap.add_argument("--command-note")
+    ap.add_argument("--append-log")
     ap.add_argument("--out")
     args = ap.parse_args()
     if args.summarize_pmc:
@@ -767,6 +837,8 @@ def main():
         sys.exit(2)
     if args.profile_target:
         return profile_target(args)
+    if args.library_ref:
+        return library_ref(args)
 
     import torch
 
