@@ -313,6 +313,7 @@ def _ffn_inputs(seed, counts, d, f, dtype, E_phys=None):
     # one-step k-loop in the gate/up (K = d = 64) or the down product (K = f = 64)
     ("bf16", [1024] * 31 + [1000], 64, 512),
     ("bf16", [1000] + [1024] * 31, 1024, 64),
+    ("bf16", [300, 0, 513, 64], 2048, 1024),                      # the balanced layer's width
 ])
 def test_ffn_fwd_parity(dtype, counts, d, f):
     x, wgu, wd, offsets = _ffn_inputs(len(counts) * 31 + d, counts, d, f, dtype)
@@ -546,6 +547,7 @@ def test_ffn_fwd_gather_combine_matches_three_calls(T, E, d, f, mapped, keep_y):
 @pytest.mark.parametrize("counts,d,f", [
     ([60, 0, 200, 5, 1, 130, 64, 52], 128, 256),
     ([300, 129, 128, 0, 7, 1000, 1, 40], 256, 192),
+    ([300, 0, 513, 64], 2048, 1024),                              # the balanced layer's width
 ])
 def test_ffn_bwd_parity(counts, d, f, use_h):
     x, wgu, wd, offsets = _ffn_inputs(len(counts) + d, counts, d, f, "bf16")
