@@ -53,9 +53,10 @@ Profiling helpers (used by the commands recorded under profiles/):
   --profile-target ffn|copy   run only that call a few times (for --pmc runs);
                               route_feed: moe_route_count beside a blocked read of
                               the same x bytes in the router's launch shape
-  --library-ref               the grouped FFN on 64 equal experts of 1024 rows
-                              beside torch.matmul (hipBLASLt) on the same two
-                              products as dense matrices (context, not the metric)
+  --library-ref               the grouped FFN and its backward on 64 equal experts
+                              of 1024 rows beside torch.matmul / torch.bmm
+                              (hipBLASLt) on the same products (context, not the
+                              metric)
   --summarize-pmc DIR         turn FETCH_SIZE / WRITE_SIZE counter CSVs into the
                               traffic summary (--out FILE)
   --summarize-trace DIR       turn a --kernel-trace --stats run into a summary
@@ -430,9 +431,11 @@ def library_ref(args):
     """The grouped FFN on 64 equal experts of 1024 rows (no ragged tiles, the
     `balanced` layer's d and f), beside the platform BLAS (hipBLASLt, through
     torch.matmul) on the same two products as dense matrices of the same
-    flops: [R, d] x [d, 2f] and [R, f] x [f, d].  Context for the GEMM core,
-    not the metric: the library's products gather rows and fuse SwiGLU, the
-    dense ones do neither."""
+    flops: [R, d] x [d, 2f] and [R, f] x [f, d]; and the grouped backward
+    beside its four products as bf16 batched GEMMs over the experts
+    (torch.bmm; the library writes the weight gradients in fp32, the batched
+    GEMMs in bf16).  Context for the GEMM core, not the metric: the library's
+    products fuse SwiGLU and its backward, the vendor's do neither."""
     import torch
 
     import paper_2601_14327_amd as laep
@@ -453,14 +456,41 @@ def library_ref(args):
     b2 = wd[0].t().contiguous()
     c1 = torch.empty(R, 2 * f, dtype=bf, device=dev)
     c2 = torch.empty(R, d, dtype=bf, device=dev)
+    # backward: the library's call (dY given, H_b from act_save) beside the four
+    # products as bf16 batched GEMMs over the experts (torch.bmm, every operand
+    # contiguous: the transposed ones are copies, never views)
+    _, act = laep.moe_grouped_ffn_fwd(x, wgu, wd, offsets, save_act=True)
+    dy = torch.randn(R, d, device=dev, generator=g).to(bf)
+    dx = torch.empty_like(x)
+    dwgu = torch.empty(wgu.shape, dtype=torch.float32, device=dev)
+    dwd = torch.empty(wd.shape, dtype=torch.float32, device=dev)
+    ws_b = torch.empty(laep.workspace_bytes(laep.LAEP_CALL_FFN_BWD, R, 1, E, d, f),
+                       dtype=torch.uint8, device=dev)
+    dy3 = dy.view(E, rows, d)
+    da3 = torch.randn(E, rows, 2 * f, device=dev, generator=g).to(bf)
+    x3, h3 = x.view(E, rows, d), h.view(E, rows, f)
+    dy3t = dy3.transpose(1, 2).contiguous()
+    da3t = da3.transpose(1, 2).contiguous()
+    o_dh = torch.empty(E, rows, f, dtype=bf, device=dev)
+    o_dx = torch.empty(E, rows, d, dtype=bf, device=dev)
+    o_dwd = torch.empty(E, d, f, dtype=bf, device=dev)
+    o_dwgu = torch.empty(E, 2 * f, d, dtype=bf, device=dev)
     calls = {
         "laep_grouped_ffn_fwd": lambda: laep.moe_grouped_ffn_fwd(x, wgu, wd, offsets,
                                                                  save_act=False, y_perm=y),
         "torch_matmul_gate_up": lambda: torch.matmul(x, b1, out=c1),
         "torch_matmul_down": lambda: torch.matmul(h, b2, out=c2),
+        "laep_grouped_ffn_bwd": lambda: laep.moe_grouped_ffn_bwd(
+            dy, x, act, wgu, wd, offsets, dw_gate_up=dwgu, dw_down=dwd, ws=ws_b, dx_perm=dx),
+        "torch_bmm_dgrad_dH": lambda: torch.bmm(dy3, wd, out=o_dh),
+        "torch_bmm_dgrad_dX": lambda: torch.bmm(da3, wgu, out=o_dx),
+        "torch_bmm_wgrad_dWd": lambda: torch.bmm(dy3t, h3, out=o_dwd),
+        "torch_bmm_wgrad_dWgu": lambda: torch.bmm(da3t, x3, out=o_dwgu),
     }
     flops = {"laep_grouped_ffn_fwd": 6.0 * R * d * f, "torch_matmul_gate_up": 4.0 * R * d * f,
-             "torch_matmul_down": 2.0 * R * d * f}
+             "torch_matmul_down": 2.0 * R * d * f, "laep_grouped_ffn_bwd": 12.0 * R * d * f,
+             "torch_bmm_dgrad_dH": 2.0 * R * d * f, "torch_bmm_dgrad_dX": 4.0 * R * d * f,
+             "torch_bmm_wgrad_dWd": 2.0 * R * d * f, "torch_bmm_wgrad_dWgu": 4.0 * R * d * f}
     t0 = time.perf_counter()
     while time.perf_counter() - t0 < 3.0:   # clocks up
         for fn in calls.values():
@@ -482,6 +512,10 @@ def library_ref(args):
     dense_us = out["torch_matmul_gate_up"]["median_us"] + out["torch_matmul_down"]["median_us"]
     out["torch_matmul_both"] = {"median_us": round(dense_us, 1),
                                 "TFLOPs": round(6.0 * R * d * f / (dense_us * 1e-6) / 1e12, 1)}
+    bmm_us = sum(out[k]["median_us"] for k in ("torch_bmm_dgrad_dH", "torch_bmm_dgrad_dX",
+                                                "torch_bmm_wgrad_dWd", "torch_bmm_wgrad_dWgu"))
+    out["torch_bmm_backward_all"] = {"median_us": round(bmm_us, 1),
+                                     "TFLOPs": round(12.0 * R * d * f / (bmm_us * 1e-6) / 1e12, 1)}
     print(json.dumps({"library_ref": out, "shape": {"experts": E, "rows_per_expert": rows,
                                                     "d_model": d, "d_ff": f}}), flush=True)
 
