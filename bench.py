@@ -487,7 +487,17 @@ def library_ref(args):
         "torch_bmm_wgrad_dWd": lambda: torch.bmm(dy3t, h3, out=o_dwd),
         "torch_bmm_wgrad_dWgu": lambda: torch.bmm(da3t, x3, out=o_dwgu),
     }
-    flops = {"laep_grouped_ffn_fwd": 6.0 * R * d * f, "torch_matmul_gate_up": 4.0 * R * d * f,
+    # the weight gradients with fp32 outputs, as the library writes them (where
+    # this PyTorch build offers bf16 x bf16 -> fp32 batched products)
+    try:
+        torch.bmm(dy3t[:1], h3[:1], out_dtype=torch.float32)
+        calls["torch_bmm_wgrad_dWd_f32out"] = lambda: torch.bmm(dy3t, h3, out_dtype=torch.float32)
+        calls["torch_bmm_wgrad_dWgu_f32out"] = lambda: torch.bmm(da3t, x3, out_dtype=torch.float32)
+    except (RuntimeError, NotImplementedError, TypeError):
+        pass
+    flops = {"torch_bmm_wgrad_dWd_f32out": 2.0 * R * d * f,
+             "torch_bmm_wgrad_dWgu_f32out": 4.0 * R * d * f,
+             "laep_grouped_ffn_fwd": 6.0 * R * d * f, "torch_matmul_gate_up": 4.0 * R * d * f,
              "torch_matmul_down": 2.0 * R * d * f, "laep_grouped_ffn_bwd": 12.0 * R * d * f,
              "torch_bmm_dgrad_dH": 2.0 * R * d * f, "torch_bmm_dgrad_dX": 4.0 * R * d * f,
              "torch_bmm_wgrad_dWd": 2.0 * R * d * f, "torch_bmm_wgrad_dWgu": 4.0 * R * d * f}
