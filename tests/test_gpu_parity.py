@@ -597,7 +597,7 @@ def test_ffn_bwd_parity(counts, d, f, use_h):
     assert rownorm_err(host(dwd).reshape(E, -1), (2 * rd).reshape(E, -1)) <= TOL_F32
 
 
-@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("seed", range(24))
 def test_ffn_bwd_fuzz(seed):
     """Random ragged expert loads (empty experts, single rows, one heavy
     expert) through the backward products, teacher-forced like the parity
@@ -648,6 +648,38 @@ def test_ffn_bwd_fuzz(seed):
 # ---------------------------------------------------------------------------
 # the whole layer, end to end, tiny fp32 workload
 # ---------------------------------------------------------------------------
+def _heavy_tailed_counts(rng, E, total):
+    """Per-expert row counts with a heavy tail (Pareto 1.1 weights) and about
+    15 % empty experts, summing to about `total`."""
+    w = rng.pareto(1.1, size=E) + 0.05
+    w[rng.random(E) < 0.15] = 0.0
+    if w.sum() == 0:
+        w[0] = 1.0
+    c = [int(v) for v in np.floor(w / w.sum() * total)]
+    if sum(c) == 0:
+        c[0] = 300
+    return c
+
+
+@pytest.mark.parametrize("seed,E,total,d,f", [
+    (0, 64, 80000, 128, 64),    # about 380 row tiles: several tiles per persistent workgroup
+    (1, 40, 60000, 64, 256),
+    (2, 16, 40000, 256, 128),
+])
+def test_ffn_fwd_many_tiles(seed, E, total, d, f):
+    """Uneven expert loads over hundreds of tiles per product, so every
+    persistent workgroup takes several tiles from its XCD's queue."""
+    counts = _heavy_tailed_counts(np.random.default_rng(40 + seed), E, total)
+    test_ffn_fwd_parity("bf16", counts, d, f)
+
+
+@pytest.mark.parametrize("seed,use_h", [(0, False), (1, True)])
+def test_ffn_bwd_many_tiles(seed, use_h):
+    """The backward products over uneven expert loads of about 20k rows."""
+    counts = _heavy_tailed_counts(np.random.default_rng(60 + seed), 24, 20000)
+    test_ffn_bwd_parity(counts, 128, 128, use_h)
+
+
 def test_tiny_layer_end_to_end():
     w = WORKLOADS["tiny"]
     c = generate(w)
@@ -665,7 +697,7 @@ def test_tiny_layer_end_to_end():
     assert rownorm_err(host(out)[ok], ref["out"][ok]) <= TOL_F32
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(48))
 def test_layer_fuzz(seed):
     """Random shapes through the whole forward (route + counts, dispatch, FFN,
     combine): routing against the oracle (near-ties allowed), outputs
