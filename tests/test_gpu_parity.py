@@ -496,6 +496,41 @@ def test_ffn_bwd_concurrent_calls_on_two_streams():
                 assert torch.equal(u, g), f"{n} differs (call {i}, repetition {rep})"
 
 
+def test_ffn_fwd_concurrent_calls_on_two_streams():
+    """Two gathered forward calls on two caller streams, each with its own
+    workspace (the persistent products' tile counters live there), overlap on
+    the GPU and give the same bits as the same calls made one after the other;
+    several hundred tiles per product, so every workgroup takes several."""
+    rng = np.random.default_rng(43)
+    T, k, E, d, f = 2000, 8, 16, 512, 512
+    c = random_case(78, T=T, d_model=d, E=E, k=k, d_ff=f, dtype="bf16")
+    bf = torch.bfloat16
+    wgu, wd = dev(c["w_gate_up"], bf), dev(c["w_down"], bf)
+    xs = [dev(rng.standard_normal((T, d)).astype(np.float32), bf) for _ in range(2)]
+    ids = np.stack([rng.choice(E, size=k, replace=False) for _ in range(T)]).astype(np.int32)
+    idx = dev(ids, torch.int32)
+    case(f"ffn fwd, two concurrent calls T={T} k={k} E={E} d={d} f={f}")
+    counts, offsets, dest_row, row_src = laep.moe_expert_counts(idx, E, want_row_src=True)
+
+    def call(x):
+        return laep.moe_grouped_ffn_fwd_gather(x, row_src, k, wgu, wd, offsets)[0]
+
+    ref = [call(x) for x in xs]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    for rep in range(3):
+        outs = [None, None]
+        for i, st in enumerate(streams):
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                outs[i] = call(xs[i])
+        for st in streams:
+            torch.cuda.current_stream().wait_stream(st)
+        torch.cuda.synchronize()
+        for i in range(2):
+            assert torch.equal(ref[i], outs[i]), f"y_perm differs (call {i}, repetition {rep})"
+
+
 @pytest.mark.parametrize("T,E,d,f,mapped,keep_y", [
     (300, 8, 256, 128, False, False),   # ragged tiles, an empty expert
     (1, 3, 128, 256, False, True),      # a single token
